@@ -1,0 +1,331 @@
+#!/usr/bin/env python3
+"""Benchmark of the mask-aware K/V-cached denoising step on one MI355X.
+
+One step = mask compaction + gather + every block of the stack (LN, QKV GEMM
+with the fresh-K/V scatter, masked-query attention over all tokens,
+out-projection, LN, MLP) + final scatter, over one synthetic request set
+(and, for the streamed workloads, the per-layer cache loads from pinned host
+memory). Steps cycle through seeded mask sets whose ratios follow the
+workload's distribution.
+
+Prints ONE JSON line on stdout. Default workload: the 12-block d=768 bf16
+stack over 4096 tokens with an HBM-resident cache and ellipse-union masks of
+ratio U[5%, 60%].
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "masked-token step time (ms) & tokens/s vs mask ratio; % MFMA/HBM peak"
+PEAK = {"bf16_mfma_tflops": 2500.0, "fp32_mfma_tflops": 157.3, "hbm_gbs": 8000.0}
+
+DESCR = {
+    "c1": "single pre-LN block, fp32, d=256, 4 heads, MLP 4x GELU, 32x32 grid = 1024 tokens, "
+          "12x17 rectangle mask (19.9%)",
+    "c2": "12-block stack, bf16, d=768, 12 heads, MLP 4x, 64x64 grid = 4096 tokens, HBM-resident "
+          "per-layer K/V cache, union of 1-4 random ellipses, ratio U[5%,60%]",
+    "c3": "28-block stack, bf16, d=1152, 16 heads (head_dim 72), MLP 4x, 4096 tokens, K/V cache "
+          "streamed per layer from pinned host memory, ellipse masks 5/10/25/50/100%",
+    "c4": "28-block d=1152 bf16 stack, heterogeneous batch of 8 x 4096 tokens, blob masks "
+          "log-U[3%,80%], HBM-resident cache, varlen packing",
+    "c5": "19-block dual-stream d=3072 bf16 stack, 24 heads (head_dim 128), batch 4, 4096 image "
+          "+ 512 text tokens, image K/V streamed from pinned host memory, blob masks U[10%,40%]",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=40)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="c2", choices=sorted(DESCR))
+    p.add_argument("--masks", type=int, default=8, help="distinct seeded mask sets cycled over the steps")
+    p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-profile-pass", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain 1 GiB device copy (HBM counter calibration) and exit")
+    return p.parse_args()
+
+
+# ----------------------------------------------------------------------------- inputs
+
+
+def make_inputs(key, shape, n_masks, torch, W):
+    cfg = W.CONFIG_IDS[key]
+    dev = "cuda:0"
+    tdt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    n_params = shape.n_layers * (12 * shape.d_model ** 2) * (2 if shape.dual_stream else 1)
+    weights = []
+    if n_params <= 300_000_000:
+        for w in W.stack_weights(shape, cfg):
+            sets = w if isinstance(w, tuple) else (w,)
+            dev_sets = tuple({k: torch.as_tensor(v).to(dev).to(tdt) for k, v in s.items()} for s in sets)
+            weights.append(dev_sets if shape.dual_stream else dev_sets[0])
+    else:
+        # large stacks: the same N(0, 0.02) recipe drawn by a seeded device generator
+        g = torch.Generator(device=dev)
+        g.manual_seed(1000 + cfg)
+        d, f = shape.d_model, shape.mlp_mult * shape.d_model
+        shapes = {"w_qkv": (3 * d, d), "b_qkv": (3 * d,), "w_o": (d, d), "b_o": (d,), "w_1": (f, d),
+                  "b_1": (f,), "w_2": (d, f), "b_2": (d,)}
+
+        def one():
+            w = {k: (torch.randn(s, generator=g, device=dev) * 0.02).to(tdt) for k, s in shapes.items()}
+            for k in ("ln1_g", "ln2_g"):
+                w[k] = torch.ones(d, device=dev, dtype=tdt)
+            for k in ("ln1_b", "ln2_b"):
+                w[k] = torch.zeros(d, device=dev, dtype=tdt)
+            return w
+
+        for _ in range(shape.n_layers):
+            weights.append((one(), one()) if shape.dual_stream else one())
+    masks, xs, ratios = [], [], []
+    xt = W.template_hidden(shape, cfg)
+    for i in range(n_masks):
+        if key == "c3":
+            m = W.workload_mask(key, shape, mask_id=i, ratio=W.C3_RATIOS[i % len(W.C3_RATIOS)])
+        else:
+            m = W.workload_mask(key, shape, mask_id=i)
+        masks.append(torch.as_tensor(m).to(dev))
+        ratios.append(float(m.mean()))
+        xs.append(torch.as_tensor(W.edited_hidden(shape, cfg, xt, m)).to(dev).to(tdt))
+    g = torch.Generator(device=dev)
+    g.manual_seed(2000 + cfg)
+    B, T, N, d = shape.batch, shape.n_tokens, shape.n_image, shape.d_model
+    pinned = key in ("c3", "c5")
+    kv_layers = []
+    for _ in range(shape.n_layers):
+        rows = N if pinned else T
+        t = (torch.randn((B, rows, 2, d), generator=g, device=dev) * 0.5).to(tdt)
+        if pinned:
+            h = torch.empty(t.shape, dtype=tdt, pin_memory=True)
+            h.copy_(t)
+            kv_layers.append(h)
+            del t
+        else:
+            kv_layers.append(t)
+    slots = [torch.empty((B, T, 2, d), dtype=tdt, device=dev) for _ in range(2)] if pinned else (None, None)
+    ycache = torch.randn((B, T, d), generator=g, device=dev).to(tdt)
+    return weights, masks, xs, ratios, kv_layers, slots, ycache, pinned
+
+
+# ----------------------------------------------------------------------------- CPU oracle
+
+
+def cpu_baseline(key, shape, budget_s):
+    """The oracle as it stands, timed on this host over a bounded sample of the workload."""
+    import oracle
+    from paper_2505_20600_amd import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    cfg = W.CONFIG_IDS[key]
+    one = shape.replace(batch=1)
+    mask = W.workload_mask(key, shape, mask_id=0,
+                           ratio=(W.C3_RATIOS[0] if key == "c3" else None))[:1]
+    xt = W.template_hidden(one, cfg)
+    x = W.edited_hidden(one, cfg, xt, mask)
+    toks = oracle.masked_tokens(mask[0], one.n_text)
+    M = len(toks)
+    rnd = oracle.rounder(one.dtype)
+    xm = np.asarray(x[0][toks], np.float64)
+    t_layers, n = 0.0, 0
+    for l in range(one.n_layers):
+        w = W.layer_weights(one, cfg, l)
+        if one.dual_stream:
+            w = (w, W.layer_weights(one, cfg, l, text=True))
+        kv = W.synthetic_kv_cache(one, cfg, l)[0]
+        t0 = time.perf_counter()
+        xm, _ = oracle.block_rows(xm, toks, w, kv, one, rnd)
+        t_layers += time.perf_counter() - t0
+        n += 1
+        if t_layers >= budget_s:
+            break
+    per_layer = t_layers / n
+    step_s = per_layer * shape.n_layers * shape.batch * 1.0
+    # masked tokens of the whole step: the batch's expected M equals B x this request's M
+    value = M / (per_layer * shape.n_layers)
+    try:
+        model = next(l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo") if l.startswith("model name"))
+    except Exception:
+        model = "unknown"
+    return {
+        "value": value, "unit": "masked tokens/s", "cores": int(cores), "kind": "oracle",
+        "sample": f"request 0 of mask set 0 (M={M} masked rows), {n} of {shape.n_layers} layers "
+                  f"timed ({t_layers:.1f} s), scaled to the full stack; float64 NumPy; host: {model}",
+        "ms_per_layer": per_layer * 1e3,
+    }
+
+
+# ----------------------------------------------------------------------------- main
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (the method serves each request set on a single GPU); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs an MI355X GPU", file=sys.stderr)
+        sys.exit(1)
+    from paper_2505_20600_amd import maskstep as MS
+    from paper_2505_20600_amd import workloads as W
+    import oracle
+
+    if args.copy_calibration:
+        n = 1 << 30
+        a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+        b = torch.empty_like(a)
+        a.fill_(1)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "launches": 3}))
+        return
+
+    key = args.workload
+    shape = W.CONFIGS[key]
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    weights, masks, xs, ratios, kv_layers, slots, ycache, pinned = make_inputs(key, shape, args.masks, torch, W)
+    log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f} s; ratios {np.round(ratios, 3).tolist()}")
+    wc = MS.weights_array(weights)
+    desc = MS.model_desc(shape)
+    ws = torch.empty(MS.mask_workspace_bytes(desc, shape.batch), dtype=torch.uint8, device="cuda:0")
+    y = torch.empty_like(ycache)
+    stream = torch.cuda.current_stream()
+    copy_stream = torch.cuda.Stream() if pinned else None
+    Ms = []
+
+    def one_step(i):
+        st = MS.MaskStep(desc, shape.batch, masks[i], ws, stream)
+        st.stack_forward(wc, xs[i], ycache, kv_layers, y, pinned=pinned, slots=slots, stream=stream,
+                         copy_stream=copy_stream)
+        m = st.info().rows
+        st.close()
+        return m
+
+    for i in range(args.masks):
+        Ms.append(one_step(i))
+    for i in range(args.warmup):
+        one_step(i % args.masks)
+    torch.cuda.synchronize()
+
+    def timed(k, per_step=False):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(k + 1)]
+        tot_m = 0
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        evs[0].record(stream)
+        for s in range(k):
+            tot_m += one_step(s % args.masks)
+            evs[s + 1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        ms = evs[0].elapsed_time(evs[k])
+        steps = [evs[s].elapsed_time(evs[s + 1]) for s in range(k)] if per_step else None
+        return ms, wall, tot_m, steps
+
+    ms_total, wall, tot_m, step_ms = timed(args.steps, per_step=True)
+    log(f"[bench] timed {args.steps} steps: {ms_total:.3f} ms (events), {wall * 1e3:.3f} ms (wall)")
+    ms_step = ms_total / args.steps
+    value = tot_m / (ms_total / 1e3)
+    per_mask = {}
+    for s, t in enumerate(step_ms):
+        per_mask.setdefault(s % args.masks, []).append(t)
+    per_ratio = sorted([[round(ratios[i], 4), int(Ms[i]), round(float(np.median(v)), 4)] for i, v in per_mask.items()])
+
+    # profiled pass: per-kernel event timing over a second timed region
+    kernels, roof = {}, None
+    if not args.no_profile_pass:
+        MS.profiler_start(MS.KERNEL_CLASSES, capacity=1 << 16)
+        ms_prof, _, tot_m_prof, _ = timed(args.steps)
+        prof = MS.profiler_stop()
+        log(f"[bench] profiled pass: {ms_prof / args.steps:.4f} ms/step; {prof}")
+        d, T, L, f = shape.d_model, shape.n_tokens, shape.n_layers, shape.mlp_mult * shape.d_model
+        e = 2 if shape.dtype == "bf16" else 4
+        nset = 2 if shape.dual_stream else 1
+        m_sum = tot_m_prof * L                      # masked rows summed over the layers of all steps
+        work = {
+            "attention": ("mfma", 4.0 * m_sum * T * d),
+            "gemm_qkv": ("mfma", 2.0 * m_sum * d * 3 * d),
+            "gemm_out": ("mfma", 2.0 * m_sum * d * d),
+            "gemm_up": ("mfma", 2.0 * m_sum * d * f),
+            "gemm_down": ("mfma", 2.0 * m_sum * f * d),
+            "layernorm": ("hbm", 2.0 * 2 * m_sum * d * e),
+            "gather": ("hbm", 2.0 * tot_m_prof * d * e),
+        }
+        for c, (t_ms, n) in prof.items():
+            if c.startswith("_"):
+                continue
+            kernels[c] = {"ms_total": round(t_ms, 4), "launches": n, "us_avg": round(1e3 * t_ms / max(n, 1), 3)}
+            if c in work:
+                kind, amount = work[c]
+                if kind == "mfma":
+                    kernels[c]["tflops"] = round(amount / (t_ms / 1e3) / 1e12, 2)
+                else:
+                    kernels[c]["gbs"] = round(amount / (t_ms / 1e3) / 1e9, 1)
+        dom = max((c for c in kernels if c in work), key=lambda c: kernels[c]["ms_total"])
+        kind, amount = work[dom]
+        t_s = kernels[dom]["ms_total"] / 1e3
+        if kind == "mfma":
+            peak = PEAK["bf16_mfma_tflops"] if shape.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
+            ach = amount / t_s / 1e12
+            roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                    "frac": round(ach / peak, 4), "traffic": None, "kernel": dom,
+                    "per_launch_us": kernels[dom]["us_avg"]}
+        else:
+            ach = amount / t_s / 1e9
+            roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK["hbm_gbs"], "unit": "GB/s",
+                    "frac": round(ach / PEAK["hbm_gbs"], 4), "traffic": None, "kernel": dom,
+                    "per_launch_us": kernels[dom]["us_avg"]}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        cpu = cpu_baseline(key, shape, args.cpu_seconds)
+        log(f"[bench] cpu oracle sample took {time.perf_counter() - t0:.1f} s")
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "masked tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{shape.name}: {DESCR[key]}", "global_batch": shape.batch,
+                   "seq_len": shape.n_tokens, "parallelism": "none (1 GPU)",
+                   "masks": args.masks, "mean_masked_rows": round(float(np.mean(Ms)), 1)},
+        "per_mask": {"columns": ["ratio", "masked_rows", "median_ms"], "rows": per_ratio},
+        "roofline": roof,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,212 @@
+/*
+ * maskstep — one denoising step of a diffusion-transformer block stack in
+ * which only the masked (edited) tokens are recomputed, while the unmasked
+ * tokens' per-layer keys/values come from a cache of an earlier inference of
+ * the same image template (InstGenIE, arXiv 2505.20600: Sec. 3.1 "Mask-aware
+ * attention" with Fig. 5, and the K/V-caching variant of "Alternative
+ * approaches", Fig. 7; cost model in Table 1; block-wise pipelined cache
+ * loading in Sec. 4.2, Fig. 8).
+ *
+ * C ABI over hand-written HIP kernels for gfx950 (MI355X). Plain pointers
+ * and sizes only. The caller owns every buffer (device and pinned host);
+ * the library allocates no device memory. Streams and events are passed as
+ * `void*` and are `hipStream_t` / `hipEvent_t` of the HIP runtime the
+ * caller uses (NULL = the null stream).
+ *
+ * Conventions
+ *  - Every call returns an ms_status. Validation happens before anything is
+ *    enqueued, so an error leaves no partial work. The message of the last
+ *    error of the calling thread is returned by mask_last_error().
+ *  - All work is asynchronous on the given streams. mask_step_init is the
+ *    only call that blocks (one small device-to-host copy of the packed
+ *    layout, after which it synchronizes its stream).
+ *  - Element type: float32 (MS_FP32) or bfloat16 (MS_BF16, raw 16-bit
+ *    storage), uniform over weights, activations and caches of one model.
+ *    Accumulation is float32 in both cases.
+ *  - Layouts (row-major, innermost last):
+ *      hidden states        X, Y, Y_cache   [B][T][d]
+ *      working K/V          kv              [B][T][2][d]   (K row then V row per token)
+ *      pinned host K/V      h_kv            [B][N][2][d]   (image tokens only)
+ *      mask                 uint8           [B][N]         (nonzero = masked)
+ *      Linear weights       W               [out][in], bias [out]
+ *    with T = n_text + N tokens per request, N = grid_h * grid_w image
+ *    tokens in raster order (Sec. 2.1), head j owning columns
+ *    [j*hd, (j+1)*hd) of Q, K, V and the attention output.
+ *  - Packed masked rows: request-major; text tokens (always recomputed)
+ *    first within a request. With a separate text weight set (dual_stream)
+ *    the text rows of all requests come first, then the image rows of all
+ *    requests. Each packed row m has a flat token index rows[m] = b*T + t.
+ *  - Limits: d % 64 == 0; head_dim = d / n_heads, a multiple of 8, <= 128;
+ *    every pointer 16-byte aligned; batch <= max_batch <= 64.
+ */
+#ifndef MASKSTEP_H
+#define MASKSTEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MS_OK = 0,
+    MS_EINVAL = 1,      /* null pointer, bad enum, bad layer index */
+    MS_ESHAPE = 2,      /* shape outside the limits above */
+    MS_EDTYPE = 3,      /* unknown element type */
+    MS_EALIGN = 4,      /* pointer not 16-byte aligned */
+    MS_ENOTPINNED = 5,  /* host pointer that is not pinned (page-locked) memory */
+    MS_EWORKSPACE = 6,  /* workspace smaller than mask_workspace_bytes() */
+    MS_ESTATE = 7,      /* call out of order (e.g. no step context) */
+    MS_EHIP = 8         /* HIP runtime or launch error; message has hipGetErrorString */
+} ms_status;
+
+typedef enum { MS_FP32 = 0, MS_BF16 = 1 } ms_dtype;
+
+/* Shape of the block stack (pre-LN transformer blocks, Sec. 3.1). */
+typedef struct {
+    int32_t n_layers;
+    int32_t d_model;
+    int32_t n_heads;
+    int32_t mlp_mult;     /* feed-forward width = mlp_mult * d_model */
+    int32_t grid_h, grid_w;
+    int32_t n_text;       /* tokens before the image grid, always recomputed */
+    int32_t dual_stream;  /* 1: text tokens use a second weight set */
+    int32_t max_batch;
+    int32_t dtype;        /* ms_dtype */
+    float ln_eps;
+} ms_model_desc;
+
+/* One layer's parameters, device pointers of the model's element type. */
+typedef struct {
+    const void *ln1_g, *ln1_b;   /* [d] */
+    const void *w_qkv, *b_qkv;   /* [3d][d], [3d]  (Q rows, then K, then V) */
+    const void *w_o, *b_o;       /* [d][d], [d] */
+    const void *ln2_g, *ln2_b;   /* [d] */
+    const void *w_1, *b_1;       /* [f][d], [f] */
+    const void *w_2, *b_2;       /* [d][f], [d] */
+} ms_layer_weights;
+
+typedef enum { MS_KV_DEVICE = 0, MS_KV_HOST_PINNED = 1 } ms_kv_kind;
+
+/* Where the per-layer cached K/V come from.
+ *  MS_KV_DEVICE:      layer[l] is a device [B][T][2][d] buffer, resident in
+ *                     HBM; it is also the working buffer, so the masked rows
+ *                     are overwritten with fresh K/V during the step.
+ *  MS_KV_HOST_PINNED: layer[l] is a pinned host [B][N][2][d] buffer (image
+ *                     tokens); slot[0], slot[1] are device [B][T][2][d]
+ *                     buffers that layers alternate through (layer l uses
+ *                     slot[l % 2]); loads run on the copy stream. */
+typedef struct {
+    int32_t kind;
+    const void* const* layer;   /* [n_layers] */
+    void* slot[2];
+} ms_kv_source;
+
+typedef struct ms_step ms_step;   /* opaque host object, one per mask set */
+
+typedef struct {
+    int32_t batch;
+    int32_t rows;        /* M: packed recomputed rows over the batch */
+    int32_t n_segments;  /* packed segments (one per request, two with dual_stream) */
+    int32_t n_qtiles;    /* attention query tiles */
+    int32_t text_rows;   /* packed rows that use the text weight set */
+} ms_step_info;
+
+/* Bytes of device workspace a step over `batch` requests needs (worst case,
+ * every token masked). Returns 0 and sets the error on an invalid description. */
+size_t mask_workspace_bytes(const ms_model_desc* desc, int32_t batch);
+
+/* Mask compaction (token selection of Sec. 3.1): from d_mask [B][N] builds,
+ * inside the workspace, the ascending masked-row index of every request, the
+ * inverse map and the packed-segment table, then copies the segment table to
+ * the host and synchronizes `stream`. The workspace must stay valid and
+ * unused by anyone else until mask_step_destroy. `*out` receives a new step
+ * context. Masks are constant over the denoising steps of a request, so one
+ * context serves every step of the same mask set. */
+ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch,
+                         const uint8_t* d_mask, void* d_ws, size_t ws_bytes, void* stream);
+
+ms_status mask_step_get_info(const ms_step* step, ms_step_info* info);
+
+/* Device pointers into the workspace: rows [M] (flat b*T + t of each packed
+ * row), inv [B*T] (packed row of a token, -1 if not recomputed), seg_start
+ * [n_segments + 1] (packed offset of each segment). Valid until destroy. */
+ms_status mask_step_index(const ms_step* step, const int32_t** d_rows, const int32_t** d_inv,
+                          const int32_t** d_seg_start);
+
+/* Row gather ("extract the matrix of masked tokens", Sec. 3.1):
+ * d_xm[m] = d_x[rows[m]]; d_x [B][T][d], d_xm [M][d] (may be NULL: the
+ * workspace's own packed-hidden buffer is used). */
+ms_status mask_gather_rows(ms_step* step, const void* d_x, void* d_xm, void* stream);
+
+/* One pre-LN block over the packed rows (Sec. 3.1, Fig. 5 bottom with the
+ * K/V cache of Fig. 7): LN1, QKV projection whose K/V rows are written into
+ * d_kv at the masked tokens, attention of the masked queries over all T keys
+ * of their request in d_kv, out projection + residual, LN2, feed-forward with
+ * GELU + residual. d_xm [M][d] is read and overwritten with the block output
+ * (NULL: the workspace buffer). d_kv [B][T][2][d] must hold the cached K/V of
+ * every unmasked token; its masked rows are overwritten. `w` points to one
+ * weight set, or two (image, text) when dual_stream. `layer` is only checked
+ * against n_layers. */
+ms_status mask_block_forward(ms_step* step, int32_t layer, const ms_layer_weights* w,
+                             void* d_xm, void* d_kv, void* stream);
+
+/* Final scatter ("replenishing cached activations for the unmasked tokens",
+ * Sec. 3.1): d_y = d_ycache with d_y[rows[m]] = d_xm[m]. d_y may equal
+ * d_ycache (then only the masked rows are written). d_ycache may be NULL only
+ * when every token is masked. d_xm NULL: the workspace buffer. */
+ms_status mask_scatter_rows(ms_step* step, const void* d_xm, const void* d_ycache, void* d_y,
+                            void* stream);
+
+/* Block-wise cache loading (Sec. 4.2, Fig. 8 middle): enqueues on
+ * `copy_stream` the host-to-device copies of layer `layer`'s cached K/V of
+ * the unmasked image tokens, h_kv [B][N][2][d] (pinned) -> d_slot
+ * [B][T][2][d] at rows n_text + n. Runs of unmasked tokens are merged
+ * across short masked gaps (the masked rows copied that way are overwritten
+ * by the block's fresh K/V afterwards, so the block must be ordered after the
+ * copy). If wait_event is not NULL the copies start after it; if
+ * signal_event is not NULL it is recorded after them. Nothing is copied when
+ * every token is masked. */
+ms_status cache_prefetch_layer(ms_step* step, int32_t layer, const void* h_kv, void* d_slot,
+                               void* copy_stream, void* wait_event, void* signal_event);
+
+/* The whole step: gather, the n_layers blocks, final scatter, with the cache
+ * read from HBM or streamed per layer from pinned host memory on copy_stream
+ * two layers ahead of the compute stream (Fig. 8 middle). `w` holds n_layers
+ * weight sets ([n_layers][2] when dual_stream: image, text). d_x [B][T][d]
+ * holds the current hidden states (only masked rows and text rows are read);
+ * d_y [B][T][d] receives the output; it may equal d_ycache. With the
+ * environment variable MS_SERIALIZE=1, copies run on the compute stream
+ * before each block instead (the naive loading of Fig. 8 top). */
+ms_status mask_stack_forward(ms_step* step, const ms_layer_weights* w, const void* d_x,
+                             const void* d_ycache, const ms_kv_source* kv, void* d_y,
+                             void* compute_stream, void* copy_stream);
+
+void mask_step_destroy(ms_step* step);
+
+/* Kernel timing (tracing). Between start and stop, every launch of a
+ * selected kernel class is bracketed by a pair of timing events on the
+ * stream it is launched on; stop synchronizes those events and returns, per
+ * class, the summed milliseconds and the launch count (arrays of
+ * MS_K_COUNT entries, either may be NULL). Process-wide; up to `capacity`
+ * launches are recorded, further ones are counted in `dropped`. */
+typedef enum {
+    MS_K_COMPACT = 0, MS_K_GATHER = 1, MS_K_LAYERNORM = 2, MS_K_GEMM_QKV = 3,
+    MS_K_ATTENTION = 4, MS_K_GEMM_OUT = 5, MS_K_GEMM_UP = 6, MS_K_GEMM_DOWN = 7,
+    MS_K_SCATTER = 8, MS_K_COPY = 9, MS_K_COUNT = 10
+} ms_kernel_class;
+
+ms_status mask_profiler_start(uint32_t class_mask, int32_t capacity);
+ms_status mask_profiler_stop(double* total_ms, int64_t* launches, int64_t* dropped);
+
+/* Message of the calling thread's last error ("" if none). */
+const char* mask_last_error(void);
+
+int32_t mask_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MASKSTEP_H */

@@ -1,0 +1,95 @@
+// Device-side helpers shared by the maskstep kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ms {
+
+using bf16_t = uint16_t;  // raw bfloat16 storage
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+    return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// float32 -> bfloat16, round to nearest even; NaN stays a (quiet) NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<bf16_t>(u >> 16);
+}
+
+// Element-type traits: conversion to/from float and the 16x16 MFMA step.
+template <typename T> struct Elt;
+
+template <> struct Elt<float> {
+    static constexpr int kKStep = 4;     // K depth of one v_mfma_f32_16x16x4_f32
+    static constexpr int kKPerLane = 1;  // K elements each lane feeds per MFMA
+    using frag_t = float;
+    __device__ __forceinline__ static float to_f32(float v) { return v; }
+    __device__ __forceinline__ static float from_f32(float v) { return v; }
+    __device__ __forceinline__ static f32x4_t mma(frag_t a, frag_t b, f32x4_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+};
+
+template <> struct Elt<bf16_t> {
+    static constexpr int kKStep = 32;    // K depth of one v_mfma_f32_16x16x32_bf16
+    static constexpr int kKPerLane = 8;
+    using frag_t = bf16x8_t;
+    __device__ __forceinline__ static float to_f32(bf16_t v) { return bf16_to_f32(v); }
+    __device__ __forceinline__ static bf16_t from_f32(float v) { return f32_to_bf16(v); }
+    __device__ __forceinline__ static f32x4_t mma(frag_t a, frag_t b, f32x4_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+// 16-byte vector load/store helpers.
+struct alignas(16) vec16 { uint32_t w[4]; };
+
+__device__ __forceinline__ vec16 ld16(const void* p) { return *reinterpret_cast<const vec16*>(p); }
+__device__ __forceinline__ void st16(void* p, const vec16& v) { *reinterpret_cast<vec16*>(p) = v; }
+
+// Four consecutive elements <-> float4.
+template <typename T> __device__ __forceinline__ void load4(const T* p, float out[4]);
+template <> __device__ __forceinline__ void load4<float>(const float* p, float out[4]) {
+    float4 v = *reinterpret_cast<const float4*>(p);
+    out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
+}
+template <> __device__ __forceinline__ void load4<bf16_t>(const bf16_t* p, float out[4]) {
+    uint2 v = *reinterpret_cast<const uint2*>(p);
+    out[0] = __uint_as_float(v.x << 16);
+    out[1] = __uint_as_float(v.x & 0xffff0000u);
+    out[2] = __uint_as_float(v.y << 16);
+    out[3] = __uint_as_float(v.y & 0xffff0000u);
+}
+template <typename T> __device__ __forceinline__ void store4(T* p, const float v[4]);
+template <> __device__ __forceinline__ void store4<float>(float* p, const float v[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+template <> __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, const float v[4]) {
+    uint2 o;
+    o.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+    o.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+    *reinterpret_cast<uint2*>(p) = o;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+}  // namespace ms

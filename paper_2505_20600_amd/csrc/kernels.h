@@ -1,0 +1,66 @@
+// Host-side launchers of the maskstep kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ms {
+
+constexpr int kQTile = 64;        // attention query rows per workgroup
+constexpr int kMaxSegments = 128; // packed segments per step
+
+enum Dtype { kF32 = 0, kBF16 = 1 };
+
+// a1: mask -> packed rows, inverse map, segment and query-tile tables.
+hipError_t launch_compact(const uint8_t* mask, int B, int N, int n_text, int dual,
+                          int32_t* rows, int32_t* inv, int32_t* seg_start, int32_t* seg_req,
+                          int32_t* cu_tiles, hipStream_t s);
+
+// a2: xm[m] = x[rows[m]].
+hipError_t launch_gather(const void* x, const int32_t* rows, void* xm, int M, int row_bytes,
+                         hipStream_t s);
+
+// a11: y = ycache with y[rows[m]] = xm[m] (aliased: only masked rows written).
+hipError_t launch_scatter(const void* xm, const int32_t* rows, const int32_t* inv,
+                          const void* ycache, void* y, int M, int total_rows, int row_bytes,
+                          hipStream_t s);
+
+// a3 / a8: y = LN(x) row-wise; rows [0, m_split) use (g1, b1), the rest (g0, b0).
+hipError_t launch_layernorm(int dtype, const void* x, const void* g0, const void* b0,
+                            const void* g1, const void* b1, int m_split, void* y, int M, int d,
+                            float eps, hipStream_t s);
+
+enum Epilogue { kEpiBias = 0, kEpiBiasResid = 1, kEpiBiasGelu = 2, kEpiQKV = 3 };
+
+struct GemmDesc {
+    const void* A;      // [M][K] activations, row stride lda (elements)
+    const void* W;      // [N][K] weights
+    const void* bias;   // [N]
+    const void* R;      // [M][N] residual (kEpiBiasResid), row stride ldr
+    void* C;            // [M][N] output, row stride ldc (kEpiQKV: Q columns [0, d))
+    void* kv;           // kEpiQKV: [B*T][2][d] working K/V
+    const int32_t* rows;// kEpiQKV: flat token row of each packed row
+    int M, N, K;
+    int lda, ldr, ldc;
+    int d;              // kEpiQKV: model width
+    int epilogue;
+};
+
+// a4/a5/a7/a8/a9: out = epi(A W^T + bias).
+hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t s);
+
+struct AttnDesc {
+    const void* q;        // [M][d]
+    const void* kv;       // [B][T][2][d]
+    void* o;              // [M][d]
+    const int32_t* seg_start;
+    const int32_t* seg_req;
+    const int32_t* cu_tiles;
+    int nseg, T, d, hd, n_qtiles, n_heads;
+    float scale_log2;     // log2(e) / sqrt(hd)
+};
+
+// a6: attention of the packed masked queries over every key of their request.
+hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s);
+
+}  // namespace ms

@@ -1,0 +1,610 @@
+// C-ABI of the mask-aware K/V-cached step: validation, workspace carving,
+// per-layer orchestration and the pinned-host cache stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <mutex>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/maskstep.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int32_t kAbiVersion = 1;
+constexpr int kMaxBatch = 64;
+// Host-to-device copy spans are merged across masked gaps of at most this
+// many bytes: a gap costs less PCIe time than one more copy submission.
+constexpr size_t kGapMergeBytes = 256 * 1024;
+
+thread_local std::string g_err;
+
+ms_status fail(ms_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+ms_status ok() {
+    g_err.clear();
+    return MS_OK;
+}
+
+#define MS_HIP(call)                                                                    \
+    do {                                                                                \
+        hipError_t e_ = (call);                                                         \
+        if (e_ != hipSuccess) return fail(MS_EHIP, "%s: %s", #call, hipGetErrorString(e_)); \
+    } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+    size_t rows, inv, seg_start, seg_req, cu_tiles, xm, a, q, o, h, u, total;
+};
+
+int elt_bytes(int32_t dtype) { return dtype == MS_BF16 ? 2 : 4; }
+
+ms_status validate_desc(const ms_model_desc* d) {
+    if (!d) return fail(MS_EINVAL, "model description is NULL");
+    if (d->dtype != MS_FP32 && d->dtype != MS_BF16) return fail(MS_EDTYPE, "unknown dtype %d", d->dtype);
+    if (d->n_layers < 1) return fail(MS_ESHAPE, "n_layers must be >= 1");
+    if (d->d_model < 64 || d->d_model % 64) return fail(MS_ESHAPE, "d_model must be a positive multiple of 64");
+    if (d->n_heads < 1 || d->d_model % d->n_heads) return fail(MS_ESHAPE, "d_model %% n_heads != 0");
+    const int hd = d->d_model / d->n_heads;
+    if (hd % 8 || hd > 128) return fail(MS_ESHAPE, "head_dim %d must be a multiple of 8 and <= 128", hd);
+    if (d->dtype == MS_FP32 && hd > 64) return fail(MS_ESHAPE, "fp32 supports head_dim <= 64");
+    if (d->dtype == MS_BF16 && d->d_model > 4096) return fail(MS_ESHAPE, "bf16 supports d_model <= 4096");
+    if (d->dtype == MS_FP32 && d->d_model > 2048) return fail(MS_ESHAPE, "fp32 supports d_model <= 2048");
+    if (d->mlp_mult < 1 || d->mlp_mult > 8) return fail(MS_ESHAPE, "mlp_mult must be in 1..8");
+    if (d->grid_h < 1 || d->grid_w < 1) return fail(MS_ESHAPE, "grid must be at least 1x1");
+    if (d->n_text < 0) return fail(MS_ESHAPE, "n_text must be >= 0");
+    if ((int64_t)d->grid_h * d->grid_w + d->n_text > (1 << 20)) return fail(MS_ESHAPE, "too many tokens");
+    if (d->dual_stream != 0 && d->dual_stream != 1) return fail(MS_EINVAL, "dual_stream must be 0 or 1");
+    if (d->max_batch < 1 || d->max_batch > kMaxBatch) return fail(MS_ESHAPE, "max_batch must be in 1..%d", kMaxBatch);
+    if (!(d->ln_eps >= 0.f) || !std::isfinite(d->ln_eps)) return fail(MS_EINVAL, "ln_eps must be finite and >= 0");
+    return MS_OK;
+}
+
+Layout make_layout(const ms_model_desc& d, int32_t B) {
+    Layout L{};
+    const size_t T = (size_t)d.n_text + (size_t)d.grid_h * d.grid_w;
+    const size_t BT = (size_t)B * T;
+    const size_t e = elt_bytes(d.dtype);
+    const size_t dm = d.d_model, f = (size_t)d.mlp_mult * d.d_model;
+    size_t off = 0;
+    auto take = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return o; };
+    L.rows = take(BT * 4);
+    L.inv = take(BT * 4);
+    L.seg_start = take((ms::kMaxSegments + 1) * 4);
+    L.seg_req = take(ms::kMaxSegments * 4);
+    L.cu_tiles = take((ms::kMaxSegments + 1) * 4);
+    L.xm = take(BT * dm * e);
+    L.a = take(BT * dm * e);
+    L.q = take(BT * dm * e);
+    L.o = take(BT * dm * e);
+    L.h = take(BT * dm * e);
+    L.u = take(BT * f * e);
+    L.total = off;
+    return L;
+}
+
+struct Span {
+    int b, n0, n1;   // image rows [n0, n1) of request b
+};
+
+// Kernel timing: event pairs around launches of the selected classes.
+struct Profiler {
+    std::mutex mu;
+    std::atomic<bool> on{false};
+    uint32_t mask = 0;
+    int capacity = 0, used = 0;
+    int64_t dropped = 0;
+    std::vector<hipEvent_t> pool;   // 2 per recorded launch
+    std::vector<int> cls;
+};
+Profiler g_prof;
+
+class ProfScope {
+  public:
+    ProfScope(int c, hipStream_t s) : s_(s) {
+        if (!g_prof.on.load(std::memory_order_relaxed) || !(g_prof.mask & (1u << c))) return;
+        std::lock_guard<std::mutex> lk(g_prof.mu);
+        if (g_prof.used >= g_prof.capacity) { ++g_prof.dropped; return; }
+        idx_ = g_prof.used++;
+        g_prof.cls[idx_] = c;
+        (void)hipEventRecord(g_prof.pool[2 * idx_], s_);
+    }
+    ~ProfScope() {
+        if (idx_ >= 0) (void)hipEventRecord(g_prof.pool[2 * idx_ + 1], s_);
+    }
+    ProfScope(const ProfScope&) = delete;
+    ProfScope& operator=(const ProfScope&) = delete;
+
+  private:
+    hipStream_t s_;
+    int idx_ = -1;
+};
+
+}  // namespace
+
+struct ms_step {
+    ms_model_desc desc;
+    int B = 0, T = 0, N = 0, d = 0, f = 0, hd = 0, elt = 0;
+    int M = 0, nseg = 0, n_qtiles = 0, text_rows = 0;
+    bool all_masked = false;
+    char* ws = nullptr;
+    Layout lay{};
+    std::vector<int32_t> seg_start;
+    std::vector<Span> spans;
+    hipEvent_t ev_copied[2] = {nullptr, nullptr};
+    hipEvent_t ev_consumed[2] = {nullptr, nullptr};
+    hipEvent_t ev_start = nullptr;
+
+    int32_t* rows() const { return reinterpret_cast<int32_t*>(ws + lay.rows); }
+    int32_t* inv() const { return reinterpret_cast<int32_t*>(ws + lay.inv); }
+    int32_t* segs() const { return reinterpret_cast<int32_t*>(ws + lay.seg_start); }
+    int32_t* segreq() const { return reinterpret_cast<int32_t*>(ws + lay.seg_req); }
+    int32_t* cutiles() const { return reinterpret_cast<int32_t*>(ws + lay.cu_tiles); }
+    void* buf(size_t off) const { return ws + off; }
+};
+
+namespace {
+
+void destroy_events(ms_step* s) {
+    for (int i = 0; i < 2; ++i) {
+        if (s->ev_copied[i]) (void)hipEventDestroy(s->ev_copied[i]);
+        if (s->ev_consumed[i]) (void)hipEventDestroy(s->ev_consumed[i]);
+    }
+    if (s->ev_start) (void)hipEventDestroy(s->ev_start);
+}
+
+void plan_spans(ms_step* s, const std::vector<uint8_t>& mask) {
+    s->spans.clear();
+    const size_t row_bytes = 2ull * s->d * s->elt;
+    const int gap_rows = (int)std::max<size_t>(1, kGapMergeBytes / row_bytes);
+    for (int b = 0; b < s->B; ++b) {
+        const uint8_t* m = mask.data() + (size_t)b * s->N;
+        int n = 0;
+        Span cur{b, -1, -1};
+        while (n < s->N) {
+            while (n < s->N && m[n]) ++n;
+            if (n >= s->N) break;
+            int n0 = n;
+            while (n < s->N && !m[n]) ++n;
+            if (cur.n0 >= 0 && n0 - cur.n1 <= gap_rows) {
+                cur.n1 = n;
+            } else {
+                if (cur.n0 >= 0) s->spans.push_back(cur);
+                cur = Span{b, n0, n};
+            }
+        }
+        if (cur.n0 >= 0) s->spans.push_back(cur);
+    }
+}
+
+ms_status check_weights(const ms_step* s, const ms_layer_weights* w) {
+    const int nsets = (s->desc.dual_stream && s->desc.n_text > 0) ? 2 : 1;
+    for (int i = 0; i < nsets; ++i) {
+        const void* p[] = {w[i].ln1_g, w[i].ln1_b, w[i].w_qkv, w[i].b_qkv, w[i].w_o, w[i].b_o,
+                           w[i].ln2_g, w[i].ln2_b, w[i].w_1, w[i].b_1, w[i].w_2, w[i].b_2};
+        for (const void* q : p) {
+            if (!q) return fail(MS_EINVAL, "weight set %d has a NULL pointer", i);
+            if (!aligned16(q)) return fail(MS_EALIGN, "weight set %d has a pointer not 16-byte aligned", i);
+        }
+    }
+    return MS_OK;
+}
+
+ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* kv, hipStream_t st) {
+    if (s->M == 0) return MS_OK;
+    const int dt = s->desc.dtype;
+    const bool dual = s->desc.dual_stream && s->desc.n_text > 0;
+    const ms_layer_weights& wi = w[0];
+    const ms_layer_weights& wt = dual ? w[1] : w[0];
+    const int M = s->M, d = s->d, f = s->f, e = s->elt;
+    const int msplit = s->text_rows;
+    char* a = static_cast<char*>(s->buf(s->lay.a));
+    char* q = static_cast<char*>(s->buf(s->lay.q));
+    char* o = static_cast<char*>(s->buf(s->lay.o));
+    char* h = static_cast<char*>(s->buf(s->lay.h));
+    char* u = static_cast<char*>(s->buf(s->lay.u));
+    char* x = static_cast<char*>(xm);
+
+    {
+        ProfScope p(MS_K_LAYERNORM, st);
+        MS_HIP(ms::launch_layernorm(dt, x, wi.ln1_g, wi.ln1_b, wt.ln1_g, wt.ln1_b, msplit, a, M, d,
+                                    s->desc.ln_eps, st));
+    }
+    // row ranges per weight set: text rows [0, msplit) then image rows
+    struct Range { int r0, r1; const ms_layer_weights* w; };
+    Range ranges[2] = {{0, msplit, &wt}, {msplit, M, &wi}};
+    for (const Range& r : ranges) {
+        if (r.r1 <= r.r0) continue;
+        ms::GemmDesc g{};
+        g.A = a + (size_t)r.r0 * d * e;
+        g.W = r.w->w_qkv;
+        g.bias = r.w->b_qkv;
+        g.C = q + (size_t)r.r0 * d * e;
+        g.kv = kv;
+        g.rows = s->rows() + r.r0;
+        g.M = r.r1 - r.r0; g.N = 3 * d; g.K = d;
+        g.lda = d; g.ldc = d; g.d = d;
+        g.epilogue = ms::kEpiQKV;
+        ProfScope p(MS_K_GEMM_QKV, st);
+        MS_HIP(ms::launch_gemm(dt, g, st));
+    }
+    ms::AttnDesc ad{};
+    ad.q = q; ad.kv = kv; ad.o = o;
+    ad.seg_start = s->segs(); ad.seg_req = s->segreq(); ad.cu_tiles = s->cutiles();
+    ad.nseg = s->nseg; ad.T = s->T; ad.d = d; ad.hd = s->hd;
+    ad.n_qtiles = s->n_qtiles; ad.n_heads = s->desc.n_heads;
+    ad.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)s->hd));
+    {
+        ProfScope p(MS_K_ATTENTION, st);
+        MS_HIP(ms::launch_attention(dt, ad, st));
+    }
+    for (const Range& r : ranges) {
+        if (r.r1 <= r.r0) continue;
+        ms::GemmDesc g{};
+        g.A = o + (size_t)r.r0 * d * e; g.W = r.w->w_o; g.bias = r.w->b_o;
+        g.R = x + (size_t)r.r0 * d * e; g.C = h + (size_t)r.r0 * d * e;
+        g.M = r.r1 - r.r0; g.N = d; g.K = d; g.lda = d; g.ldr = d; g.ldc = d;
+        g.epilogue = ms::kEpiBiasResid;
+        ProfScope p(MS_K_GEMM_OUT, st);
+        MS_HIP(ms::launch_gemm(dt, g, st));
+    }
+    {
+        ProfScope p(MS_K_LAYERNORM, st);
+        MS_HIP(ms::launch_layernorm(dt, h, wi.ln2_g, wi.ln2_b, wt.ln2_g, wt.ln2_b, msplit, a, M, d,
+                                    s->desc.ln_eps, st));
+    }
+    for (const Range& r : ranges) {
+        if (r.r1 <= r.r0) continue;
+        ms::GemmDesc g{};
+        g.A = a + (size_t)r.r0 * d * e; g.W = r.w->w_1; g.bias = r.w->b_1;
+        g.C = u + (size_t)r.r0 * f * e;
+        g.M = r.r1 - r.r0; g.N = f; g.K = d; g.lda = d; g.ldc = f;
+        g.epilogue = ms::kEpiBiasGelu;
+        ProfScope p(MS_K_GEMM_UP, st);
+        MS_HIP(ms::launch_gemm(dt, g, st));
+    }
+    for (const Range& r : ranges) {
+        if (r.r1 <= r.r0) continue;
+        ms::GemmDesc g{};
+        g.A = u + (size_t)r.r0 * f * e; g.W = r.w->w_2; g.bias = r.w->b_2;
+        g.R = h + (size_t)r.r0 * d * e; g.C = x + (size_t)r.r0 * d * e;
+        g.M = r.r1 - r.r0; g.N = d; g.K = f; g.lda = f; g.ldr = d; g.ldc = d;
+        g.epilogue = ms::kEpiBiasResid;
+        ProfScope p(MS_K_GEMM_DOWN, st);
+        MS_HIP(ms::launch_gemm(dt, g, st));
+    }
+    return MS_OK;
+}
+
+ms_status prefetch(ms_step* s, const void* h_kv, void* d_slot, hipStream_t cs, hipEvent_t wait) {
+    if (wait) MS_HIP(hipStreamWaitEvent(cs, wait, 0));
+    ProfScope p(MS_K_COPY, cs);
+    const size_t row_bytes = 2ull * s->d * s->elt;
+    const char* src = static_cast<const char*>(h_kv);
+    char* dst = static_cast<char*>(d_slot);
+    for (const Span& sp : s->spans) {
+        const size_t so = ((size_t)sp.b * s->N + sp.n0) * row_bytes;
+        const size_t dof = ((size_t)sp.b * s->T + s->desc.n_text + sp.n0) * row_bytes;
+        MS_HIP(hipMemcpyAsync(dst + dof, src + so, (size_t)(sp.n1 - sp.n0) * row_bytes,
+                              hipMemcpyHostToDevice, cs));
+    }
+    return MS_OK;
+}
+
+ms_status prefetch_signal(ms_step* s, const void* h_kv, void* d_slot, hipStream_t cs, hipEvent_t wait,
+                          hipEvent_t signal) {
+    ms_status st = prefetch(s, h_kv, d_slot, cs, wait);
+    if (st != MS_OK) return st;
+    if (signal) MS_HIP(hipEventRecord(signal, cs));
+    return MS_OK;
+}
+
+ms_status check_pinned(const void* p) {
+    hipPointerAttribute_t attr;
+    hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(MS_ENOTPINNED, "host K/V pointer is not pinned host memory (%s)", hipGetErrorString(e));
+    }
+    if (attr.type != hipMemoryTypeHost)
+        return fail(MS_ENOTPINNED, "host K/V pointer is not pinned host memory (memory type %d)", (int)attr.type);
+    return MS_OK;
+}
+
+bool env_flag(const char* name) {
+    const char* v = std::getenv(name);
+    return v && v[0] && std::strcmp(v, "0") != 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t mask_abi_version(void) { return kAbiVersion; }
+
+const char* mask_last_error(void) { return g_err.c_str(); }
+
+size_t mask_workspace_bytes(const ms_model_desc* desc, int32_t batch) {
+    if (validate_desc(desc) != MS_OK) return 0;
+    if (batch < 1 || batch > desc->max_batch) {
+        fail(MS_ESHAPE, "batch %d outside 1..max_batch", batch);
+        return 0;
+    }
+    g_err.clear();
+    return make_layout(*desc, batch).total;
+}
+
+ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch,
+                         const uint8_t* d_mask, void* d_ws, size_t ws_bytes, void* stream) {
+    if (!out) return fail(MS_EINVAL, "out is NULL");
+    *out = nullptr;
+    ms_status st = validate_desc(desc);
+    if (st != MS_OK) return st;
+    if (batch < 1 || batch > desc->max_batch) return fail(MS_ESHAPE, "batch %d outside 1..max_batch", batch);
+    if (!d_mask || !d_ws) return fail(MS_EINVAL, "mask or workspace is NULL");
+    if (!aligned16(d_ws)) return fail(MS_EALIGN, "workspace not 16-byte aligned");
+    const Layout lay = make_layout(*desc, batch);
+    if (ws_bytes < lay.total)
+        return fail(MS_EWORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, lay.total);
+
+    ms_step* s = new (std::nothrow) ms_step();
+    if (!s) return fail(MS_EINVAL, "out of host memory");
+    s->desc = *desc;
+    s->B = batch;
+    s->N = desc->grid_h * desc->grid_w;
+    s->T = desc->n_text + s->N;
+    s->d = desc->d_model;
+    s->f = desc->mlp_mult * desc->d_model;
+    s->hd = desc->d_model / desc->n_heads;
+    s->elt = elt_bytes(desc->dtype);
+    s->ws = static_cast<char*>(d_ws);
+    s->lay = lay;
+    const bool split = desc->dual_stream && desc->n_text > 0;
+    s->nseg = split ? 2 * batch : batch;
+    s->text_rows = split ? batch * desc->n_text : 0;
+
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    auto bail = [&](ms_status code) { destroy_events(s); delete s; return code; };
+    hipError_t e;
+    {
+        ProfScope p(MS_K_COMPACT, hs);
+        e = ms::launch_compact(d_mask, batch, s->N, desc->n_text, split ? 1 : 0, s->rows(), s->inv(),
+                               s->segs(), s->segreq(), s->cutiles(), hs);
+    }
+    if (e != hipSuccess) return bail(fail(MS_EHIP, "compaction launch: %s", hipGetErrorString(e)));
+    s->seg_start.assign(s->nseg + 1, 0);
+    std::vector<uint8_t> hmask((size_t)batch * s->N);
+    e = hipMemcpyAsync(s->seg_start.data(), s->segs(), (s->nseg + 1) * sizeof(int32_t),
+                       hipMemcpyDeviceToHost, hs);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(hmask.data(), d_mask, hmask.size(), hipMemcpyDeviceToHost, hs);
+    if (e == hipSuccess) e = hipStreamSynchronize(hs);
+    if (e != hipSuccess) return bail(fail(MS_EHIP, "compaction readback: %s", hipGetErrorString(e)));
+    s->M = s->seg_start[s->nseg];
+    s->n_qtiles = 0;
+    for (int i = 0; i < s->nseg; ++i)
+        s->n_qtiles += (s->seg_start[i + 1] - s->seg_start[i] + ms::kQTile - 1) / ms::kQTile;
+    s->all_masked = s->M == batch * s->T;
+    plan_spans(s, hmask);
+    for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+        e = hipEventCreateWithFlags(&s->ev_copied[i], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&s->ev_consumed[i], hipEventDisableTiming);
+    }
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&s->ev_start, hipEventDisableTiming);
+    if (e != hipSuccess) return bail(fail(MS_EHIP, "event creation: %s", hipGetErrorString(e)));
+    *out = s;
+    return ok();
+}
+
+ms_status mask_step_get_info(const ms_step* s, ms_step_info* info) {
+    if (!s || !info) return fail(MS_EINVAL, "NULL argument");
+    info->batch = s->B;
+    info->rows = s->M;
+    info->n_segments = s->nseg;
+    info->n_qtiles = s->n_qtiles;
+    info->text_rows = s->text_rows;
+    return ok();
+}
+
+ms_status mask_step_index(const ms_step* s, const int32_t** d_rows, const int32_t** d_inv,
+                          const int32_t** d_seg_start) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (d_rows) *d_rows = s->rows();
+    if (d_inv) *d_inv = s->inv();
+    if (d_seg_start) *d_seg_start = s->segs();
+    return ok();
+}
+
+ms_status mask_gather_rows(ms_step* s, const void* d_x, void* d_xm, void* stream) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (!d_x) return fail(MS_EINVAL, "x is NULL");
+    void* xm = d_xm ? d_xm : s->buf(s->lay.xm);
+    if (!aligned16(d_x) || !aligned16(xm)) return fail(MS_EALIGN, "x / xm not 16-byte aligned");
+    ProfScope p(MS_K_GATHER, static_cast<hipStream_t>(stream));
+    MS_HIP(ms::launch_gather(d_x, s->rows(), xm, s->M, s->d * s->elt, static_cast<hipStream_t>(stream)));
+    return ok();
+}
+
+ms_status mask_block_forward(ms_step* s, int32_t layer, const ms_layer_weights* w, void* d_xm,
+                             void* d_kv, void* stream) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (layer < 0 || layer >= s->desc.n_layers) return fail(MS_EINVAL, "layer %d out of range", layer);
+    if (!w || !d_kv) return fail(MS_EINVAL, "weights or kv is NULL");
+    void* xm = d_xm ? d_xm : s->buf(s->lay.xm);
+    if (!aligned16(xm) || !aligned16(d_kv)) return fail(MS_EALIGN, "xm / kv not 16-byte aligned");
+    ms_status st = check_weights(s, w);
+    if (st != MS_OK) return st;
+    st = block_forward(s, w, xm, d_kv, static_cast<hipStream_t>(stream));
+    return st == MS_OK ? ok() : st;
+}
+
+ms_status mask_scatter_rows(ms_step* s, const void* d_xm, const void* d_ycache, void* d_y,
+                            void* stream) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (!d_y) return fail(MS_EINVAL, "y is NULL");
+    if (!d_ycache && !s->all_masked) return fail(MS_EINVAL, "y_cache may be NULL only when every token is masked");
+    const void* xm = d_xm ? d_xm : s->buf(s->lay.xm);
+    if (!aligned16(d_y) || !aligned16(xm) || !aligned16(d_ycache)) return fail(MS_EALIGN, "pointer not 16-byte aligned");
+    ProfScope p(MS_K_SCATTER, static_cast<hipStream_t>(stream));
+    MS_HIP(ms::launch_scatter(xm, s->rows(), s->inv(), d_ycache, d_y, s->M, s->B * s->T,
+                              s->d * s->elt, static_cast<hipStream_t>(stream)));
+    return ok();
+}
+
+ms_status cache_prefetch_layer(ms_step* s, int32_t layer, const void* h_kv, void* d_slot,
+                               void* copy_stream, void* wait_event, void* signal_event) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (layer < 0 || layer >= s->desc.n_layers) return fail(MS_EINVAL, "layer %d out of range", layer);
+    if (!h_kv || !d_slot) return fail(MS_EINVAL, "h_kv or slot is NULL");
+    if (!aligned16(h_kv) || !aligned16(d_slot)) return fail(MS_EALIGN, "h_kv / slot not 16-byte aligned");
+    ms_status st = check_pinned(h_kv);
+    if (st != MS_OK) return st;
+    st = prefetch_signal(s, h_kv, d_slot, static_cast<hipStream_t>(copy_stream),
+                         static_cast<hipEvent_t>(wait_event), static_cast<hipEvent_t>(signal_event));
+    return st == MS_OK ? ok() : st;
+}
+
+ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* d_x,
+                             const void* d_ycache, const ms_kv_source* kv, void* d_y,
+                             void* compute_stream, void* copy_stream) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (!w || !d_x || !kv || !d_y) return fail(MS_EINVAL, "NULL argument");
+    if (!d_ycache && !s->all_masked) return fail(MS_EINVAL, "y_cache may be NULL only when every token is masked");
+    if (kv->kind != MS_KV_DEVICE && kv->kind != MS_KV_HOST_PINNED) return fail(MS_EINVAL, "unknown kv kind %d", kv->kind);
+    if (!kv->layer) return fail(MS_EINVAL, "kv->layer is NULL");
+    const int L = s->desc.n_layers;
+    const int nsets = (s->desc.dual_stream && s->desc.n_text > 0) ? 2 : 1;
+    const int wstride = s->desc.dual_stream ? 2 : 1;
+    for (int l = 0; l < L; ++l) {
+        if (!kv->layer[l]) return fail(MS_EINVAL, "kv->layer[%d] is NULL", l);
+        if (!aligned16(kv->layer[l])) return fail(MS_EALIGN, "kv->layer[%d] not 16-byte aligned", l);
+        ms_status st = check_weights(s, w + (size_t)l * wstride);
+        if (st != MS_OK) return st;
+    }
+    (void)nsets;
+    const bool pinned = kv->kind == MS_KV_HOST_PINNED;
+    if (pinned) {
+        for (int i = 0; i < 2; ++i) {
+            if (!kv->slot[i] && (i == 0 || L > 1)) return fail(MS_EINVAL, "kv->slot[%d] is NULL", i);
+            if (kv->slot[i] && !aligned16(kv->slot[i])) return fail(MS_EALIGN, "kv->slot[%d] not aligned", i);
+        }
+        if (!s->all_masked && s->M > 0) {
+            ms_status st = check_pinned(kv->layer[0]);
+            if (st != MS_OK) return st;
+        }
+    }
+    if (!aligned16(d_x) || !aligned16(d_y) || !aligned16(d_ycache)) return fail(MS_EALIGN, "pointer not 16-byte aligned");
+
+    hipStream_t cs = static_cast<hipStream_t>(compute_stream);
+    hipStream_t ps = static_cast<hipStream_t>(copy_stream);
+    void* xm = s->buf(s->lay.xm);
+    if (s->M > 0) {
+        {
+            ProfScope p(MS_K_GATHER, cs);
+            MS_HIP(ms::launch_gather(d_x, s->rows(), xm, s->M, s->d * s->elt, cs));
+        }
+        const bool stream_cache = pinned && !s->all_masked;
+        const bool serialize = stream_cache && (env_flag("MS_SERIALIZE") || ps == cs);
+        if (stream_cache && !serialize) {
+            // the copy stream must not overwrite a slot an earlier call still reads
+            MS_HIP(hipEventRecord(s->ev_start, cs));
+            MS_HIP(hipStreamWaitEvent(ps, s->ev_start, 0));
+            for (int l = 0; l < std::min(L, 2); ++l) {
+                ms_status st = prefetch_signal(s, kv->layer[l], kv->slot[l], ps, nullptr, s->ev_copied[l]);
+                if (st != MS_OK) return st;
+            }
+        }
+        for (int l = 0; l < L; ++l) {
+            void* kvbuf = const_cast<void*>(kv->layer[l]);
+            if (pinned) {
+                kvbuf = kv->slot[l % 2];
+                if (serialize) {
+                    ms_status st = prefetch(s, kv->layer[l], kvbuf, cs, nullptr);
+                    if (st != MS_OK) return st;
+                } else if (stream_cache) {
+                    MS_HIP(hipStreamWaitEvent(cs, s->ev_copied[l % 2], 0));
+                }
+            }
+            ms_status st = block_forward(s, w + (size_t)l * wstride, xm, kvbuf, cs);
+            if (st != MS_OK) return st;
+            if (stream_cache && !serialize && l + 2 < L) {
+                MS_HIP(hipEventRecord(s->ev_consumed[l % 2], cs));
+                st = prefetch_signal(s, kv->layer[l + 2], kv->slot[l % 2], ps, s->ev_consumed[l % 2],
+                                     s->ev_copied[l % 2]);
+                if (st != MS_OK) return st;
+            }
+        }
+    }
+    {
+        ProfScope p(MS_K_SCATTER, cs);
+        MS_HIP(ms::launch_scatter(xm, s->rows(), s->inv(), d_ycache, d_y, s->M, s->B * s->T,
+                                  s->d * s->elt, cs));
+    }
+    return ok();
+}
+
+void mask_step_destroy(ms_step* s) {
+    if (!s) return;
+    destroy_events(s);
+    delete s;
+}
+
+ms_status mask_profiler_start(uint32_t class_mask, int32_t capacity) {
+    if (capacity < 1 || capacity > (1 << 20)) return fail(MS_EINVAL, "capacity must be in 1..2^20");
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    while ((int)g_prof.pool.size() < 2 * capacity) {
+        hipEvent_t e;
+        hipError_t r = hipEventCreate(&e);
+        if (r != hipSuccess) return fail(MS_EHIP, "hipEventCreate: %s", hipGetErrorString(r));
+        g_prof.pool.push_back(e);
+    }
+    g_prof.cls.assign(capacity, 0);
+    g_prof.capacity = capacity;
+    g_prof.used = 0;
+    g_prof.dropped = 0;
+    g_prof.mask = class_mask;
+    g_prof.on.store(true);
+    return ok();
+}
+
+ms_status mask_profiler_stop(double* total_ms, int64_t* launches, int64_t* dropped) {
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    g_prof.on.store(false);
+    std::vector<double> tot(MS_K_COUNT, 0.0);
+    std::vector<int64_t> cnt(MS_K_COUNT, 0);
+    for (int i = 0; i < g_prof.used; ++i) {
+        MS_HIP(hipEventSynchronize(g_prof.pool[2 * i + 1]));
+        float ms = 0.f;
+        MS_HIP(hipEventElapsedTime(&ms, g_prof.pool[2 * i], g_prof.pool[2 * i + 1]));
+        tot[g_prof.cls[i]] += ms;
+        cnt[g_prof.cls[i]] += 1;
+    }
+    for (int c = 0; c < MS_K_COUNT; ++c) {
+        if (total_ms) total_ms[c] = tot[c];
+        if (launches) launches[c] = cnt[c];
+    }
+    if (dropped) *dropped = g_prof.dropped;
+    g_prof.used = 0;
+    return ok();
+}
+
+}  // extern "C"

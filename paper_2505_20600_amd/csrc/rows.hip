@@ -1,0 +1,177 @@
+// Token-wise row kernels: gather of the masked rows, the final scatter into the
+// cached hidden state (Sec. 3.1: extract the masked tokens, replenish the
+// unmasked ones from the cache) and LayerNorm over packed rows.
+//
+// Gather and scatter are pure HBM copies: 16-byte vector loads/stores, one
+// row chunk per thread, grid-stride so that any M fills the chip.
+#include "common.h"
+#include "kernels.h"
+
+namespace ms {
+namespace {
+
+constexpr int kCopyThreads = 256;
+
+__global__ __launch_bounds__(kCopyThreads) void gather_kernel(
+    const uint8_t* __restrict__ x, const int32_t* __restrict__ rows, uint8_t* __restrict__ xm,
+    long total, int row_vecs) {
+    const long stride = (long)gridDim.x * blockDim.x;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const long m = i / row_vecs;
+        const int c = (int)(i - m * row_vecs);
+        const long src = (long)rows[m] * row_vecs + c;
+        st16(xm + (m * row_vecs + c) * 16, ld16(x + src * 16));
+    }
+}
+
+// Aliased output: only the recomputed rows change.
+__global__ __launch_bounds__(kCopyThreads) void scatter_masked_kernel(
+    const uint8_t* __restrict__ xm, const int32_t* __restrict__ rows, uint8_t* __restrict__ y,
+    long total, int row_vecs) {
+    const long stride = (long)gridDim.x * blockDim.x;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const long m = i / row_vecs;
+        const int c = (int)(i - m * row_vecs);
+        const long dst = (long)rows[m] * row_vecs + c;
+        st16(y + dst * 16, ld16(xm + (m * row_vecs + c) * 16));
+    }
+}
+
+// Separate output: every row of y is written once, from xm or from the cache.
+__global__ __launch_bounds__(kCopyThreads) void merge_kernel(
+    const uint8_t* __restrict__ xm, const int32_t* __restrict__ inv,
+    const uint8_t* __restrict__ ycache, uint8_t* __restrict__ y, long total, int row_vecs) {
+    const long stride = (long)gridDim.x * blockDim.x;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const long r = i / row_vecs;
+        const int c = (int)(i - r * row_vecs);
+        const int m = inv[r];
+        const uint8_t* src = m >= 0 ? xm + ((long)m * row_vecs + c) * 16 : ycache + i * 16;
+        st16(y + i * 16, ld16(src));
+    }
+}
+
+int copy_grid(long total) {
+    long blocks = (total + kCopyThreads - 1) / kCopyThreads;
+    if (blocks > 256 * 16) blocks = 256 * 16;
+    return blocks < 1 ? 1 : (int)blocks;
+}
+
+// LayerNorm: one wave per row, the row held in registers (two-pass mean and
+// variance in float32), 16-byte vectors.
+constexpr int kLnWaves = 4;
+constexpr int kLnMaxVecPerLane = 8;
+
+template <typename T>
+__global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
+    const T* __restrict__ x, const T* __restrict__ g0, const T* __restrict__ b0,
+    const T* __restrict__ g1, const T* __restrict__ b1, int m_split, T* __restrict__ y, int M,
+    int d, float eps) {
+    constexpr int V = 16 / sizeof(T);   // elements per 16-byte vector
+    const int lane = threadIdx.x % kWave;
+    const int row = blockIdx.x * kLnWaves + threadIdx.x / kWave;
+    if (row >= M) return;
+    const T* gam = row < m_split ? g1 : g0;
+    const T* bet = row < m_split ? b1 : b0;
+    const int nvec = d / V;
+    const T* xr = x + (long)row * d;
+    float v[kLnMaxVecPerLane][V];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+        const int c = lane + i * kWave;
+        if (c < nvec) {
+#pragma unroll
+            for (int e = 0; e < V; e += 4) load4<T>(xr + c * V + e, &v[i][e]);
+#pragma unroll
+            for (int e = 0; e < V; ++e) s += v[i][e];
+        }
+    }
+    const float mean = wave_sum(s) / d;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+        const int c = lane + i * kWave;
+        if (c < nvec) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                const float t = v[i][e] - mean;
+                q += t * t;
+            }
+        }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(q) / d + eps);
+    T* yr = y + (long)row * d;
+#pragma unroll
+    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+        const int c = lane + i * kWave;
+        if (c < nvec) {
+#pragma unroll
+            for (int e = 0; e < V; e += 4) {
+                float gg[4], bb[4], o[4];
+                load4<T>(gam + c * V + e, gg);
+                load4<T>(bet + c * V + e, bb);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) o[k] = (v[i][e + k] - mean) * rstd * gg[k] + bb[k];
+                store4<T>(yr + c * V + e, o);
+            }
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_gather(const void* x, const int32_t* rows, void* xm, int M, int row_bytes,
+                         hipStream_t s) {
+    if (M == 0) return hipSuccess;
+    const int row_vecs = row_bytes / 16;
+    const long total = (long)M * row_vecs;
+    hipLaunchKernelGGL(gather_kernel, dim3(copy_grid(total)), dim3(kCopyThreads), 0, s,
+                       static_cast<const uint8_t*>(x), rows, static_cast<uint8_t*>(xm), total,
+                       row_vecs);
+    return hipGetLastError();
+}
+
+hipError_t launch_scatter(const void* xm, const int32_t* rows, const int32_t* inv,
+                          const void* ycache, void* y, int M, int total_rows, int row_bytes,
+                          hipStream_t s) {
+    const int row_vecs = row_bytes / 16;
+    if (y == ycache) {
+        if (M == 0) return hipSuccess;
+        const long total = (long)M * row_vecs;
+        hipLaunchKernelGGL(scatter_masked_kernel, dim3(copy_grid(total)), dim3(kCopyThreads), 0,
+                           s, static_cast<const uint8_t*>(xm), rows, static_cast<uint8_t*>(y),
+                           total, row_vecs);
+    } else {
+        const long total = (long)total_rows * row_vecs;
+        if (total == 0) return hipSuccess;
+        hipLaunchKernelGGL(merge_kernel, dim3(copy_grid(total)), dim3(kCopyThreads), 0, s,
+                           static_cast<const uint8_t*>(xm), inv,
+                           static_cast<const uint8_t*>(ycache), static_cast<uint8_t*>(y), total,
+                           row_vecs);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_layernorm(int dtype, const void* x, const void* g0, const void* b0,
+                            const void* g1, const void* b1, int m_split, void* y, int M, int d,
+                            float eps, hipStream_t s) {
+    if (M == 0) return hipSuccess;
+    dim3 grid((M + kLnWaves - 1) / kLnWaves), block(kLnWaves * kWave);
+    if (dtype == kBF16) {
+        hipLaunchKernelGGL(layernorm_kernel<bf16_t>, grid, block, 0, s,
+                           static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(g0),
+                           static_cast<const bf16_t*>(b0), static_cast<const bf16_t*>(g1),
+                           static_cast<const bf16_t*>(b1), m_split, static_cast<bf16_t*>(y), M, d,
+                           eps);
+    } else {
+        hipLaunchKernelGGL(layernorm_kernel<float>, grid, block, 0, s,
+                           static_cast<const float*>(x), static_cast<const float*>(g0),
+                           static_cast<const float*>(b0), static_cast<const float*>(g1),
+                           static_cast<const float*>(b1), m_split, static_cast<float*>(y), M, d,
+                           eps);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace ms

@@ -1,0 +1,248 @@
+"""Thin ctypes binding of ``libmaskstep.so`` (the C ABI in ``include/maskstep.h``).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels. Torch tensors are passed by device pointer, streams by their HIP
+handle. Loading fails loudly when the library has not been built; there is no
+fallback of any kind.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch  # loads torch's HIP runtime first, so the library binds to the same one
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmaskstep.so")
+
+MS_OK, MS_EINVAL, MS_ESHAPE, MS_EDTYPE, MS_EALIGN, MS_ENOTPINNED, MS_EWORKSPACE, MS_ESTATE, MS_EHIP = range(9)
+MS_FP32, MS_BF16 = 0, 1
+MS_KV_DEVICE, MS_KV_HOST_PINNED = 0, 1
+
+STATUS_NAMES = {0: "MS_OK", 1: "MS_EINVAL", 2: "MS_ESHAPE", 3: "MS_EDTYPE", 4: "MS_EALIGN",
+                5: "MS_ENOTPINNED", 6: "MS_EWORKSPACE", 7: "MS_ESTATE", 8: "MS_EHIP"}
+
+
+class ModelDesc(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("mlp_mult", C.c_int32), ("grid_h", C.c_int32), ("grid_w", C.c_int32),
+                ("n_text", C.c_int32), ("dual_stream", C.c_int32), ("max_batch", C.c_int32),
+                ("dtype", C.c_int32), ("ln_eps", C.c_float)]
+
+
+WEIGHT_FIELDS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
+                 "ln2_g", "ln2_b", "w_1", "b_1", "w_2", "b_2")
+
+
+class LayerWeights(C.Structure):
+    _fields_ = [(k, C.c_void_p) for k in WEIGHT_FIELDS]
+
+
+class KVSource(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("layer", C.POINTER(C.c_void_p)), ("slot", C.c_void_p * 2)]
+
+
+class StepInfo(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("rows", C.c_int32), ("n_segments", C.c_int32),
+                ("n_qtiles", C.c_int32), ("text_rows", C.c_int32)]
+
+
+class MaskStepError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def load() -> C.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with paper_2505_20600_amd.build.build()")
+        lib = C.CDLL(LIB_PATH)
+        vp, i32, sz = C.c_void_p, C.c_int32, C.c_size_t
+        sig = {
+            "mask_abi_version": (i32, []),
+            "mask_last_error": (C.c_char_p, []),
+            "mask_workspace_bytes": (sz, [C.POINTER(ModelDesc), i32]),
+            "mask_step_init": (i32, [C.POINTER(vp), C.POINTER(ModelDesc), i32, vp, vp, sz, vp]),
+            "mask_step_get_info": (i32, [vp, C.POINTER(StepInfo)]),
+            "mask_step_index": (i32, [vp, C.POINTER(vp), C.POINTER(vp), C.POINTER(vp)]),
+            "mask_gather_rows": (i32, [vp, vp, vp, vp]),
+            "mask_block_forward": (i32, [vp, i32, C.POINTER(LayerWeights), vp, vp, vp]),
+            "mask_scatter_rows": (i32, [vp, vp, vp, vp, vp]),
+            "cache_prefetch_layer": (i32, [vp, i32, vp, vp, vp, vp, vp]),
+            "mask_stack_forward": (i32, [vp, C.POINTER(LayerWeights), vp, vp, C.POINTER(KVSource),
+                                         vp, vp, vp]),
+            "mask_step_destroy": (None, [vp]),
+            "mask_profiler_start": (i32, [C.c_uint32, i32]),
+            "mask_profiler_stop": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask_step_init",
+            "mask_step_get_info", "mask_step_index", "mask_gather_rows", "mask_block_forward",
+            "mask_scatter_rows", "cache_prefetch_layer", "mask_stack_forward", "mask_step_destroy",
+            "mask_profiler_start", "mask_profiler_stop")
+
+KERNEL_CLASSES = ("compact", "gather", "layernorm", "gemm_qkv", "attention", "gemm_out", "gemm_up",
+                  "gemm_down", "scatter", "copy")
+
+
+def profiler_start(classes=KERNEL_CLASSES, capacity: int = 65536):
+    mask = 0
+    for c in classes:
+        mask |= 1 << KERNEL_CLASSES.index(c)
+    _check(load().mask_profiler_start(mask, capacity))
+
+
+def profiler_stop() -> dict:
+    """{class: (total_ms, launches)} of the launches recorded since profiler_start()."""
+    n = len(KERNEL_CLASSES)
+    ms = (C.c_double * n)()
+    cnt = (C.c_int64 * n)()
+    dropped = C.c_int64()
+    _check(load().mask_profiler_stop(ms, cnt, C.byref(dropped)))
+    out = {c: (ms[i], cnt[i]) for i, c in enumerate(KERNEL_CLASSES) if cnt[i]}
+    out["_dropped"] = dropped.value
+    return out
+
+
+def _check(status: int):
+    if status != MS_OK:
+        raise MaskStepError(status, load().mask_last_error().decode())
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(s) -> int | None:
+    if s is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def model_desc(shape, max_batch: int | None = None) -> ModelDesc:
+    """ModelDesc from an object with the ModelShape fields."""
+    return ModelDesc(shape.n_layers, shape.d_model, shape.n_heads, shape.mlp_mult, shape.grid_h,
+                     shape.grid_w, shape.n_text, 1 if shape.dual_stream else 0,
+                     max_batch if max_batch is not None else max(1, shape.batch),
+                     MS_BF16 if shape.dtype == "bf16" else MS_FP32, shape.ln_eps)
+
+
+def mask_workspace_bytes(desc: ModelDesc, batch: int) -> int:
+    n = load().mask_workspace_bytes(C.byref(desc), batch)
+    if n == 0:
+        raise MaskStepError(MS_ESHAPE, load().mask_last_error().decode())
+    return n
+
+
+def layer_weights_struct(w: dict) -> LayerWeights:
+    return LayerWeights(*[_ptr(w[k]) for k in WEIGHT_FIELDS])
+
+
+def weights_array(layers) -> C.Array:
+    """[L] (or [L][2] image, text) weight dicts of device tensors -> a C array of structs."""
+    flat = []
+    for w in layers:
+        if isinstance(w, (tuple, list)):
+            flat.extend(w)
+        else:
+            flat.append(w)
+    arr = (LayerWeights * len(flat))(*[layer_weights_struct(w) for w in flat])
+    return arr
+
+
+class MaskStep:
+    """One step context (mask set): wraps mask_step_init ... mask_step_destroy."""
+
+    def __init__(self, desc: ModelDesc, batch: int, d_mask: torch.Tensor, workspace: torch.Tensor,
+                 stream=None):
+        self._lib = load()
+        self.desc = desc
+        self.batch = batch
+        self.workspace = workspace
+        self.mask = d_mask
+        h = C.c_void_p()
+        _check(self._lib.mask_step_init(C.byref(h), C.byref(desc), batch, _ptr(d_mask), _ptr(workspace),
+                                        workspace.numel() * workspace.element_size(), _stream(stream)))
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            self._lib.mask_step_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def info(self) -> StepInfo:
+        info = StepInfo()
+        _check(self._lib.mask_step_get_info(self.handle, C.byref(info)))
+        return info
+
+    def index_views(self):
+        """(rows [M], inv [B*T], seg_start [n_seg+1]) as int32 views into the workspace."""
+        r, i, s = C.c_void_p(), C.c_void_p(), C.c_void_p()
+        _check(self._lib.mask_step_index(self.handle, C.byref(r), C.byref(i), C.byref(s)))
+        info = self.info()
+        T = self.desc.n_text + self.desc.grid_h * self.desc.grid_w
+        base = self.workspace.data_ptr()
+        ws8 = self.workspace.view(torch.uint8)
+
+        def view(p, n):
+            off = p - base
+            return ws8[off:off + 4 * n].view(torch.int32)
+
+        return view(r.value, info.rows), view(i.value, self.batch * T), view(s.value, info.n_segments + 1)
+
+    def gather_rows(self, x, xm=None, stream=None):
+        _check(self._lib.mask_gather_rows(self.handle, _ptr(x), _ptr(xm), _stream(stream)))
+
+    def block_forward(self, layer: int, weights, xm, kv, stream=None):
+        arr = weights_array([weights])
+        _check(self._lib.mask_block_forward(self.handle, layer, arr, _ptr(xm), _ptr(kv), _stream(stream)))
+
+    def scatter_rows(self, xm, ycache, y, stream=None):
+        _check(self._lib.mask_scatter_rows(self.handle, _ptr(xm), _ptr(ycache), _ptr(y), _stream(stream)))
+
+    def prefetch_layer(self, layer: int, h_kv, d_slot, copy_stream, wait_event=None, signal_event=None):
+        ev = lambda e: None if e is None else (e if isinstance(e, int) else e.cuda_event)
+        _check(self._lib.cache_prefetch_layer(self.handle, layer, _ptr(h_kv), _ptr(d_slot),
+                                              _stream(copy_stream), ev(wait_event), ev(signal_event)))
+
+    def stack_forward(self, weights_c, x, ycache, kv_layers, y, *, pinned: bool = False, slots=(None, None),
+                      stream=None, copy_stream=None):
+        """``weights_c`` from weights_array(); ``kv_layers``: [L] tensors (device or pinned host)."""
+        L = len(kv_layers)
+        ptrs = (C.c_void_p * L)(*[_ptr(t) for t in kv_layers])
+        src = KVSource(MS_KV_HOST_PINNED if pinned else MS_KV_DEVICE, C.cast(ptrs, C.POINTER(C.c_void_p)),
+                       (C.c_void_p * 2)(_ptr(slots[0]), _ptr(slots[1])))
+        cs = _stream(stream)
+        ps = _stream(copy_stream) if copy_stream is not None else cs
+        _check(self._lib.mask_stack_forward(self.handle, weights_c, _ptr(x), _ptr(ycache), C.byref(src),
+                                            _ptr(y), cs, ps))

@@ -1,0 +1,112 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function the
+headers declare, and rejects bad arguments before touching a device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2505_20600_amd import maskstep as MS
+from paper_2505_20600_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if not fn.endswith(".h"):
+            continue
+        src = open(os.path.join(ROOT, "include", fn)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        for m in re.finditer(r"^[A-Za-z_][\w \*]*?\b([a-z_][a-z0-9_]*)\s*\(", src, flags=re.M):
+            if m.group(1) not in ("if", "while", "for", "return", "sizeof"):
+                names.add(m.group(1))
+    return names
+
+
+def test_library_exports_every_declared_function():
+    lib = MS.load()
+    declared = _declared_functions()
+    assert {"mask_step_init", "mask_block_forward", "mask_stack_forward", "cache_prefetch_layer"} <= declared
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert set(MS.EXPORTED) == declared
+
+
+def test_abi_version():
+    assert MS.load().mask_abi_version() == 1
+
+
+def _desc(**kw):
+    d = MS.model_desc(W.CONFIGS["c2"])
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+def test_workspace_bytes_scales_with_batch_and_rejects_bad_shapes():
+    lib = MS.load()
+    n1 = MS.mask_workspace_bytes(_desc(max_batch=4), 1)
+    n4 = MS.mask_workspace_bytes(_desc(max_batch=4), 4)
+    assert n4 > 3 * n1 > 0
+    # c2: six [T][d] bf16 activation buffers + [T][4d], plus indices
+    T, d = 4096, 768
+    assert n1 >= T * d * 2 * 5 + T * 4 * d * 2
+    bad = [
+        dict(d_model=100), dict(n_heads=5), dict(d_model=768, n_heads=4),   # head_dim 192
+        dict(dtype=7), dict(n_layers=0), dict(grid_h=0), dict(max_batch=0), dict(max_batch=65),
+        dict(mlp_mult=0), dict(dual_stream=3), dict(n_text=-1), dict(ln_eps=float("nan")),
+    ]
+    for kw in bad:
+        assert lib.mask_workspace_bytes(C.byref(_desc(**kw)), 1) == 0, kw
+        assert lib.mask_last_error()
+    assert lib.mask_workspace_bytes(C.byref(_desc(max_batch=2)), 3) == 0
+    assert lib.mask_workspace_bytes(None, 1) == 0
+
+
+def test_fp32_limits():
+    lib = MS.load()
+    d = MS.model_desc(W.CONFIGS["c1"])
+    assert lib.mask_workspace_bytes(C.byref(d), 1) > 0
+    d.n_heads = 2  # head_dim 128 in fp32: not supported
+    assert lib.mask_workspace_bytes(C.byref(d), 1) == 0
+
+
+def test_step_init_validates_before_any_device_work():
+    lib = MS.load()
+    desc = _desc()
+    h = C.c_void_p()
+    ws = 1 << 12
+    cases = [
+        ((None, C.byref(desc), 1, 16, 16, ws, None), MS.MS_EINVAL),
+        ((C.byref(h), None, 1, 16, 16, ws, None), MS.MS_EINVAL),
+        ((C.byref(h), C.byref(desc), 0, 16, 16, ws, None), MS.MS_ESHAPE),
+        ((C.byref(h), C.byref(desc), 1, None, 16, ws, None), MS.MS_EINVAL),
+        ((C.byref(h), C.byref(desc), 1, 16, None, ws, None), MS.MS_EINVAL),
+        ((C.byref(h), C.byref(desc), 1, 16, 24, ws, None), MS.MS_EALIGN),
+        ((C.byref(h), C.byref(desc), 1, 16, 16, ws, None), MS.MS_EWORKSPACE),
+    ]
+    for args, want in cases:
+        assert lib.mask_step_init(*args) == want, (args, lib.mask_last_error())
+        assert h.value is None
+
+
+def test_calls_without_a_step_context_fail_cleanly():
+    lib = MS.load()
+    assert lib.mask_gather_rows(None, 16, 16, None) == MS.MS_ESTATE
+    assert lib.mask_block_forward(None, 0, None, 16, 16, None) == MS.MS_ESTATE
+    assert lib.mask_scatter_rows(None, 16, 16, 16, None) == MS.MS_ESTATE
+    assert lib.cache_prefetch_layer(None, 0, 16, 16, None, None, None) == MS.MS_ESTATE
+    assert lib.mask_stack_forward(None, None, 16, 16, None, 16, None, None) == MS.MS_ESTATE
+    info = MS.StepInfo()
+    assert lib.mask_step_get_info(None, C.byref(info)) == MS.MS_EINVAL
+    lib.mask_step_destroy(None)  # no-op
+
+
+def test_error_message_is_per_call():
+    lib = MS.load()
+    assert lib.mask_workspace_bytes(C.byref(_desc(d_model=100)), 1) == 0
+    assert b"d_model" in lib.mask_last_error()
+    assert lib.mask_workspace_bytes(C.byref(_desc()), 1) > 0
+    assert lib.mask_last_error() == b""
