@@ -272,9 +272,8 @@ def main():
             "layernorm": ("hbm", 2.0 * 2 * m_sum * d * e),
             "gather": ("hbm", 2.0 * tot_m_prof * d * e),
         }
+        prof.pop("_dropped", None)
         for c, (t_ms, n) in prof.items():
-            if c.startswith("_"):
-                continue
             kernels[c] = {"ms_total": round(t_ms, 4), "launches": n, "us_avg": round(1e3 * t_ms / max(n, 1), 3)}
             if c in work:
                 kind, amount = work[c]

@@ -208,12 +208,355 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnDesc a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 kernel for head_dim 64 / 72 / 128.
+//
+// Workgroup = 128 packed query rows of one segment x one head x one key range;
+// each wave owns 32 queries (two 16-query MFMA column blocks), so every K and
+// V fragment read from LDS feeds two MFMAs. The next 64-key K/V tile is
+// fetched into registers while the current one is computed. V is written to
+// LDS transposed, four keys per 8-byte store. head_dim 72 runs its QK^T
+// contraction as two 32-deep steps plus one zero-padded 16-deep step.
+// Softmax: the scale is folded into one FMA before exp2, probabilities are
+// packed to bf16 by the hardware converter.
+// ---------------------------------------------------------------------------
+
+template <int HD>
+struct FastCfg {
+    static constexpr int NK32 = HD / 32;                  // 32-deep QK^T steps
+    static constexpr bool K16 = (HD % 32) != 0;           // one extra 16-deep step
+    static constexpr int HDQ = NK32 * 32 + (K16 ? 16 : 0);
+    static constexpr int NHS = (HD + 15) / 16;            // 16-row subtiles of O^T
+    static constexpr int HDV = NHS * 16;
+    static constexpr int KL = HDQ + 8;                    // K row stride in LDS (elements)
+    static constexpr int VL = kKeyTile + 4;               // V^T row stride in LDS (elements)
+    static constexpr int CH = HD / 8;                     // 16-byte chunks per key row
+    static constexpr int KITEMS = kKeyTile * CH;
+    static constexpr int VITEMS = (kKeyTile / 4) * CH;    // 4-key groups x chunks
+    static constexpr int KPT = (KITEMS + 127) / 128;
+    static constexpr int VPT = (VITEMS + 127) / 128;
+    static constexpr int NPRE = KPT > 4 * VPT ? KPT : 4 * VPT;
+    static_assert(HD % 8 == 0 && HD % 32 <= 16, "head_dim layout");
+};
+
+__device__ __forceinline__ f32x4_t mfma32(bf16x8_t a, bf16x8_t b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mfma16(bf16x4_t a, bf16x4_t b, f32x4_t c) {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s4, a), __builtin_bit_cast(s4, b), c, 0, 0, 0);
+}
+
+template <int HD>
+__global__ __launch_bounds__(kThreads) void attention_fast_kernel(AttnDesc a) {
+    using C = FastCfg<HD>;
+    __shared__ __attribute__((aligned(16))) bf16_t sK[kKeyTile * C::KL];
+    __shared__ __attribute__((aligned(16))) bf16_t sVt[C::HDV * C::VL];
+
+    const int tid = threadIdx.x;
+    const int lane = tid % kWave;
+    const int wave = tid / kWave;
+    const int grp = lane / 16;
+    const int l16 = lane % 16;
+    const int head = blockIdx.y;
+    const int split = blockIdx.z;
+    const int T_ = a.T, d = a.d;
+
+    // query tile -> segment (128-row tiles counted per segment)
+    int tile = blockIdx.x, seg = 0, row0 = 0, row_end = 0;
+    for (; seg < a.nseg; ++seg) {
+        const int r0 = a.seg_start[seg], r1 = a.seg_start[seg + 1];
+        const int nt = (r1 - r0 + kFastQTile - 1) / kFastQTile;
+        if (tile < nt) { row0 = r0 + tile * kFastQTile; row_end = r1; break; }
+        tile -= nt;
+    }
+    if (seg >= a.nseg) return;   // grid larger than the tile count: nothing to do
+    const int b = a.seg_req[seg];
+    const bf16_t* __restrict__ kvb = static_cast<const bf16_t*>(a.kv) + (long)b * T_ * 2 * d + head * HD;
+
+    const int ntiles_all = (T_ + kKeyTile - 1) / kKeyTile;
+    const int kt0 = split * a.tiles_per_split;
+    const int kt1 = min(ntiles_all, kt0 + a.tiles_per_split);
+
+    if constexpr (C::HDQ > HD) {
+        for (int i = tid; i < kKeyTile * (C::HDQ - HD); i += kThreads)
+            sK[(i / (C::HDQ - HD)) * C::KL + HD + i % (C::HDQ - HD)] = 0;
+    }
+    if constexpr (C::HDV > HD) {
+        for (int i = tid; i < (C::HDV - HD) * C::VL; i += kThreads) sVt[HD * C::VL + i] = 0;
+    }
+
+    // Q^T fragments (B operand): query column l16 of block qb, head_dim slots by lane group
+    bf16x8_t qf[2][C::NK32 > 0 ? C::NK32 : 1];
+    bf16x4_t qf16[2];
+    const bf16_t* __restrict__ q = static_cast<const bf16_t*>(a.q);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const int qrow = row0 + wave * 32 + qb * 16 + l16;
+        const bool valid = qrow < row_end;
+        const bf16_t* qp = q + (long)qrow * d + head * HD;
+#pragma unroll
+        for (int kc = 0; kc < C::NK32; ++kc) {
+            vec16 v = {{0u, 0u, 0u, 0u}};
+            if (valid) v = ld16(qp + kc * 32 + grp * 8);
+            qf[qb][kc] = __builtin_bit_cast(bf16x8_t, v);
+        }
+        if constexpr (C::K16) {
+            const int k = C::NK32 * 32 + grp * 4;
+            uint2 v = make_uint2(0u, 0u);
+            if (valid && k < HD) v = *reinterpret_cast<const uint2*>(qp + k);
+            qf16[qb] = __builtin_bit_cast(bf16x4_t, v);
+        }
+    }
+
+    f32x4_t oacc[2][C::NHS];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int h = 0; h < C::NHS; ++h) oacc[qb][h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    const float cs = a.scale_log2;
+
+    // waves 0-1 stage V (transposed), waves 2-3 stage K
+    const bool vrole = tid < 128;
+    const int rt = tid % 128;
+    vec16 pre[C::NPRE];
+    auto gload = [&](int kt) {
+        const int k0 = kt * kKeyTile;
+        if (vrole) {
+#pragma unroll
+            for (int j = 0; j < C::VPT; ++j) {
+                const int item = rt + j * 128;
+                if (item < C::VITEMS) {
+                    const int kg = item / C::CH, c = item % C::CH;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int t = k0 + kg * 4 + e;
+                        vec16 v = {{0u, 0u, 0u, 0u}};
+                        if (t < T_) v = ld16(kvb + (long)t * 2 * d + d + c * 8);
+                        pre[j * 4 + e] = v;
+                    }
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < C::KPT; ++j) {
+                const int item = rt + j * 128;
+                if (item < C::KITEMS) {
+                    const int key = item / C::CH, c = item % C::CH;
+                    const int t = k0 + key;
+                    vec16 v = {{0u, 0u, 0u, 0u}};
+                    if (t < T_) v = ld16(kvb + (long)t * 2 * d + c * 8);
+                    pre[j] = v;
+                }
+            }
+        }
+    };
+    auto sstore = [&]() {
+        if (vrole) {
+#pragma unroll
+            for (int j = 0; j < C::VPT; ++j) {
+                const int item = rt + j * 128;
+                if (item < C::VITEMS) {
+                    const int kg = item / C::CH, c = item % C::CH;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int sh = (e & 1) * 16;
+                        const uint32_t k0 = (pre[j * 4 + 0].w[e >> 1] >> sh) & 0xffffu;
+                        const uint32_t k1 = (pre[j * 4 + 1].w[e >> 1] >> sh) & 0xffffu;
+                        const uint32_t k2 = (pre[j * 4 + 2].w[e >> 1] >> sh) & 0xffffu;
+                        const uint32_t k3 = (pre[j * 4 + 3].w[e >> 1] >> sh) & 0xffffu;
+                        *reinterpret_cast<uint2*>(&sVt[(c * 8 + e) * C::VL + kg * 4]) =
+                            make_uint2(k0 | (k1 << 16), k2 | (k3 << 16));
+                    }
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < C::KPT; ++j) {
+                const int item = rt + j * 128;
+                if (item < C::KITEMS) {
+                    const int key = item / C::CH, c = item % C::CH;
+                    st16(&sK[key * C::KL + c * 8], pre[j]);
+                }
+            }
+        }
+    };
+
+    if (kt0 < kt1) gload(kt0);
+    for (int kt = kt0; kt < kt1; ++kt) {
+        __syncthreads();
+        sstore();
+        __syncthreads();
+        if (kt + 1 < kt1) gload(kt + 1);
+
+        // S^T = K Q^T: keys ks*16 + 4*grp + r, query l16 of block qb
+        f32x4_t sacc[2][4];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) sacc[qb][ks] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const bf16_t* kr = &sK[(ks * 16 + l16) * C::KL];
+#pragma unroll
+            for (int kc = 0; kc < C::NK32; ++kc) {
+                const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(kr + kc * 32 + grp * 8);
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) sacc[qb][ks] = mfma32(kf, qf[qb][kc], sacc[qb][ks]);
+            }
+            if constexpr (C::K16) {
+                const bf16x4_t kf = *reinterpret_cast<const bf16x4_t*>(kr + C::NK32 * 32 + grp * 4);
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) sacc[qb][ks] = mfma16(kf, qf16[qb], sacc[qb][ks]);
+            }
+        }
+
+        const int k0 = kt * kKeyTile;
+        const bool tail = k0 + kKeyTile > T_;
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            if (tail) {
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (k0 + ks * 16 + grp * 4 + r >= T_) sacc[qb][ks][r] = -INFINITY;
+            }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+                mx = fmaxf(fmaxf(mx, fmaxf(sacc[qb][ks][0], sacc[qb][ks][1])), fmaxf(sacc[qb][ks][2], sacc[qb][ks][3]));
+            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+            const float m_new = fmaxf(m_run[qb], mx);
+            const float corr = exp2f((m_run[qb] - m_new) * cs);
+            const float mc = m_new * cs;
+            float psum = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float p = exp2f(fmaf(sacc[qb][ks][r], cs, -mc));
+                    sacc[qb][ks][r] = p;
+                    psum += p;
+                }
+            l_run[qb] = l_run[qb] * corr + psum;
+            m_run[qb] = m_new;
+#pragma unroll
+            for (int h = 0; h < C::NHS; ++h) oacc[qb][h] *= corr;
+        }
+
+        // O^T += V^T P^T; K-slots 0..3 = keys 32c + 4*grp + r, slots 4..7 = keys 32c + 16 + 4*grp + r
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            bf16x8_t pf[2];
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) {
+                uint4 w;
+                w.x = pack_bf16x2(sacc[qb][2 * c][0], sacc[qb][2 * c][1]);
+                w.y = pack_bf16x2(sacc[qb][2 * c][2], sacc[qb][2 * c][3]);
+                w.z = pack_bf16x2(sacc[qb][2 * c + 1][0], sacc[qb][2 * c + 1][1]);
+                w.w = pack_bf16x2(sacc[qb][2 * c + 1][2], sacc[qb][2 * c + 1][3]);
+                pf[qb] = __builtin_bit_cast(bf16x8_t, w);
+            }
+#pragma unroll
+            for (int h = 0; h < C::NHS; ++h) {
+                const bf16_t* vr = &sVt[(h * 16 + l16) * C::VL + 32 * c + 4 * grp];
+                const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
+                const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 16);
+                const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) oacc[qb][h] = mfma32(vf, pf[qb], oacc[qb][h]);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        float l = l_run[qb];
+        l += __shfl_xor(l, 16, kWave);
+        l += __shfl_xor(l, 32, kWave);
+        const int qrow = row0 + wave * 32 + qb * 16 + l16;
+        if (qrow >= row_end) continue;
+        if (a.nsplit == 1) {
+            const float inv_l = 1.0f / l;
+            bf16_t* op = static_cast<bf16_t*>(a.o) + (long)qrow * d + head * HD;
+#pragma unroll
+            for (int h = 0; h < C::NHS; ++h) {
+                const int cidx = h * 16 + grp * 4;
+                if (cidx < HD) {
+                    float v[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[r] = oacc[qb][h][r] * inv_l;
+                    store4<bf16_t>(op + cidx, v);
+                }
+            }
+        } else {
+            float* po = a.part_o + ((long)split * a.M + qrow) * d + head * HD;
+#pragma unroll
+            for (int h = 0; h < C::NHS; ++h) {
+                const int cidx = h * 16 + grp * 4;
+                if (cidx < HD)
+                    *reinterpret_cast<float4*>(po + cidx) =
+                        make_float4(oacc[qb][h][0], oacc[qb][h][1], oacc[qb][h][2], oacc[qb][h][3]);
+            }
+            if (grp == 0)
+                *reinterpret_cast<float2*>(a.part_ml + 2 * (((long)split * a.M + qrow) * a.n_heads + head)) =
+                    make_float2(m_run[qb], l);
+        }
+    }
+}
+
+// Combine of the key-range partials (log-sum-exp weights), fixed split order.
+__global__ __launch_bounds__(256) void attention_combine_kernel(AttnDesc a) {
+    const long n4 = (long)a.M * a.d / 4;
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    const long m = i / (a.d / 4);
+    const int col = (int)(i - m * (a.d / 4)) * 4;
+    const int head = col / a.hd;
+    float gmax = -INFINITY;
+    for (int s = 0; s < a.nsplit; ++s)
+        gmax = fmaxf(gmax, a.part_ml[2 * (((long)s * a.M + m) * a.n_heads + head)]);
+    float L = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < a.nsplit; ++s) {
+        const float* ml = a.part_ml + 2 * (((long)s * a.M + m) * a.n_heads + head);
+        const float w = exp2f((ml[0] - gmax) * a.scale_log2);
+        L += w * ml[1];
+        const float4 po = *reinterpret_cast<const float4*>(a.part_o + ((long)s * a.M + m) * a.d + col);
+        acc[0] += w * po.x; acc[1] += w * po.y; acc[2] += w * po.z; acc[3] += w * po.w;
+    }
+    const float inv = 1.0f / L;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] *= inv;
+    store4<bf16_t>(static_cast<bf16_t*>(a.o) + m * a.d + col, acc);
+}
+
 }  // namespace
 
-// bf16: head_dim up to 128 (padded to 64 / 96 / 128 in LDS and registers);
-// fp32: head_dim up to 64.
+bool attention_fast_path(int dtype, int hd) {
+    return dtype == kBF16 && (hd == 64 || hd == 72 || hd == 128);
+}
+
+// bf16, head_dim 64 / 72 / 128: the fast kernel (+ combine when split). Other
+// bf16 head_dims up to 128 and fp32 up to 64: the generic kernel.
 hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s) {
-    if (a.n_qtiles == 0) return hipSuccess;
+    if (a.M == 0) return hipSuccess;
+    if (attention_fast_path(dtype, a.hd)) {
+        dim3 grid(a.n_qtiles_fast, a.n_heads, a.nsplit), block(kThreads);
+        if (a.hd == 64)
+            hipLaunchKernelGGL((attention_fast_kernel<64>), grid, block, 0, s, a);
+        else if (a.hd == 72)
+            hipLaunchKernelGGL((attention_fast_kernel<72>), grid, block, 0, s, a);
+        else
+            hipLaunchKernelGGL((attention_fast_kernel<128>), grid, block, 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess || a.nsplit == 1) return e;
+        const long n4 = (long)a.M * a.d / 4;
+        hipLaunchKernelGGL(attention_combine_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, a);
+        return hipGetLastError();
+    }
     dim3 grid(a.n_qtiles, a.n_heads), block(kThreads);
     if (dtype == kBF16) {
         if (a.hd <= 64)

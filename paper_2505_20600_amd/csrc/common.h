@@ -9,6 +9,7 @@ namespace ms {
 using bf16_t = uint16_t;  // raw bfloat16 storage
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
@@ -17,12 +18,19 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
     return __uint_as_float(static_cast<uint32_t>(h) << 16);
 }
 
-// float32 -> bfloat16, round to nearest even; NaN stays a (quiet) NaN.
+// float32 -> bfloat16, round to nearest even, NaN kept (gfx950 v_cvt_pk_bf16_f32).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<bf16_t>(u >> 16);
+    __bf16 h = static_cast<__bf16>(f);
+    return __builtin_bit_cast(bf16_t, h);
+}
+
+// Two floats -> two packed bf16 in one 32-bit word (low = a).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    bf16x2_t v;
+    v.x = static_cast<__bf16>(a);
+    v.y = static_cast<__bf16>(b);
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 // Element-type traits: conversion to/from float and the 16x16 MFMA step.
@@ -75,8 +83,8 @@ template <> __device__ __forceinline__ void store4<float>(float* p, const float 
 }
 template <> __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, const float v[4]) {
     uint2 o;
-    o.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-    o.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+    o.x = pack_bf16x2(v[0], v[1]);
+    o.y = pack_bf16x2(v[2], v[3]);
     *reinterpret_cast<uint2*>(p) = o;
 }
 

@@ -6,7 +6,8 @@
 
 namespace ms {
 
-constexpr int kQTile = 64;        // attention query rows per workgroup
+constexpr int kQTile = 64;        // query rows per workgroup of the generic attention kernel
+constexpr int kFastQTile = 128;   // query rows per workgroup of the bf16 attention kernel
 constexpr int kMaxSegments = 128; // packed segments per step
 
 enum Dtype { kF32 = 0, kBF16 = 1 };
@@ -58,7 +59,16 @@ struct AttnDesc {
     const int32_t* cu_tiles;
     int nseg, T, d, hd, n_qtiles, n_heads;
     float scale_log2;     // log2(e) / sqrt(hd)
+    // bf16 path: 128-row query tiles, keys split over `nsplit` workgroups of
+    // `tiles_per_split` 64-key tiles; partials (unnormalised O, running max
+    // and sum) go to part_o [nsplit][M][d] / part_ml [nsplit][M][n_heads].
+    int M, n_qtiles_fast, nsplit, tiles_per_split;
+    float* part_o;
+    float* part_ml;
 };
+
+// True when launch_attention uses the bf16 fast kernel for this head_dim.
+bool attention_fast_path(int dtype, int hd);
 
 // a6: attention of the packed masked queries over every key of their request.
 hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s);

@@ -53,8 +53,12 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-    size_t rows, inv, seg_start, seg_req, cu_tiles, xm, a, q, o, h, u, total;
+    size_t rows, inv, seg_start, seg_req, cu_tiles, xm, a, q, o, h, u, part_o, part_ml, total;
 };
+
+// Attention key-range split: enough workgroups to give every CU about two,
+// bounded by the partial buffers (split count x rows <= B*T).
+constexpr int kAttnTargetGroups = 512;
 
 int elt_bytes(int32_t dtype) { return dtype == MS_BF16 ? 2 : 4; }
 
@@ -98,6 +102,8 @@ Layout make_layout(const ms_model_desc& d, int32_t B) {
     L.o = take(BT * dm * e);
     L.h = take(BT * dm * e);
     L.u = take(BT * f * e);
+    L.part_o = take(BT * dm * 4);
+    L.part_ml = take(BT * (size_t)d.n_heads * 2 * 4);
     L.total = off;
     return L;
 }
@@ -145,6 +151,7 @@ struct ms_step {
     ms_model_desc desc;
     int B = 0, T = 0, N = 0, d = 0, f = 0, hd = 0, elt = 0;
     int M = 0, nseg = 0, n_qtiles = 0, text_rows = 0;
+    int n_qtiles_fast = 0, attn_nsplit = 1, attn_tps = 1;
     bool all_masked = false;
     char* ws = nullptr;
     Layout lay{};
@@ -253,6 +260,12 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
     ad.nseg = s->nseg; ad.T = s->T; ad.d = d; ad.hd = s->hd;
     ad.n_qtiles = s->n_qtiles; ad.n_heads = s->desc.n_heads;
     ad.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)s->hd));
+    ad.M = M;
+    ad.n_qtiles_fast = s->n_qtiles_fast;
+    ad.nsplit = s->attn_nsplit;
+    ad.tiles_per_split = s->attn_tps;
+    ad.part_o = static_cast<float*>(s->buf(s->lay.part_o));
+    ad.part_ml = static_cast<float*>(s->buf(s->lay.part_ml));
     {
         ProfScope p(MS_K_ATTENTION, st);
         MS_HIP(ms::launch_attention(dt, ad, st));
@@ -404,6 +417,21 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
     for (int i = 0; i < s->nseg; ++i)
         s->n_qtiles += (s->seg_start[i + 1] - s->seg_start[i] + ms::kQTile - 1) / ms::kQTile;
     s->all_masked = s->M == batch * s->T;
+    s->n_qtiles_fast = 0;
+    for (int i = 0; i < s->nseg; ++i)
+        s->n_qtiles_fast += (s->seg_start[i + 1] - s->seg_start[i] + ms::kFastQTile - 1) / ms::kFastQTile;
+    {
+        const int ntiles = (s->T + 63) / 64;
+        const int base = std::max(1, s->n_qtiles_fast * desc->n_heads);
+        int target = kAttnTargetGroups;
+        if (const char* ev = std::getenv("MS_ATTN_SPLIT_TARGET")) target = std::max(1, std::atoi(ev));
+        int ns = std::min(ntiles, std::max(1, (target + base - 1) / base));
+        if (s->M > 0) ns = std::min(ns, std::max(1, batch * s->T / s->M));
+        if (!ms::attention_fast_path(desc->dtype, s->hd)) ns = 1;
+        const int tps = (ntiles + ns - 1) / ns;
+        s->attn_tps = tps;
+        s->attn_nsplit = (ntiles + tps - 1) / tps;
+    }
     plan_spans(s, hmask);
     for (int i = 0; i < 2 && e == hipSuccess; ++i) {
         e = hipEventCreateWithFlags(&s->ev_copied[i], hipEventDisableTiming);

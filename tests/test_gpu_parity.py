@@ -1,8 +1,8 @@
 """GPU parity: the HIP path through the C ABI against the CPU oracle.
 
 Index work (compaction, gather, scatter, untouched cache rows) is compared bit
-for bit; floating point within max relative error 1e-4 (fp32) and 2e-2 (bf16),
-the error of each element taken relative to max(|ref|, rms(ref)).
+for bit; floating point within max relative error 1e-4 (fp32) and 2e-2 (bf16)
+in the max norm, plus an element-wise guard (see gpu_helpers).
 """
 import numpy as np
 import pytest
@@ -126,8 +126,8 @@ def test_block_fresh_kv_rows_match_oracle():
     toks = oracle.masked_tokens(mask[0], 0)
     keep = np.setdiff1d(np.arange(shape.n_tokens), toks)
     np.testing.assert_array_equal(kv_gpu[0][0, keep], kv[0][0, keep])
-    assert G.rel_err(kv_gpu[0][0, toks], kv_ref[0, 0, toks]) <= G.TOL["bf16"]
-    assert G.rel_err(y[0, toks], y_ref[0, toks]) <= G.TOL["bf16"]
+    G.assert_close(kv_gpu[0][0, toks], kv_ref[0, 0, toks], "bf16", "fresh K/V")
+    G.assert_close(y[0, toks], y_ref[0, toks], "bf16", "block output")
     np.testing.assert_array_equal(y[0, keep], yc[0, keep])
 
 
@@ -142,10 +142,11 @@ def test_c1_fp32_block_matches_oracle():
     x = W.edited_hidden(shape, 1, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
     y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
-    assert G.rel_err(y, y_ref) <= G.TOL["fp32"]
-    assert G.rel_err(kv_gpu[0], kv_ref[0]) <= G.TOL["fp32"]
+    G.assert_close(y, y_ref, "fp32", "c1 output")
+    G.assert_close(kv_gpu[0], kv_ref[0], "fp32", "c1 working K/V")
     keep = mask[0] == 0
-    np.testing.assert_array_equal(y[0, keep], yc[0, keep])
+    # the cached rows pass through the device's float32 copy of the cache unchanged
+    np.testing.assert_array_equal(y[0, keep], yc[0, keep].astype(np.float32))
 
 
 def test_c1_own_cache_reproduces_dense():
@@ -154,7 +155,7 @@ def test_c1_own_cache_reproduces_dense():
     ws, xt, kv, yc = _inputs(shape, 1, dense_cache=True, random_ln=True)
     mask = W.workload_mask("c1", shape)
     y, _, _ = G.run_stack(shape, mask, xt, kv, yc, ws)
-    assert G.rel_err(y, yc) <= G.TOL["fp32"]
+    G.assert_close(y, yc, "fp32", "c1 own-cache")
 
 
 SMALL_BF16 = [
@@ -177,10 +178,9 @@ def test_small_bf16_stack_matches_oracle(shape, ratio):
     x = W.edited_hidden(shape, 30, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
     y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
-    err = G.rel_err(y, y_ref)
-    assert err <= G.TOL["bf16"], err
+    G.assert_close(y, y_ref, "bf16", f"{shape.name} output")
     for l in range(shape.n_layers):
-        assert G.rel_err(kv_gpu[l], kv_ref[l]) <= G.TOL["bf16"], l
+        G.assert_close(kv_gpu[l], kv_ref[l], "bf16", f"{shape.name} K/V layer {l}")
     for b in range(shape.batch):
         keep = np.concatenate([np.zeros(shape.n_text, bool), mask[b] == 0])
         np.testing.assert_array_equal(y[b, keep], yc[b, keep])
@@ -195,7 +195,7 @@ def test_all_ones_mask_with_poisoned_cache_equals_dense():
     kv = np.zeros((shape.n_layers, shape.batch, shape.n_tokens, 2, shape.d_model))
     y, _, _ = G.run_stack(shape, ones, xt, kv, None, ws, poison_cache=True)
     assert np.all(np.isfinite(y))
-    assert G.rel_err(y, y_ref) <= G.TOL["bf16"]
+    G.assert_close(y, y_ref, "bf16", "all-ones")
 
 
 @pytest.mark.parametrize("aliased", [False, True])
@@ -209,15 +209,25 @@ def test_empty_mask_returns_cache_bit_exact(aliased):
     np.testing.assert_array_equal(kv_gpu[1], kv[1])
 
 
-def test_batch_equals_single_requests():
+def test_batch_equals_single_requests(monkeypatch):
+    """Requests are independent: bit-exact with one key range per query tile (the key-range
+    split count depends on the whole batch's row count), within tolerance with the default split."""
     shape = W.ModelShape("sep", 2, 256, 4, 4, 12, 12, dtype="bf16", batch=3)
     ws, xt, kv, yc = _inputs(shape, 42, std=0.03)
     mask = _random_mask(shape, [0.2, 0.6, 0.05], 9)
-    yb, _, _ = G.run_stack(shape, mask, xt, kv, yc, ws)
     one = shape.replace(batch=1)
-    for b in range(3):
-        y1, _, _ = G.run_stack(one, mask[b:b + 1], xt[b:b + 1], kv[:, b:b + 1], yc[b:b + 1], ws)
-        np.testing.assert_array_equal(y1[0], yb[b])
+    for target in ("1", None):
+        if target:
+            monkeypatch.setenv("MS_ATTN_SPLIT_TARGET", target)
+        else:
+            monkeypatch.delenv("MS_ATTN_SPLIT_TARGET", raising=False)
+        yb, _, _ = G.run_stack(shape, mask, xt, kv, yc, ws)
+        for b in range(3):
+            y1, _, _ = G.run_stack(one, mask[b:b + 1], xt[b:b + 1], kv[:, b:b + 1], yc[b:b + 1], ws)
+            if target:
+                np.testing.assert_array_equal(y1[0], yb[b])
+            else:
+                G.assert_close(y1[0], yb[b], "bf16", f"request {b} alone vs in the batch")
 
 
 # ------------------------------------------------------------------ streamed cache
@@ -239,7 +249,7 @@ def test_streamed_cache_matches_resident_and_serialized(shape):
     np.testing.assert_array_equal(y_pipe, y_res)
     np.testing.assert_array_equal(y_ser, y_res)
     y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape)
-    assert G.rel_err(y_res, y_ref) <= G.TOL["bf16"]
+    G.assert_close(y_res, y_ref, "bf16", f"{shape.name} streamed")
 
 
 def test_streamed_repeated_steps_are_identical():
@@ -286,6 +296,29 @@ def test_full_size_stack_sampled_request(cfg_key, ratio):
     x = W.edited_hidden(shape, W.CONFIG_IDS[cfg_key], xt, mask)
     y, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=(cfg_key == "c3"))
     toks, xm_ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, b=0)
-    assert G.rel_err(y[0, toks], xm_ref) <= G.TOL["bf16"]
+    G.assert_close(y[0, toks], xm_ref, "bf16", f"{cfg_key} full size")
     keep = np.setdiff1d(np.arange(shape.n_tokens), toks)
     np.testing.assert_array_equal(y[0, keep], yc[0, keep])
+
+
+# ------------------------------------------------------------------ attention key-range split
+
+@pytest.mark.parametrize("hd_shape", [
+    W.ModelShape("split_hd64", 1, 256, 4, 4, 16, 20, dtype="bf16", batch=2),
+    W.ModelShape("split_hd72", 1, 576, 8, 4, 12, 20, dtype="bf16"),
+    W.ModelShape("split_hd128", 1, 256, 2, 4, 20, 16, dtype="bf16"),
+], ids=lambda s: s.name)
+def test_attention_split_and_unsplit_match_oracle(hd_shape, monkeypatch):
+    """The key range of a query tile is split over workgroups (log-sum-exp combine) or not."""
+    shape = hd_shape
+    ws, xt, kv, yc = _inputs(shape, 60, std=0.03)
+    mask = _random_mask(shape, 0.4, 13)
+    x = W.edited_hidden(shape, 60, xt, mask)
+    y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape)
+    outs = []
+    for target in ("1", "100000"):
+        monkeypatch.setenv("MS_ATTN_SPLIT_TARGET", target)
+        y, _, _ = G.run_stack(shape, mask, x, kv, yc, ws)
+        G.assert_close(y, y_ref, "bf16", f"{shape.name} split target {target}")
+        outs.append(y)
+    G.assert_close(outs[1], outs[0], "bf16", "split vs unsplit")
