@@ -47,6 +47,10 @@ def _run(cmd, verbose):
         print(err, file=sys.stderr)
 
 
+# per-source extra flags: attention's softmax max-reductions need no NaN ordering
+EXTRA = {"attention.hip": ["-fno-honor-nans"]}
+
+
 def build(verbose: bool = False, jobs: int = 8) -> str:
     os.makedirs(BUILD, exist_ok=True)
     cc = hipcc()
@@ -55,7 +59,7 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmds.append([cc, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([cc, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
     with cf.ThreadPoolExecutor(max_workers=max(1, min(jobs, len(cmds)))) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
     tmp = LIB + ".tmp"

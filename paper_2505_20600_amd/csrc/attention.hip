@@ -138,13 +138,13 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnDesc a) {
         mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
         mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
         const float m_new = fmaxf(m_run, mx);
-        const float corr = (m_run == -INFINITY) ? 0.f : exp2f(m_run - m_new);
+        const float corr = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
         float psum = 0.f;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                sc[ks][r] = exp2f(sc[ks][r] - m_new);
+                sc[ks][r] = fast_exp2(sc[ks][r] - m_new);
                 psum += sc[ks][r];
             }
         l_run = l_run * corr + psum;
@@ -231,11 +231,10 @@ struct FastCfg {
     static constexpr int KL = HDQ + 8;                    // K row stride in LDS (elements)
     static constexpr int VL = kKeyTile + 4;               // V^T row stride in LDS (elements)
     static constexpr int CH = HD / 8;                     // 16-byte chunks per key row
-    static constexpr int KITEMS = kKeyTile * CH;
-    static constexpr int VITEMS = (kKeyTile / 4) * CH;    // 4-key groups x chunks
-    static constexpr int KPT = (KITEMS + 127) / 128;
-    static constexpr int VPT = (VITEMS + 127) / 128;
-    static constexpr int NPRE = KPT > 4 * VPT ? KPT : 4 * VPT;
+    static constexpr int KITEMS = kKeyTile * CH;          // K: key x chunk
+    static constexpr int VITEMS = (kKeyTile / 2) * CH;    // V: key pair x chunk
+    static constexpr int KPT = (KITEMS + kThreads - 1) / kThreads;
+    static constexpr int VPT = (VITEMS + kThreads - 1) / kThreads;
     static_assert(HD % 8 == 0 && HD % 32 <= 16, "head_dim layout");
 };
 
@@ -248,7 +247,7 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x4_t a, bf16x4_t b, f32x4_t c) {
 }
 
 template <int HD>
-__global__ __launch_bounds__(kThreads) void attention_fast_kernel(AttnDesc a) {
+__global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a) {
     using C = FastCfg<HD>;
     __shared__ __attribute__((aligned(16))) bf16_t sK[kKeyTile * C::KL];
     __shared__ __attribute__((aligned(16))) bf16_t sVt[C::HDV * C::VL];
@@ -258,12 +257,16 @@ __global__ __launch_bounds__(kThreads) void attention_fast_kernel(AttnDesc a) {
     const int wave = tid / kWave;
     const int grp = lane / 16;
     const int l16 = lane % 16;
-    const int head = blockIdx.y;
-    const int split = blockIdx.z;
+    // 1-D launch, logical order head-major (head, split, query tile), placed so
+    // that each XCD works on a contiguous range of heads and keeps their K/V in L2
+    const int total = a.n_qtiles_fast * a.nsplit * a.n_heads;
+    const int lb = xcd_logical_block(blockIdx.x, total);
+    const int head = lb / (a.nsplit * a.n_qtiles_fast);
+    const int split = (lb / a.n_qtiles_fast) % a.nsplit;
     const int T_ = a.T, d = a.d;
 
     // query tile -> segment (128-row tiles counted per segment)
-    int tile = blockIdx.x, seg = 0, row0 = 0, row_end = 0;
+    int tile = lb % a.n_qtiles_fast, seg = 0, row0 = 0, row_end = 0;
     for (; seg < a.nseg; ++seg) {
         const int r0 = a.seg_start[seg], r1 = a.seg_start[seg + 1];
         const int nt = (r1 - r0 + kFastQTile - 1) / kFastQTile;
@@ -317,80 +320,76 @@ __global__ __launch_bounds__(kThreads) void attention_fast_kernel(AttnDesc a) {
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
     const float cs = a.scale_log2;
 
-    // waves 0-1 stage V (transposed), waves 2-3 stage K
-    const bool vrole = tid < 128;
-    const int rt = tid % 128;
-    vec16 pre[C::NPRE];
+    // Every thread stages both K and V items of the next tile into its own
+    // registers, with no branches around the loads, so the loads stay in
+    // flight while the current tile is computed. Addresses: a uniform tile
+    // base plus fixed 32-bit per-thread offsets; only the last, partial tile
+    // clamps its key index (keys past T are masked out of its scores).
+    int offk[C::KPT], offv[C::VPT][2];
+    int keyk[C::KPT], keyv[C::VPT];
+#pragma unroll
+    for (int j = 0; j < C::KPT; ++j) {
+        const int item = min(tid + j * kThreads, C::KITEMS - 1);
+        keyk[j] = item / C::CH;
+        offk[j] = keyk[j] * 2 * d + (item % C::CH) * 8;
+    }
+#pragma unroll
+    for (int j = 0; j < C::VPT; ++j) {
+        const int item = min(tid + j * kThreads, C::VITEMS - 1);
+        keyv[j] = 2 * (item / C::CH);
+#pragma unroll
+        for (int e = 0; e < 2; ++e) offv[j][e] = (keyv[j] + e) * 2 * d + d + (item % C::CH) * 8;
+    }
+    vec16 pk[C::KPT], pv[C::VPT][2];
     auto gload = [&](int kt) {
         const int k0 = kt * kKeyTile;
-        if (vrole) {
+        const bf16_t* base = kvb + (long)k0 * 2 * d;
+        if (k0 + kKeyTile <= T_) {
 #pragma unroll
-            for (int j = 0; j < C::VPT; ++j) {
-                const int item = rt + j * 128;
-                if (item < C::VITEMS) {
-                    const int kg = item / C::CH, c = item % C::CH;
+            for (int j = 0; j < C::KPT; ++j) pk[j] = ld16(base + offk[j]);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int t = k0 + kg * 4 + e;
-                        vec16 v = {{0u, 0u, 0u, 0u}};
-                        if (t < T_) v = ld16(kvb + (long)t * 2 * d + d + c * 8);
-                        pre[j * 4 + e] = v;
-                    }
-                }
-            }
+            for (int j = 0; j < C::VPT; ++j)
+#pragma unroll
+                for (int e = 0; e < 2; ++e) pv[j][e] = ld16(base + offv[j][e]);
         } else {
+            const int last = T_ - 1 - k0;
 #pragma unroll
-            for (int j = 0; j < C::KPT; ++j) {
-                const int item = rt + j * 128;
-                if (item < C::KITEMS) {
-                    const int key = item / C::CH, c = item % C::CH;
-                    const int t = k0 + key;
-                    vec16 v = {{0u, 0u, 0u, 0u}};
-                    if (t < T_) v = ld16(kvb + (long)t * 2 * d + c * 8);
-                    pre[j] = v;
-                }
-            }
+            for (int j = 0; j < C::KPT; ++j)
+                pk[j] = ld16(base + offk[j] - (keyk[j] - min(keyk[j], last)) * 2 * d);
+#pragma unroll
+            for (int j = 0; j < C::VPT; ++j)
+#pragma unroll
+                for (int e = 0; e < 2; ++e)
+                    pv[j][e] = ld16(base + offv[j][e] - (keyv[j] + e - min(keyv[j] + e, last)) * 2 * d);
         }
     };
     auto sstore = [&]() {
-        if (vrole) {
 #pragma unroll
-            for (int j = 0; j < C::VPT; ++j) {
-                const int item = rt + j * 128;
-                if (item < C::VITEMS) {
-                    const int kg = item / C::CH, c = item % C::CH;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int sh = (e & 1) * 16;
-                        const uint32_t k0 = (pre[j * 4 + 0].w[e >> 1] >> sh) & 0xffffu;
-                        const uint32_t k1 = (pre[j * 4 + 1].w[e >> 1] >> sh) & 0xffffu;
-                        const uint32_t k2 = (pre[j * 4 + 2].w[e >> 1] >> sh) & 0xffffu;
-                        const uint32_t k3 = (pre[j * 4 + 3].w[e >> 1] >> sh) & 0xffffu;
-                        *reinterpret_cast<uint2*>(&sVt[(c * 8 + e) * C::VL + kg * 4]) =
-                            make_uint2(k0 | (k1 << 16), k2 | (k3 << 16));
-                    }
-                }
+        for (int j = 0; j < C::KPT; ++j) {
+            const int item = tid + j * kThreads;
+            if (C::KITEMS % kThreads == 0 || item < C::KITEMS) {
+                const int key = item / C::CH, c = item % C::CH;
+                st16(&sK[key * C::KL + c * 8], pk[j]);
             }
-        } else {
+        }
 #pragma unroll
-            for (int j = 0; j < C::KPT; ++j) {
-                const int item = rt + j * 128;
-                if (item < C::KITEMS) {
-                    const int key = item / C::CH, c = item % C::CH;
-                    st16(&sK[key * C::KL + c * 8], pre[j]);
+        for (int j = 0; j < C::VPT; ++j) {
+            const int item = tid + j * kThreads;
+            if (C::VITEMS % kThreads == 0 || item < C::VITEMS) {
+                const int kp = item / C::CH, c = item % C::CH;
+                // V^T[c*8 + e][2kp .. 2kp+1] = (V[2kp][c*8+e], V[2kp+1][c*8+e])
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t w = __builtin_amdgcn_perm(pv[j][1].w[e >> 1], pv[j][0].w[e >> 1],
+                                                             (e & 1) ? 0x07060302u : 0x05040100u);
+                    *reinterpret_cast<uint32_t*>(&sVt[(c * 8 + e) * C::VL + 2 * kp]) = w;
                 }
             }
         }
     };
 
-    if (kt0 < kt1) gload(kt0);
-    for (int kt = kt0; kt < kt1; ++kt) {
-        __syncthreads();
-        sstore();
-        __syncthreads();
-        if (kt + 1 < kt1) gload(kt + 1);
-
-        // S^T = K Q^T: keys ks*16 + 4*grp + r, query l16 of block qb
+    // One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
+    auto compute = [&](int k0, bool tail) {
         f32x4_t sacc[2][4];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
@@ -411,42 +410,43 @@ __global__ __launch_bounds__(kThreads) void attention_fast_kernel(AttnDesc a) {
                 for (int qb = 0; qb < 2; ++qb) sacc[qb][ks] = mfma16(kf, qf16[qb], sacc[qb][ks]);
             }
         }
-
-        const int k0 = kt * kKeyTile;
-        const bool tail = k0 + kKeyTile > T_;
+        if (tail) {
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            if (tail) {
+            for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
                         if (k0 + ks * 16 + grp * 4 + r >= T_) sacc[qb][ks][r] = -INFINITY;
-            }
+        }
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
             float mx = -INFINITY;
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks)
                 mx = fmaxf(fmaxf(mx, fmaxf(sacc[qb][ks][0], sacc[qb][ks][1])), fmaxf(sacc[qb][ks][2], sacc[qb][ks][3]));
-            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+            mx = rows_max(mx);
             const float m_new = fmaxf(m_run[qb], mx);
-            const float corr = exp2f((m_run[qb] - m_new) * cs);
-            const float mc = m_new * cs;
+            // rescale the accumulators only when some query's running max grew
+            if (__any(m_new > m_run[qb])) {
+                const float corr = fast_exp2((m_run[qb] - m_new) * cs);
+                l_run[qb] *= corr;
+#pragma unroll
+                for (int h = 0; h < C::NHS; ++h) oacc[qb][h] *= corr;
+                m_run[qb] = m_new;
+            }
+            const float mc = m_run[qb] * cs;
             float psum = 0.f;
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const float p = exp2f(fmaf(sacc[qb][ks][r], cs, -mc));
+                    const float p = fast_exp2(fmaf(sacc[qb][ks][r], cs, -mc));
                     sacc[qb][ks][r] = p;
                     psum += p;
                 }
-            l_run[qb] = l_run[qb] * corr + psum;
-            m_run[qb] = m_new;
-#pragma unroll
-            for (int h = 0; h < C::NHS; ++h) oacc[qb][h] *= corr;
+            l_run[qb] += psum;
         }
-
         // O^T += V^T P^T; K-slots 0..3 = keys 32c + 4*grp + r, slots 4..7 = keys 32c + 16 + 4*grp + r
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
@@ -470,13 +470,29 @@ __global__ __launch_bounds__(kThreads) void attention_fast_kernel(AttnDesc a) {
                 for (int qb = 0; qb < 2; ++qb) oacc[qb][h] = mfma32(vf, pf[qb], oacc[qb][h]);
             }
         }
+    };
+
+    // full 64-key tiles first (no masking), then the partial last tile if any
+    const int kfull = min(kt1, max(kt0, T_ / kKeyTile));
+    if (kt0 < kt1) gload(kt0);
+    for (int kt = kt0; kt < kfull; ++kt) {
+        __syncthreads();
+        sstore();
+        __syncthreads();
+        if (kt + 1 < kt1) gload(kt + 1);
+        compute(kt * kKeyTile, false);
+    }
+    for (int kt = kfull; kt < kt1; ++kt) {
+        __syncthreads();
+        sstore();
+        __syncthreads();
+        if (kt + 1 < kt1) gload(kt + 1);
+        compute(kt * kKeyTile, true);
     }
 
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        float l = l_run[qb];
-        l += __shfl_xor(l, 16, kWave);
-        l += __shfl_xor(l, 32, kWave);
+        const float l = rows_sum(l_run[qb]);
         const int qrow = row0 + wave * 32 + qb * 16 + l16;
         if (qrow >= row_end) continue;
         if (a.nsplit == 1) {
@@ -522,7 +538,7 @@ __global__ __launch_bounds__(256) void attention_combine_kernel(AttnDesc a) {
     float L = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < a.nsplit; ++s) {
         const float* ml = a.part_ml + 2 * (((long)s * a.M + m) * a.n_heads + head);
-        const float w = exp2f((ml[0] - gmax) * a.scale_log2);
+        const float w = fast_exp2((ml[0] - gmax) * a.scale_log2);
         L += w * ml[1];
         const float4 po = *reinterpret_cast<const float4*>(a.part_o + ((long)s * a.M + m) * a.d + col);
         acc[0] += w * po.x; acc[1] += w * po.y; acc[2] += w * po.z; acc[3] += w * po.w;
@@ -544,7 +560,7 @@ bool attention_fast_path(int dtype, int hd) {
 hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s) {
     if (a.M == 0) return hipSuccess;
     if (attention_fast_path(dtype, a.hd)) {
-        dim3 grid(a.n_qtiles_fast, a.n_heads, a.nsplit), block(kThreads);
+        dim3 grid(a.n_qtiles_fast * a.n_heads * a.nsplit), block(kThreads);
         if (a.hd == 64)
             hipLaunchKernelGGL((attention_fast_kernel<64>), grid, block, 0, s, a);
         else if (a.hd == 72)

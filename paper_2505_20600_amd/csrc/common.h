@@ -88,6 +88,39 @@ template <> __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, const floa
     *reinterpret_cast<uint2*>(p) = o;
 }
 
+// MI355X dispatches consecutive workgroups of a launch round-robin over its
+// 8 XCDs, each with a private L2. Remap the hardware block id so that every
+// XCD receives one contiguous range of logical ids: work that shares operands
+// (one attention head's K/V, one GEMM weight slice) then shares an L2.
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ int xcd_logical_block(int hw, int total) {
+    const int x = hw % kXcds, i = hw / kXcds;
+    const int per = total / kXcds, rem = total % kXcds;
+    return x * per + min(x, rem) + i;
+}
+
+// 2^x with the hardware v_exp_f32 (no denormal-result fix-up: softmax
+// weights below 2^-126 of the running maximum are irrelevant).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Reductions over the four 16-lane rows holding the same column (lanes l,
+// l^16, l^32, l^48) with the gfx950 cross-row swaps: given the same register
+// twice, each swap returns {own value, partner value} in some order.
+__device__ __forceinline__ float rows_max(float x) {
+    auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float rows_sum(float x) {
+    auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);

@@ -4,26 +4,63 @@
 //     out[m][n] = epilogue( sum_k A[m][k] * W[n][k] + bias[n] )
 //
 // Both operands are K-contiguous (activations [M][K], Linear weights
-// [N][K]), which is the native operand layout of the CDNA4 matrix cores.
-// The weight tile is the MFMA "A" operand and the activation tile the "B"
-// operand, so each lane ends up with four consecutive output columns of one
-// row and the epilogue writes 4-element vectors.
+// [N][K]), the native operand layout of the CDNA4 matrix cores. The weight
+// tile is the MFMA "A" operand and the activation tile the "B" operand, so
+// each lane ends up with four consecutive output columns of one row and the
+// epilogue writes 4-element vectors.
 //
 // Epilogues: bias; bias + residual (out-projection and MLP-down); bias +
 // exact GELU (MLP-up); QKV, which writes Q to its own buffer and the fresh
 // K/V of each masked token straight into that token's row of the working
 // K/V (the K/V cache of Fig. 7 with the masked rows replaced).
+//
+// Tiles: BM x BN in {128, 64}^2, four waves (2 x 2), K step of 128 bytes,
+// LDS double-buffered with one barrier per step (the next tile is fetched
+// into registers while the current one feeds the MFMAs). The host picks the
+// largest tile that still gives every CU a workgroup; when even 64 x 64 does
+// not, the K range is split over workgroups that write float32 partials,
+// summed in a fixed order by a second kernel that applies the epilogue.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace ms {
 namespace {
 
-constexpr int kBM = 128;   // activation rows per workgroup
-constexpr int kBN = 128;   // output columns per workgroup
 constexpr int kThreads = 256;
+constexpr int kCUs = 256;
 
 template <typename T, int EPI>
+__device__ __forceinline__ void epilogue_store(const GemmDesc& g, int m, int n, float v[4]) {
+    const T* __restrict__ bias = static_cast<const T*>(g.bias);
+    float bv[4];
+    load4<T>(bias + n, bv);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] += bv[r];
+    if constexpr (EPI == kEpiBiasResid) {
+        float rv[4];
+        load4<T>(static_cast<const T*>(g.R) + (long)m * g.ldr + n, rv);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] += rv[r];
+    }
+    if constexpr (EPI == kEpiBiasGelu) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = 0.5f * v[r] * (1.0f + erff(v[r] * 0.70710678118654752f));
+    }
+    if constexpr (EPI == kEpiQKV) {
+        if (n < g.d) {
+            store4<T>(static_cast<T*>(g.C) + (long)m * g.ldc + n, v);
+        } else {
+            const long tok = g.rows[m];
+            store4<T>(static_cast<T*>(g.kv) + tok * 2 * g.d + (n - g.d), v);
+        }
+    } else {
+        store4<T>(static_cast<T*>(g.C) + (long)m * g.ldc + n, v);
+    }
+}
+
+template <typename T, int BM, int BN, int EPI>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
     using E = Elt<T>;
     using frag_t = typename E::frag_t;
@@ -32,123 +69,197 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
     constexpr int LDS = BK + V;             // padded LDS row (elements): 144 bytes
     constexpr int CHUNKS = BK / V;          // 16-byte chunks per tile row (8)
     constexpr int ROWS_PER_PASS = kThreads / CHUNKS;   // 32
-    constexpr int PASSES = kBM / ROWS_PER_PASS;        // 4
-    __shared__ __attribute__((aligned(16))) T sA[kBM * LDS];
-    __shared__ __attribute__((aligned(16))) T sW[kBN * LDS];
+    constexpr int PA = BM / ROWS_PER_PASS;
+    constexpr int PW = BN / ROWS_PER_PASS;
+    constexpr int SM = BM / 32;             // 16-row MFMA blocks per wave (rows m)
+    constexpr int SN = BN / 32;             // 16-col MFMA blocks per wave (cols n)
+    __shared__ __attribute__((aligned(16))) T sA[2][BM * LDS];
+    __shared__ __attribute__((aligned(16))) T sW[2][BN * LDS];
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
     const int wave = tid / kWave;
     const int wm = wave & 1, wn = wave >> 1;
-    const int n0 = blockIdx.x * kBN;
-    const int m0 = blockIdx.y * kBM;
     const int M = g.M, N = g.N, K = g.K;
+    // 1-D launch, logical order (k split, n tile, m tile) with m fastest, placed
+    // so that each XCD covers a contiguous range of weight (n) tiles
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    const int lb = xcd_logical_block(blockIdx.x, tiles_m * tiles_n * g.ksplit);
+    const int kz = lb / (tiles_m * tiles_n);
+    const int n0 = ((lb / tiles_m) % tiles_n) * BN;
+    const int m0 = (lb % tiles_m) * BM;
+    const int kbeg = kz * g.kchunk;
+    const int kend = min(K, kbeg + g.kchunk);
     const T* __restrict__ A = static_cast<const T*>(g.A);
     const T* __restrict__ W = static_cast<const T*>(g.W);
 
     const int lr = tid / CHUNKS;
     const int lc = tid % CHUNKS;
-    vec16 ra[PASSES], rw[PASSES];
+    vec16 ra[PA], rw[PW];
     auto gload = [&](int k0) {
 #pragma unroll
-        for (int i = 0; i < PASSES; ++i) {
+        for (int i = 0; i < PA; ++i) {
             const int m = min(m0 + lr + ROWS_PER_PASS * i, M - 1);
             ra[i] = ld16(A + (long)m * g.lda + k0 + lc * V);
+        }
+#pragma unroll
+        for (int i = 0; i < PW; ++i) {
             const int n = min(n0 + lr + ROWS_PER_PASS * i, N - 1);
             rw[i] = ld16(W + (long)n * K + k0 + lc * V);
         }
     };
-
-    f32x4_t acc[4][4];
+    auto sstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < PA; ++i) st16(&sA[buf][(lr + ROWS_PER_PASS * i) * LDS + lc * V], ra[i]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < PW; ++i) st16(&sW[buf][(lr + ROWS_PER_PASS * i) * LDS + lc * V], rw[i]);
+    };
 
-    const int nk = K / BK;
-    gload(0);
+    f32x4_t acc[SN][SM];
+#pragma unroll
+    for (int i = 0; i < SN; ++i)
+#pragma unroll
+        for (int j = 0; j < SM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = (kend - kbeg) / BK;
+    if (nk > 0) {
+        gload(kbeg);
+        sstore(0);
+    }
+    __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < PASSES; ++i) {
-            st16(&sA[(lr + ROWS_PER_PASS * i) * LDS + lc * V], ra[i]);
-            st16(&sW[(lr + ROWS_PER_PASS * i) * LDS + lc * V], rw[i]);
-        }
-        __syncthreads();
-        if (kt + 1 < nk) gload((kt + 1) * BK);
+        const int buf = kt & 1;
+        if (kt + 1 < nk) gload(kbeg + (kt + 1) * BK);
 #pragma unroll
         for (int ks = 0; ks < BK / E::kKStep; ++ks) {
             const int kk = ks * E::kKStep + (lane / 16) * E::kKPerLane;
-            frag_t fw[4], fa[4];
+            frag_t fw[SN], fa[SM];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                fw[i] = *reinterpret_cast<const frag_t*>(&sW[(wn * 64 + i * 16 + lane % 16) * LDS + kk]);
+            for (int i = 0; i < SN; ++i)
+                fw[i] = *reinterpret_cast<const frag_t*>(&sW[buf][(wn * (BN / 2) + i * 16 + lane % 16) * LDS + kk]);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                fa[j] = *reinterpret_cast<const frag_t*>(&sA[(wm * 64 + j * 16 + lane % 16) * LDS + kk]);
+            for (int j = 0; j < SM; ++j)
+                fa[j] = *reinterpret_cast<const frag_t*>(&sA[buf][(wm * (BM / 2) + j * 16 + lane % 16) * LDS + kk]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < SN; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = E::mma(fw[i], fa[j], acc[i][j]);
+                for (int j = 0; j < SM; ++j) acc[i][j] = E::mma(fw[i], fa[j], acc[i][j]);
         }
+        if (kt + 1 < nk) sstore(buf ^ 1);
+        __syncthreads();
     }
 
-    const T* __restrict__ bias = static_cast<const T*>(g.bias);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int n = n0 + wn * 64 + i * 16 + (lane / 16) * 4;
+    for (int i = 0; i < SN; ++i) {
+        const int n = n0 + wn * (BN / 2) + i * 16 + (lane / 16) * 4;
         if (n >= N) continue;
-        float bv[4];
-        load4<T>(bias + n, bv);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int m = m0 + wm * 64 + j * 16 + lane % 16;
+        for (int j = 0; j < SM; ++j) {
+            const int m = m0 + wm * (BM / 2) + j * 16 + lane % 16;
             if (m >= M) continue;
-            float v[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = acc[i][j][r] + bv[r];
-            if constexpr (EPI == kEpiBiasResid) {
-                float rv[4];
-                load4<T>(static_cast<const T*>(g.R) + (long)m * g.ldr + n, rv);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] += rv[r];
-            }
-            if constexpr (EPI == kEpiBiasGelu) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = 0.5f * v[r] * (1.0f + erff(v[r] * 0.70710678118654752f));
-            }
-            if constexpr (EPI == kEpiQKV) {
-                if (n < g.d) {
-                    store4<T>(static_cast<T*>(g.C) + (long)m * g.ldc + n, v);
-                } else {
-                    const long tok = g.rows[m];
-                    store4<T>(static_cast<T*>(g.kv) + tok * 2 * g.d + (n - g.d), v);
-                }
+            float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+            if (g.ksplit == 1) {
+                epilogue_store<T, EPI>(g, m, n, v);
             } else {
-                store4<T>(static_cast<T*>(g.C) + (long)m * g.ldc + n, v);
+                *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) =
+                    make_float4(v[0], v[1], v[2], v[3]);
             }
         }
     }
 }
 
-template <typename T>
-hipError_t launch_typed(const GemmDesc& g, hipStream_t s) {
-    dim3 grid((g.N + kBN - 1) / kBN, (g.M + kBM - 1) / kBM), block(kThreads);
+// Split-K: sum the partials in split order, then the epilogue.
+template <typename T, int EPI>
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmDesc g) {
+    const long n4 = (long)g.M * g.N / 4;
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    const int m = (int)(i / (g.N / 4));
+    const int n = (int)(i - (long)m * (g.N / 4)) * 4;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < g.ksplit; ++s) {
+        const float4 p = *reinterpret_cast<const float4*>(g.part + ((long)s * g.M + m) * g.N + n);
+        v[0] += p.x; v[1] += p.y; v[2] += p.z; v[3] += p.w;
+    }
+    epilogue_store<T, EPI>(g, m, n, v);
+}
+
+template <typename T, int BM, int BN>
+hipError_t launch_tile(const GemmDesc& g, hipStream_t s) {
+    dim3 grid(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM) * g.ksplit), block(kThreads);
     switch (g.epilogue) {
-        case kEpiBias: hipLaunchKernelGGL((gemm_kernel<T, kEpiBias>), grid, block, 0, s, g); break;
-        case kEpiBiasResid: hipLaunchKernelGGL((gemm_kernel<T, kEpiBiasResid>), grid, block, 0, s, g); break;
-        case kEpiBiasGelu: hipLaunchKernelGGL((gemm_kernel<T, kEpiBiasGelu>), grid, block, 0, s, g); break;
-        case kEpiQKV: hipLaunchKernelGGL((gemm_kernel<T, kEpiQKV>), grid, block, 0, s, g); break;
+        case kEpiBias: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, kEpiBias>), grid, block, 0, s, g); break;
+        case kEpiBiasResid: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, kEpiBiasResid>), grid, block, 0, s, g); break;
+        case kEpiBiasGelu: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, kEpiBiasGelu>), grid, block, 0, s, g); break;
+        case kEpiQKV: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, kEpiQKV>), grid, block, 0, s, g); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
+template <typename T>
+hipError_t launch_reduce(const GemmDesc& g, hipStream_t s) {
+    const long n4 = (long)g.M * g.N / 4;
+    dim3 grid((unsigned)((n4 + 255) / 256)), block(256);
+    switch (g.epilogue) {
+        case kEpiBias: hipLaunchKernelGGL((gemm_reduce_kernel<T, kEpiBias>), grid, block, 0, s, g); break;
+        case kEpiBiasResid: hipLaunchKernelGGL((gemm_reduce_kernel<T, kEpiBiasResid>), grid, block, 0, s, g); break;
+        case kEpiBiasGelu: hipLaunchKernelGGL((gemm_reduce_kernel<T, kEpiBiasGelu>), grid, block, 0, s, g); break;
+        case kEpiQKV: hipLaunchKernelGGL((gemm_reduce_kernel<T, kEpiQKV>), grid, block, 0, s, g); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+long groups(const GemmDesc& g, int bm, int bn) {
+    return (long)((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn);
+}
+
 }  // namespace
 
-hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t s) {
-    if (g.M == 0) return hipSuccess;
-    return dtype == kBF16 ? launch_typed<bf16_t>(g, s) : launch_typed<float>(g, s);
+GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats) {
+    GemmPlan p{64, 64, 1};
+    if (dtype != kBF16) return p;   // fp32 path: one tile shape
+    GemmDesc g{};
+    g.M = M; g.N = N;
+    static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+    for (const auto& c : cand) {
+        if (groups(g, c[0], c[1]) >= kCUs) {
+            p.bm = c[0]; p.bn = c[1];
+            return p;
+        }
+    }
+    // even 64 x 64 leaves CUs idle: split K (each split keeps >= 4 K steps of 64)
+    const long base = groups(g, 64, 64);
+    int ks = (int)((2 * kCUs + base - 1) / base);
+    ks = std::min(ks, std::max(1, K / 256));
+    while (ks > 1 && (size_t)ks * M * N > part_capacity_floats) --ks;
+    p.ksplit = std::max(1, ks);
+    return p;
+}
+
+hipError_t launch_gemm(int dtype, const GemmDesc& gin, hipStream_t s) {
+    if (gin.M == 0) return hipSuccess;
+    GemmDesc g = gin;
+    const int bk = dtype == kBF16 ? 64 : 32;
+    if (g.ksplit < 1) g.ksplit = 1;
+    // K range per split, a multiple of the K step
+    const int steps = g.K / bk;
+    const int per = (steps + g.ksplit - 1) / g.ksplit;
+    g.kchunk = per * bk;
+    g.ksplit = (steps + per - 1) / per;
+    hipError_t e;
+    if (dtype == kBF16) {
+        if (g.bm == 128 && g.bn == 128) e = launch_tile<bf16_t, 128, 128>(g, s);
+        else if (g.bm == 128 && g.bn == 64) e = launch_tile<bf16_t, 128, 64>(g, s);
+        else if (g.bm == 64 && g.bn == 128) e = launch_tile<bf16_t, 64, 128>(g, s);
+        else e = launch_tile<bf16_t, 64, 64>(g, s);
+        if (e == hipSuccess && g.ksplit > 1) e = launch_reduce<bf16_t>(g, s);
+    } else {
+        e = launch_tile<float, 64, 64>(g, s);
+        if (e == hipSuccess && g.ksplit > 1) e = launch_reduce<float>(g, s);
+    }
+    return e;
 }
 
 }  // namespace ms

@@ -45,7 +45,21 @@ struct GemmDesc {
     int lda, ldr, ldc;
     int d;              // kEpiQKV: model width
     int epilogue;
+    int bm, bn;         // output tile (from plan_gemm)
+    int ksplit;         // K-range splits (1: epilogue fused in the GEMM)
+    int kchunk;         // set by launch_gemm
+    float* part;        // ksplit > 1: [ksplit][M][N] float32 partials
 };
+
+struct GemmPlan {
+    int bm, bn, ksplit;
+};
+
+// Partial buffer the split-K plan may use (float32 elements).
+constexpr size_t kGemmPartFloats = size_t(4) << 20;
+
+// Tile shape and K split for an M x N x K product on 256 CUs.
+GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats);
 
 // a4/a5/a7/a8/a9: out = epi(A W^T + bias).
 hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t s);

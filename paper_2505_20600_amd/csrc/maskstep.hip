@@ -53,12 +53,17 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-    size_t rows, inv, seg_start, seg_req, cu_tiles, xm, a, q, o, h, u, part_o, part_ml, total;
+    size_t rows, inv, seg_start, seg_req, cu_tiles, xm, a, q, o, h, u, part_o, part_ml, gemm_part, total;
 };
 
-// Attention key-range split: enough workgroups to give every CU about two,
-// bounded by the partial buffers (split count x rows <= B*T).
-constexpr int kAttnTargetGroups = 512;
+// Attention key-range split: enough workgroups to give every CU two to three,
+// bounded by the partial buffers (split count x rows <= attn_part_rows).
+constexpr int kAttnTargetGroups = 640;
+
+size_t attn_part_rows(const ms_model_desc& d, int32_t B) {
+    const size_t BT = (size_t)B * ((size_t)d.n_text + (size_t)d.grid_h * d.grid_w);
+    return std::max(BT, (size_t)(131072 / d.n_heads));
+}
 
 int elt_bytes(int32_t dtype) { return dtype == MS_BF16 ? 2 : 4; }
 
@@ -102,8 +107,9 @@ Layout make_layout(const ms_model_desc& d, int32_t B) {
     L.o = take(BT * dm * e);
     L.h = take(BT * dm * e);
     L.u = take(BT * f * e);
-    L.part_o = take(BT * dm * 4);
-    L.part_ml = take(BT * (size_t)d.n_heads * 2 * 4);
+    L.part_o = take(attn_part_rows(d, B) * dm * 4);
+    L.part_ml = take(attn_part_rows(d, B) * (size_t)d.n_heads * 2 * 4);
+    L.gemm_part = take(ms::kGemmPartFloats * 4);
     L.total = off;
     return L;
 }
@@ -216,6 +222,15 @@ ms_status check_weights(const ms_step* s, const ms_layer_weights* w) {
     return MS_OK;
 }
 
+hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, hipStream_t st) {
+    const ms::GemmPlan p = ms::plan_gemm(s->desc.dtype, g.M, g.N, g.K, ms::kGemmPartFloats);
+    g.bm = p.bm;
+    g.bn = p.bn;
+    g.ksplit = p.ksplit;
+    g.part = static_cast<float*>(s->buf(s->lay.gemm_part));
+    return ms::launch_gemm(s->desc.dtype, g, st);
+}
+
 ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* kv, hipStream_t st) {
     if (s->M == 0) return MS_OK;
     const int dt = s->desc.dtype;
@@ -252,7 +267,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.lda = d; g.ldc = d; g.d = d;
         g.epilogue = ms::kEpiQKV;
         ProfScope p(MS_K_GEMM_QKV, st);
-        MS_HIP(ms::launch_gemm(dt, g, st));
+        MS_HIP(run_gemm(s, g, st));
     }
     ms::AttnDesc ad{};
     ad.q = q; ad.kv = kv; ad.o = o;
@@ -278,7 +293,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.M = r.r1 - r.r0; g.N = d; g.K = d; g.lda = d; g.ldr = d; g.ldc = d;
         g.epilogue = ms::kEpiBiasResid;
         ProfScope p(MS_K_GEMM_OUT, st);
-        MS_HIP(ms::launch_gemm(dt, g, st));
+        MS_HIP(run_gemm(s, g, st));
     }
     {
         ProfScope p(MS_K_LAYERNORM, st);
@@ -293,7 +308,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.M = r.r1 - r.r0; g.N = f; g.K = d; g.lda = d; g.ldc = f;
         g.epilogue = ms::kEpiBiasGelu;
         ProfScope p(MS_K_GEMM_UP, st);
-        MS_HIP(ms::launch_gemm(dt, g, st));
+        MS_HIP(run_gemm(s, g, st));
     }
     for (const Range& r : ranges) {
         if (r.r1 <= r.r0) continue;
@@ -303,7 +318,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.M = r.r1 - r.r0; g.N = d; g.K = f; g.lda = f; g.ldr = d; g.ldc = d;
         g.epilogue = ms::kEpiBiasResid;
         ProfScope p(MS_K_GEMM_DOWN, st);
-        MS_HIP(ms::launch_gemm(dt, g, st));
+        MS_HIP(run_gemm(s, g, st));
     }
     return MS_OK;
 }
@@ -426,7 +441,7 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
         int target = kAttnTargetGroups;
         if (const char* ev = std::getenv("MS_ATTN_SPLIT_TARGET")) target = std::max(1, std::atoi(ev));
         int ns = std::min(ntiles, std::max(1, (target + base - 1) / base));
-        if (s->M > 0) ns = std::min(ns, std::max(1, batch * s->T / s->M));
+        if (s->M > 0) ns = std::min(ns, std::max(1, (int)(attn_part_rows(*desc, batch) / s->M)));
         if (!ms::attention_fast_path(desc->dtype, s->hd)) ns = 1;
         const int tps = (ntiles + ns - 1) / ns;
         s->attn_tps = tps;
