@@ -121,6 +121,35 @@ def make_inputs(key, shape, n_masks, torch, W):
     return weights, masks, xs, ratios, kv_layers, slots, ycache, pinned
 
 
+# ----------------------------------------------------------------------------- measured HBM traffic
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+
+
+def measured_traffic(kernel: str):
+    """Calibrated HBM bytes per launch of `kernel` from a profiles/hbm_traffic_*.txt summary
+    (rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by a plain-copy calibration), or None
+    when there is none or the kernel's source changed since it was taken."""
+    import glob
+    import hashlib
+    for fn in sorted(glob.glob(os.path.join(ROOT, "profiles", "hbm_traffic_*.txt"))):
+        kv = {}
+        for line in open(fn):
+            if "=" in line and not line.startswith("#"):
+                k, v = line.strip().split("=", 1)
+                kv[k] = v
+        if kv.get("kernel") != kernel:
+            continue
+        src = os.path.join(ROOT, kv.get("source", ""))
+        if not os.path.exists(src):
+            continue
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        if sha != kv.get("source_sha256_16"):
+            return None
+        return {"bytes_per_launch": float(kv["hbm_bytes_per_launch"]), "file": os.path.relpath(fn, ROOT)}
+    return None
+
+
 # ----------------------------------------------------------------------------- CPU oracle
 
 
@@ -284,17 +313,28 @@ def main():
         dom = max((c for c in kernels if c in work), key=lambda c: kernels[c]["ms_total"])
         kind, amount = work[dom]
         t_s = kernels[dom]["ms_total"] / 1e3
+        hd = shape.d_model // shape.n_heads
+        kname = {"attention": f"attention_fast_kernel<{hd}>"}.get(dom, dom)
+        # algorithmic HBM bytes per launch of the dominant kernel
+        n_launch = kernels[dom]["launches"]
+        m_avg = tot_m_prof * L / n_launch
+        alg_bytes = {"attention": (4 * shape.batch * T * d + 4 * m_avg * d) * e / 2}.get(dom)
+        tr = measured_traffic(kname)
         if kind == "mfma":
             peak = PEAK["bf16_mfma_tflops"] if shape.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
             ach = amount / t_s / 1e12
             roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
-                    "frac": round(ach / peak, 4), "traffic": None, "kernel": dom,
-                    "per_launch_us": kernels[dom]["us_avg"]}
+                    "frac": round(ach / peak, 4)}
         else:
             ach = amount / t_s / 1e9
             roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK["hbm_gbs"], "unit": "GB/s",
-                    "frac": round(ach / PEAK["hbm_gbs"], 4), "traffic": None, "kernel": dom,
-                    "per_launch_us": kernels[dom]["us_avg"]}
+                    "frac": round(ach / PEAK["hbm_gbs"], 4)}
+        roof.update({"traffic": round(tr["bytes_per_launch"]) if tr else None,
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "traffic_source": tr["file"] if tr else None,
+                     "algorithmic_bytes_per_launch": round(alg_bytes) if alg_bytes else None,
+                     "kernel": kname, "per_launch_us": kernels[dom]["us_avg"],
+                     "algorithmic_flops_per_launch": round(amount / n_launch) if kind == "mfma" else None})
 
     cpu = None
     if not args.no_cpu_baseline:

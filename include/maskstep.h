@@ -194,7 +194,8 @@ void mask_step_destroy(ms_step* step);
 typedef enum {
     MS_K_COMPACT = 0, MS_K_GATHER = 1, MS_K_LAYERNORM = 2, MS_K_GEMM_QKV = 3,
     MS_K_ATTENTION = 4, MS_K_GEMM_OUT = 5, MS_K_GEMM_UP = 6, MS_K_GEMM_DOWN = 7,
-    MS_K_SCATTER = 8, MS_K_COPY = 9, MS_K_COUNT = 10
+    MS_K_SCATTER = 8, MS_K_COPY = 9, MS_K_ATTN_COMBINE = 10, MS_K_GEMM_REDUCE = 11,
+    MS_K_COUNT = 12
 } ms_kernel_class;
 
 ms_status mask_profiler_start(uint32_t class_mask, int32_t capacity);

@@ -567,10 +567,6 @@ hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s) {
             hipLaunchKernelGGL((attention_fast_kernel<72>), grid, block, 0, s, a);
         else
             hipLaunchKernelGGL((attention_fast_kernel<128>), grid, block, 0, s, a);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess || a.nsplit == 1) return e;
-        const long n4 = (long)a.M * a.d / 4;
-        hipLaunchKernelGGL(attention_combine_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, a);
         return hipGetLastError();
     }
     dim3 grid(a.n_qtiles, a.n_heads), block(kThreads);
@@ -587,6 +583,13 @@ hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s) {
         if (a.hd > 64) return hipErrorInvalidValue;
         hipLaunchKernelGGL((attention_kernel<float, 64>), grid, block, 0, s, a);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_combine(int dtype, const AttnDesc& a, hipStream_t s) {
+    if (a.M == 0 || a.nsplit <= 1 || !attention_fast_path(dtype, a.hd)) return hipSuccess;
+    const long n4 = (long)a.M * a.d / 4;
+    hipLaunchKernelGGL(attention_combine_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

@@ -238,9 +238,8 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats) 
     return p;
 }
 
-hipError_t launch_gemm(int dtype, const GemmDesc& gin, hipStream_t s) {
-    if (gin.M == 0) return hipSuccess;
-    GemmDesc g = gin;
+hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
+    if (g.M == 0) return hipSuccess;
     const int bk = dtype == kBF16 ? 64 : 32;
     if (g.ksplit < 1) g.ksplit = 1;
     // K range per split, a multiple of the K step
@@ -254,12 +253,15 @@ hipError_t launch_gemm(int dtype, const GemmDesc& gin, hipStream_t s) {
         else if (g.bm == 128 && g.bn == 64) e = launch_tile<bf16_t, 128, 64>(g, s);
         else if (g.bm == 64 && g.bn == 128) e = launch_tile<bf16_t, 64, 128>(g, s);
         else e = launch_tile<bf16_t, 64, 64>(g, s);
-        if (e == hipSuccess && g.ksplit > 1) e = launch_reduce<bf16_t>(g, s);
     } else {
         e = launch_tile<float, 64, 64>(g, s);
-        if (e == hipSuccess && g.ksplit > 1) e = launch_reduce<float>(g, s);
     }
     return e;
+}
+
+hipError_t launch_gemm_reduce(int dtype, const GemmDesc& g, hipStream_t s) {
+    if (g.M == 0 || g.ksplit <= 1) return hipSuccess;
+    return dtype == kBF16 ? launch_reduce<bf16_t>(g, s) : launch_reduce<float>(g, s);
 }
 
 }  // namespace ms

@@ -61,8 +61,10 @@ constexpr size_t kGemmPartFloats = size_t(4) << 20;
 // Tile shape and K split for an M x N x K product on 256 CUs.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats);
 
-// a4/a5/a7/a8/a9: out = epi(A W^T + bias).
-hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t s);
+// a4/a5/a7/a8/a9: out = epi(A W^T + bias); with ksplit > 1 only the partials
+// (launch_gemm_reduce applies the epilogue). launch_gemm sets g.kchunk/ksplit.
+hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s);
+hipError_t launch_gemm_reduce(int dtype, const GemmDesc& g, hipStream_t s);
 
 struct AttnDesc {
     const void* q;        // [M][d]
@@ -84,7 +86,11 @@ struct AttnDesc {
 // True when launch_attention uses the bf16 fast kernel for this head_dim.
 bool attention_fast_path(int dtype, int hd);
 
-// a6: attention of the packed masked queries over every key of their request.
+// a6: attention of the packed masked queries over every key of their request
+// (when the key range is split, the partials are left for launch_attention_combine).
 hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s);
+
+// Combine of the key-range partials (no-op when nsplit == 1).
+hipError_t launch_attention_combine(int dtype, const AttnDesc& a, hipStream_t s);
 
 }  // namespace ms

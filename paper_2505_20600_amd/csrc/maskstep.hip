@@ -222,13 +222,20 @@ ms_status check_weights(const ms_step* s, const ms_layer_weights* w) {
     return MS_OK;
 }
 
-hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, hipStream_t st) {
+hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, int cls, hipStream_t st) {
     const ms::GemmPlan p = ms::plan_gemm(s->desc.dtype, g.M, g.N, g.K, ms::kGemmPartFloats);
     g.bm = p.bm;
     g.bn = p.bn;
     g.ksplit = p.ksplit;
     g.part = static_cast<float*>(s->buf(s->lay.gemm_part));
-    return ms::launch_gemm(s->desc.dtype, g, st);
+    hipError_t e;
+    {
+        ProfScope prof(cls, st);
+        e = ms::launch_gemm(s->desc.dtype, g, st);
+    }
+    if (e != hipSuccess || g.ksplit <= 1) return e;
+    ProfScope prof(MS_K_GEMM_REDUCE, st);
+    return ms::launch_gemm_reduce(s->desc.dtype, g, st);
 }
 
 ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* kv, hipStream_t st) {
@@ -266,8 +273,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.M = r.r1 - r.r0; g.N = 3 * d; g.K = d;
         g.lda = d; g.ldc = d; g.d = d;
         g.epilogue = ms::kEpiQKV;
-        ProfScope p(MS_K_GEMM_QKV, st);
-        MS_HIP(run_gemm(s, g, st));
+        MS_HIP(run_gemm(s, g, MS_K_GEMM_QKV, st));
     }
     ms::AttnDesc ad{};
     ad.q = q; ad.kv = kv; ad.o = o;
@@ -285,6 +291,10 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         ProfScope p(MS_K_ATTENTION, st);
         MS_HIP(ms::launch_attention(dt, ad, st));
     }
+    {
+        ProfScope p(MS_K_ATTN_COMBINE, st);
+        MS_HIP(ms::launch_attention_combine(dt, ad, st));
+    }
     for (const Range& r : ranges) {
         if (r.r1 <= r.r0) continue;
         ms::GemmDesc g{};
@@ -292,8 +302,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.R = x + (size_t)r.r0 * d * e; g.C = h + (size_t)r.r0 * d * e;
         g.M = r.r1 - r.r0; g.N = d; g.K = d; g.lda = d; g.ldr = d; g.ldc = d;
         g.epilogue = ms::kEpiBiasResid;
-        ProfScope p(MS_K_GEMM_OUT, st);
-        MS_HIP(run_gemm(s, g, st));
+        MS_HIP(run_gemm(s, g, MS_K_GEMM_OUT, st));
     }
     {
         ProfScope p(MS_K_LAYERNORM, st);
@@ -307,8 +316,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.C = u + (size_t)r.r0 * f * e;
         g.M = r.r1 - r.r0; g.N = f; g.K = d; g.lda = d; g.ldc = f;
         g.epilogue = ms::kEpiBiasGelu;
-        ProfScope p(MS_K_GEMM_UP, st);
-        MS_HIP(run_gemm(s, g, st));
+        MS_HIP(run_gemm(s, g, MS_K_GEMM_UP, st));
     }
     for (const Range& r : ranges) {
         if (r.r1 <= r.r0) continue;
@@ -317,8 +325,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.R = h + (size_t)r.r0 * d * e; g.C = x + (size_t)r.r0 * d * e;
         g.M = r.r1 - r.r0; g.N = d; g.K = f; g.lda = f; g.ldr = d; g.ldc = d;
         g.epilogue = ms::kEpiBiasResid;
-        ProfScope p(MS_K_GEMM_DOWN, st);
-        MS_HIP(run_gemm(s, g, st));
+        MS_HIP(run_gemm(s, g, MS_K_GEMM_DOWN, st));
     }
     return MS_OK;
 }

@@ -94,7 +94,7 @@ EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask
             "mask_profiler_start", "mask_profiler_stop")
 
 KERNEL_CLASSES = ("compact", "gather", "layernorm", "gemm_qkv", "attention", "gemm_out", "gemm_up",
-                  "gemm_down", "scatter", "copy")
+                  "gemm_down", "scatter", "copy", "attn_combine", "gemm_reduce")
 
 
 def profiler_start(classes=KERNEL_CLASSES, capacity: int = 65536):
