@@ -100,6 +100,23 @@ __device__ __forceinline__ int xcd_logical_block(int hw, int total) {
     return x * per + min(x, rem) + i;
 }
 
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
+// lane i's 16 bytes land at lds + 16 * i; `lds` must be the same for the whole wave.
+__device__ __forceinline__ void load_lds16(const void* g, void* lds) {
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds), 16, 0, 0);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (<= n, n < 64).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x3f70 | (N & 15) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without the memory fence of __syncthreads (callers order
+// their own memory operations with explicit waits).
+__device__ __forceinline__ void barrier_only() { __builtin_amdgcn_s_barrier(); }
+
 // 2^x with the hardware v_exp_f32 (no denormal-result fix-up: softmax
 // weights below 2^-126 of the running maximum are irrelevant).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

@@ -21,6 +21,9 @@
 // not, the K range is split over workgroups that write float32 partials,
 // summed in a fixed order by a second kernel that applies the epilogue.
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
 
 #include "common.h"
 #include "kernels.h"
@@ -133,17 +136,17 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
 #pragma unroll
         for (int ks = 0; ks < BK / E::kKStep; ++ks) {
             const int kk = ks * E::kKStep + (lane / 16) * E::kKPerLane;
-            frag_t fw[SN], fa[SM];
-#pragma unroll
-            for (int i = 0; i < SN; ++i)
-                fw[i] = *reinterpret_cast<const frag_t*>(&sW[buf][(wn * (BN / 2) + i * 16 + lane % 16) * LDS + kk]);
+            // all activation fragments, then one weight fragment at a time
+            frag_t fa[SM];
 #pragma unroll
             for (int j = 0; j < SM; ++j)
                 fa[j] = *reinterpret_cast<const frag_t*>(&sA[buf][(wm * (BM / 2) + j * 16 + lane % 16) * LDS + kk]);
 #pragma unroll
-            for (int i = 0; i < SN; ++i)
+            for (int i = 0; i < SN; ++i) {
+                const frag_t fw = *reinterpret_cast<const frag_t*>(&sW[buf][(wn * (BN / 2) + i * 16 + lane % 16) * LDS + kk]);
 #pragma unroll
-                for (int j = 0; j < SM; ++j) acc[i][j] = E::mma(fw[i], fa[j], acc[i][j]);
+                for (int j = 0; j < SM; ++j) acc[i][j] = E::mma(fw, fa[j], acc[i][j]);
+            }
         }
         if (kt + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
@@ -160,6 +163,119 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
             float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
             if (g.ksplit == 1) {
                 epilogue_store<T, EPI>(g, m, n, v);
+            } else {
+                *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) =
+                    make_float4(v[0], v[1], v[2], v[3]);
+            }
+        }
+    }
+}
+
+// bf16 main loop with direct global->LDS loads (gfx950 global_load_lds_dwordx4)
+// into S LDS stages, so S-1 K steps are in flight without staging registers.
+// LDS rows are 128 bytes (one K step of 64 bf16) with their eight 16-byte
+// chunks XOR-swizzled by (row >> 1) & 7: each load instruction fills 1 KB
+// (8 rows) contiguously, and the 16-row MFMA fragment reads of one K chunk
+// still touch 16 distinct bank groups.
+template <int BM, int BN, int S, int EPI>
+__global__ __launch_bounds__(kThreads) void gemm_dl_kernel(GemmDesc g) {
+    using E = Elt<bf16_t>;
+    using frag_t = typename E::frag_t;
+    constexpr int BK = 64;
+    constexpr int ROWE = 64;                    // elements per LDS row
+    constexpr int IPW = (BM + BN) / 32;         // 1 KB load instructions per wave per stage
+    constexpr int IA = BM / 32;                 // of which for the activation tile
+    constexpr int SM = BM / 32;
+    constexpr int SN = BN / 32;
+    __shared__ __attribute__((aligned(1024))) bf16_t sA[S][BM * ROWE];
+    __shared__ __attribute__((aligned(1024))) bf16_t sW[S][BN * ROWE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid % kWave;
+    const int wave = tid / kWave;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int M = g.M, N = g.N, K = g.K;
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    const int lb = xcd_logical_block(blockIdx.x, tiles_m * tiles_n * g.ksplit);
+    const int kz = lb / (tiles_m * tiles_n);
+    const int n0 = ((lb / tiles_m) % tiles_n) * BN;
+    const int m0 = (lb % tiles_m) * BM;
+    const int kbeg = kz * g.kchunk;
+    const int kend = min(K, kbeg + g.kchunk);
+    const int nk = (kend - kbeg) / BK;
+    const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.A);
+    const bf16_t* __restrict__ W = static_cast<const bf16_t*>(g.W);
+
+    // per load instruction: this lane's element offset (row * ld + swizzled chunk)
+    int goff[IPW];
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+        const int blk = i * 4 + wave;                       // 8-row block
+        const bool isA = i < IA;
+        const int rloc = (isA ? blk : blk - BM / 8) * 8 + lane / 8;
+        const int c = (lane % 8) ^ ((rloc >> 1) & 7);
+        if (isA) goff[i] = min(m0 + rloc, M - 1) * g.lda + c * 8;
+        else goff[i] = min(n0 + rloc, N - 1) * K + c * 8;
+    }
+    auto issue = [&](int kt, int st) {
+        const int k0 = kbeg + kt * BK;
+#pragma unroll
+        for (int i = 0; i < IPW; ++i) {
+            const int blk = i * 4 + wave;
+            if (i < IA)
+                load_lds16(A + goff[i] + k0, &sA[st][blk * 512]);
+            else
+                load_lds16(W + goff[i] + k0, &sW[st][(blk - BM / 8) * 512]);
+        }
+    };
+
+    f32x4_t acc[SN][SM];
+#pragma unroll
+    for (int i = 0; i < SN; ++i)
+#pragma unroll
+        for (int j = 0; j < SM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // fragment offsets inside a stage: row r, logical chunk ks*4 + grp, swizzled by (r >> 1) & 7
+    const int sw = (lane % 16) >> 1;
+    const int grp = lane / 16;
+
+#pragma unroll
+    for (int st = 0; st < S - 1; ++st)
+        if (st < nk) issue(st, st);
+    for (int kt = 0; kt < nk; ++kt) {
+        const int st = kt % S;
+        // stage kt complete: allow the loads of the stages issued after it
+        if (kt + S - 1 <= nk) wait_vmcnt<(S - 2) * IPW>();
+        else wait_vmcnt<0>();
+        barrier_only();
+        if (kt + S - 1 < nk) issue(kt + S - 1, (kt + S - 1) % S);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int ch = ((ks * 4 + grp) ^ sw) * 8;
+            frag_t fa[SM];
+#pragma unroll
+            for (int j = 0; j < SM; ++j)
+                fa[j] = *reinterpret_cast<const frag_t*>(&sA[st][(wm * (BM / 2) + j * 16 + lane % 16) * ROWE + ch]);
+#pragma unroll
+            for (int i = 0; i < SN; ++i) {
+                const frag_t fw = *reinterpret_cast<const frag_t*>(&sW[st][(wn * (BN / 2) + i * 16 + lane % 16) * ROWE + ch]);
+#pragma unroll
+                for (int j = 0; j < SM; ++j) acc[i][j] = E::mma(fw, fa[j], acc[i][j]);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int i = 0; i < SN; ++i) {
+        const int n = n0 + wn * (BN / 2) + i * 16 + grp * 4;
+        if (n >= N) continue;
+#pragma unroll
+        for (int j = 0; j < SM; ++j) {
+            const int m = m0 + wm * (BM / 2) + j * 16 + lane % 16;
+            if (m >= M) continue;
+            float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+            if (g.ksplit == 1) {
+                epilogue_store<bf16_t, EPI>(g, m, n, v);
             } else {
                 *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) =
                     make_float4(v[0], v[1], v[2], v[3]);
@@ -197,6 +313,19 @@ hipError_t launch_tile(const GemmDesc& g, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int BM, int BN, int S>
+hipError_t launch_dl(const GemmDesc& g, hipStream_t s) {
+    dim3 grid(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM) * g.ksplit), block(kThreads);
+    switch (g.epilogue) {
+        case kEpiBias: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiBias>), grid, block, 0, s, g); break;
+        case kEpiBiasResid: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiBiasResid>), grid, block, 0, s, g); break;
+        case kEpiBiasGelu: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiBiasGelu>), grid, block, 0, s, g); break;
+        case kEpiQKV: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiQKV>), grid, block, 0, s, g); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_reduce(const GemmDesc& g, hipStream_t s) {
     const long n4 = (long)g.M * g.N / 4;
@@ -217,24 +346,34 @@ long groups(const GemmDesc& g, int bm, int bn) {
 
 }  // namespace
 
+// Tile choice measured on MI355X (bf16, 2-stage direct-to-LDS main loop):
+// 128x128 sustains the most per CU once the grid has enough groups to give
+// every CU at least one (and to keep the last round's quantisation small);
+// smaller problems run 64x64 tiles, split over K when even those leave CUs idle.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats) {
     GemmPlan p{64, 64, 1};
     if (dtype != kBF16) return p;   // fp32 path: one tile shape
     GemmDesc g{};
     g.M = M; g.N = N;
-    static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
-    for (const auto& c : cand) {
-        if (groups(g, c[0], c[1]) >= kCUs) {
-            p.bm = c[0]; p.bn = c[1];
-            return p;
+    if (groups(g, 128, 128) >= (3 * kCUs) / 2) {
+        p.bm = 128; p.bn = 128;
+    } else {
+        const long grp = groups(g, 64, 64);
+        if (grp < kCUs) {
+            int ks = (int)((2 * kCUs + grp - 1) / grp);
+            ks = std::min(ks, std::max(1, K / 256));
+            while (ks > 1 && (size_t)ks * M * N > part_capacity_floats) --ks;
+            p.ksplit = std::max(1, ks);
         }
     }
-    // even 64 x 64 leaves CUs idle: split K (each split keeps >= 4 K steps of 64)
-    const long base = groups(g, 64, 64);
-    int ks = (int)((2 * kCUs + base - 1) / base);
-    ks = std::min(ks, std::max(1, K / 256));
-    while (ks > 1 && (size_t)ks * M * N > part_capacity_floats) --ks;
-    p.ksplit = std::max(1, ks);
+    if (const char* f = std::getenv("MS_GEMM_TILE")) {   // tuning override "BMxBN"
+        int bm = 0, bn = 0;
+        if (std::sscanf(f, "%dx%d", &bm, &bn) == 2) {
+            const int ok[6][2] = {{256, 256}, {256, 128}, {128, 128}, {128, 64}, {64, 128}, {64, 64}};
+            for (const auto& t : ok)
+                if (t[0] == bm && t[1] == bn) { p.bm = bm; p.bn = bn; p.ksplit = 1; }
+        }
+    }
     return p;
 }
 
@@ -248,11 +387,35 @@ hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
     g.kchunk = per * bk;
     g.ksplit = (steps + per - 1) / per;
     hipError_t e;
-    if (dtype == kBF16) {
-        if (g.bm == 128 && g.bn == 128) e = launch_tile<bf16_t, 128, 128>(g, s);
+    // main loop: direct-to-LDS with 2 stages (default); tuning knob MS_GEMM_PIPE =
+    // "staged" (register-staged double buffer) or "dl4" (direct-to-LDS, 2-4 stages)
+    static const int pipe = [] {
+        const char* v = std::getenv("MS_GEMM_PIPE");
+        if (!v) return 2;
+        return std::strcmp(v, "staged") == 0 ? 0 : std::strcmp(v, "dl4") == 0 ? 4 : 2;
+    }();
+    if (dtype == kBF16 && pipe == 2) {
+        if (g.bm == 256 && g.bn == 256) e = launch_dl<256, 256, 2>(g, s);
+        else if (g.bm == 256 && g.bn == 128) e = launch_dl<256, 128, 2>(g, s);
+        else if (g.bm == 128 && g.bn == 128) e = launch_dl<128, 128, 2>(g, s);
+        else if (g.bm == 128 && g.bn == 64) e = launch_dl<128, 64, 2>(g, s);
+        else if (g.bm == 64 && g.bn == 128) e = launch_dl<64, 128, 2>(g, s);
+        else e = launch_dl<64, 64, 2>(g, s);
+    } else if (dtype == kBF16 && pipe == 0) {
+        if (g.bm == 256 && g.bn == 256) e = launch_tile<bf16_t, 256, 256>(g, s);
+        else if (g.bm == 256 && g.bn == 128) e = launch_tile<bf16_t, 256, 128>(g, s);
+        else if (g.bm == 128 && g.bn == 128) e = launch_tile<bf16_t, 128, 128>(g, s);
         else if (g.bm == 128 && g.bn == 64) e = launch_tile<bf16_t, 128, 64>(g, s);
         else if (g.bm == 64 && g.bn == 128) e = launch_tile<bf16_t, 64, 128>(g, s);
         else e = launch_tile<bf16_t, 64, 64>(g, s);
+    } else if (dtype == kBF16) {
+        // direct-to-LDS stages: 256x256 64 KB x 2; 256x128 48 KB x 3; 128x128 32 KB x 4; smaller x 4
+        if (g.bm == 256 && g.bn == 256) e = launch_dl<256, 256, 2>(g, s);
+        else if (g.bm == 256 && g.bn == 128) e = launch_dl<256, 128, 3>(g, s);
+        else if (g.bm == 128 && g.bn == 128) e = launch_dl<128, 128, 4>(g, s);
+        else if (g.bm == 128 && g.bn == 64) e = launch_dl<128, 64, 4>(g, s);
+        else if (g.bm == 64 && g.bn == 128) e = launch_dl<64, 128, 4>(g, s);
+        else e = launch_dl<64, 64, 4>(g, s);
     } else {
         e = launch_tile<float, 64, 64>(g, s);
     }

@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "../../include/maskstep.h"
+#include "../../include/maskstep_ops.h"
 #include "kernels.h"
 
 namespace {
@@ -616,6 +617,49 @@ void mask_step_destroy(ms_step* s) {
     if (!s) return;
     destroy_events(s);
     delete s;
+}
+
+ms_status ms_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, const void* W,
+                    const void* bias, const void* resid, void* out, int32_t epilogue,
+                    int32_t tile_m, int32_t tile_n, int32_t ksplit, void* d_ws, size_t ws_bytes,
+                    void* stream) {
+    if (dtype != MS_FP32 && dtype != MS_BF16) return fail(MS_EDTYPE, "unknown dtype %d", dtype);
+    if (M < 0 || N < 4 || K < 1 || N % 4) return fail(MS_ESHAPE, "need M >= 0, N a positive multiple of 4");
+    const int bk = dtype == MS_BF16 ? 64 : 32;
+    if (K % bk) return fail(MS_ESHAPE, "K must be a multiple of %d", bk);
+    if (epilogue < MS_EPI_BIAS || epilogue > MS_EPI_BIAS_GELU) return fail(MS_EINVAL, "unknown epilogue %d", epilogue);
+    if (!A || !W || !bias || !out || (epilogue == MS_EPI_BIAS_RESID && !resid))
+        return fail(MS_EINVAL, "NULL operand");
+    if (!aligned16(A) || !aligned16(W) || !aligned16(bias) || !aligned16(out) || !aligned16(resid) ||
+        !aligned16(d_ws))
+        return fail(MS_EALIGN, "operand not 16-byte aligned");
+    if (ksplit < 0) return fail(MS_EINVAL, "ksplit must be >= 0");
+    ms::GemmPlan p = ms::plan_gemm(dtype, M, N, K, d_ws ? ws_bytes / 4 : 0);
+    if (tile_m || tile_n) {
+        const int ok_tiles[6][2] = {{256, 256}, {256, 128}, {128, 128}, {128, 64}, {64, 128}, {64, 64}};
+        bool ok = false;
+        for (const auto& t : ok_tiles) ok |= (t[0] == tile_m && t[1] == tile_n);
+        if (!ok || (dtype == MS_FP32 && !(tile_m == 64 && tile_n == 64)))
+            return fail(MS_EINVAL, "unsupported tile %dx%d", tile_m, tile_n);
+        p.bm = tile_m;
+        p.bn = tile_n;
+        p.ksplit = 1;
+    }
+    if (ksplit > 0) p.ksplit = ksplit;
+    if (p.ksplit > 1 && (!d_ws || ws_bytes < (size_t)p.ksplit * M * N * 4))
+        return fail(MS_EWORKSPACE, "split-K needs %zu bytes of workspace", (size_t)p.ksplit * M * N * 4);
+    if (M == 0) return ok();
+    ms::GemmDesc g{};
+    g.A = A; g.W = W; g.bias = bias; g.R = resid; g.C = out;
+    g.M = M; g.N = N; g.K = K; g.lda = K; g.ldr = N; g.ldc = N;
+    g.epilogue = epilogue == MS_EPI_BIAS ? ms::kEpiBias
+               : epilogue == MS_EPI_BIAS_RESID ? ms::kEpiBiasResid : ms::kEpiBiasGelu;
+    g.bm = p.bm; g.bn = p.bn; g.ksplit = p.ksplit;
+    g.part = static_cast<float*>(d_ws);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    MS_HIP(ms::launch_gemm(dtype, g, st));
+    MS_HIP(ms::launch_gemm_reduce(dtype, g, st));
+    return ok();
 }
 
 ms_status mask_profiler_start(uint32_t class_mask, int32_t capacity) {

@@ -78,6 +78,7 @@ def load() -> C.CDLL:
                                          vp, vp, vp]),
             "mask_step_destroy": (None, [vp]),
             "mask_profiler_start": (i32, [C.c_uint32, i32]),
+            "ms_linear": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, sz, vp]),
             "mask_profiler_stop": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
         }
         for name, (res, args) in sig.items():
@@ -91,7 +92,20 @@ def load() -> C.CDLL:
 EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask_step_init",
             "mask_step_get_info", "mask_step_index", "mask_gather_rows", "mask_block_forward",
             "mask_scatter_rows", "cache_prefetch_layer", "mask_stack_forward", "mask_step_destroy",
-            "mask_profiler_start", "mask_profiler_stop")
+            "mask_profiler_start", "mask_profiler_stop", "ms_linear")
+
+MS_EPI_BIAS, MS_EPI_BIAS_RESID, MS_EPI_BIAS_GELU = 0, 1, 2
+
+
+def ms_linear(A, W, bias, out, *, resid=None, epilogue=MS_EPI_BIAS, tile=(0, 0), ksplit=0,
+              workspace=None, stream=None):
+    """out = epilogue(A W^T + bias (+ resid)) through the library's GEMM kernels."""
+    M, K = A.shape
+    N = W.shape[0]
+    dt = MS_BF16 if A.dtype == torch.bfloat16 else MS_FP32
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load().ms_linear(dt, M, N, K, _ptr(A), _ptr(W), _ptr(bias), _ptr(resid), _ptr(out), epilogue,
+                            tile[0], tile[1], ksplit, _ptr(workspace), ws_bytes, _stream(stream)))
 
 KERNEL_CLASSES = ("compact", "gather", "layernorm", "gemm_qkv", "attention", "gemm_out", "gemm_up",
                   "gemm_down", "scatter", "copy", "attn_combine", "gemm_reduce")
