@@ -18,3 +18,4 @@ from .stack import (  # noqa: F401
     masked_tokens,
     rounder,
 )
+from .planner import best_dense_prefix, greedy_choice, pipeline_latency  # noqa: F401

@@ -256,7 +256,8 @@ def dense_stack(x, weights, shape):
     return y, kv
 
 
-def masked_stack(x, mask, kv_cache, y_cache, weights, shape, return_kv: bool = False):
+def masked_stack(x, mask, kv_cache, y_cache, weights, shape, return_kv: bool = False,
+                 dense_prefix: int = 0):
     """Mask-aware step with K/V caching (Sec. 3.1, Fig. 5 bottom and Fig. 7).
 
     ``kv_cache[l]`` is ``[B][T][2][d]`` (rows of recomputed tokens are ignored),
@@ -264,24 +265,41 @@ def masked_stack(x, mask, kv_cache, y_cache, weights, shape, return_kv: bool = F
     are touched; the output's other rows are copied from ``y_cache``.
     With ``return_kv`` the per-layer working K/V (cache with fresh rows) is
     returned too.
+
+    ``dense_prefix = k`` computes blocks ``0..k-1`` over every token without
+    the cache (the "compute all tokens" choice of the bubble-free pipeline,
+    Sec. 4.2 and Alg. 1) and blocks ``k..L-1`` with the cache. With K/V
+    caching a block can only skip the cache if all earlier blocks did (only
+    then do the unmasked tokens' hidden states exist), so the choice is a
+    prefix.
     """
     rnd = rounder(shape.dtype)
     x = np.asarray(x, np.float64)
     B, T, d = x.shape
+    L = len(weights)
+    k = int(dense_prefix)
+    if not 0 <= k <= L:
+        raise ValueError("dense_prefix out of range")
     y = np.array(y_cache, dtype=np.float64, copy=True)
     kv_out = [] if return_kv else None
     if return_kv:
-        kv_out = np.empty((len(weights), B, T, 2, d), np.float64)
+        kv_out = np.empty((L, B, T, 2, d), np.float64)
+    all_toks = np.arange(T)
     for b in range(B):
         toks = masked_tokens(mask[b], shape.n_text)
         if toks.size == 0:
             if return_kv:
-                for l in range(len(weights)):
+                for l in range(L):
                     kv_out[l, b] = kv_cache[l][b]
             continue
-        xm = x[b, toks]
-        for l, w in enumerate(weights):
-            xm, kvw = block_rows(xm, toks, w, kv_cache[l][b], shape, rnd)
+        xb = x[b]
+        for l in range(k):
+            xb, kvw = block_rows(xb, all_toks, weights[l], np.zeros((T, 2, d)), shape, rnd)
+            if return_kv:
+                kv_out[l, b] = kvw
+        xm = xb[toks]
+        for l in range(k, L):
+            xm, kvw = block_rows(xm, toks, weights[l], kv_cache[l][b], shape, rnd)
             if return_kv:
                 kv_out[l, b] = kvw
         y[b, toks] = xm
