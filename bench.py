@@ -54,6 +54,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-profile-pass", action="store_true")
+    p.add_argument("--prefix", default="auto",
+                   help="dense-prefix blocks for streamed caches: 'auto' (Alg. 1 planner on measured "
+                        "per-block costs) or a fixed count")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device copy (HBM counter calibration) and exit")
     return p.parse_args()
@@ -116,7 +119,8 @@ def make_inputs(key, shape, n_masks, torch, W):
             del t
         else:
             kv_layers.append(t)
-    slots = [torch.empty((B, T, 2, d), dtype=tdt, device=dev) for _ in range(2)] if pinned else (None, None)
+    # one device slot per layer: every cached layer's load can start at once
+    slots = [torch.empty((B, T, 2, d), dtype=tdt, device=dev) for _ in range(shape.n_layers)] if pinned else []
     ycache = torch.randn((B, T, d), generator=g, device=dev).to(tdt)
     return weights, masks, xs, ratios, kv_layers, slots, ycache, pinned
 
@@ -242,17 +246,58 @@ def main():
     stream = torch.cuda.current_stream()
     copy_stream = torch.cuda.Stream() if pinned else None
     Ms = []
+    prefix = [0] * args.masks
+    plan_info = []
 
     def one_step(i):
         st = MS.MaskStep(desc, shape.batch, masks[i], ws, stream)
+        if prefix[i]:
+            st.set_dense_prefix(prefix[i], stream)
         st.stack_forward(wc, xs[i], ycache, kv_layers, y, pinned=pinned, slots=slots, stream=stream,
                          copy_stream=copy_stream)
         m = st.info().rows
         st.close()
         return m
 
+    def timed_once(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
     for i in range(args.masks):
         Ms.append(one_step(i))
+    if pinned and args.prefix == "auto":
+        # Alg. 1 inputs per mask set, measured on this GPU: one block over every token, one
+        # block over the masked rows (cache resident), one block's cache load
+        L = shape.n_layers
+        for i in range(args.masks):
+            st = MS.MaskStep(desc, shape.batch, masks[i], ws, stream)
+            run = lambda: st.stack_forward(wc, xs[i], ycache, slots, y, pinned=False, stream=stream)
+            run()
+            cached_ms = min(timed_once(run) for _ in range(2)) / L
+            st.set_dense_prefix(L, stream)
+            run()
+            full_ms = min(timed_once(run) for _ in range(2)) / L
+            st.set_dense_prefix(0, stream)
+            MS.profiler_start(("copy",))
+            st.stack_forward(wc, xs[i], ycache, kv_layers, y, pinned=True, slots=slots, stream=stream,
+                             copy_stream=copy_stream)
+            torch.cuda.synchronize()
+            prof = MS.profiler_stop()
+            load_ms = prof["copy"][0] / max(1, prof["copy"][1]) if "copy" in prof else 0.0
+            st.close()
+            k, model_ms = MS.mask_plan_dense_prefix(L, load_ms, cached_ms, full_ms)
+            prefix[i] = k
+            plan_info.append({"ratio": round(ratios[i], 4), "load_ms": round(load_ms, 4),
+                              "cached_ms": round(cached_ms, 4), "full_ms": round(full_ms, 4),
+                              "dense_prefix": k, "modelled_ms": round(model_ms, 3)})
+        log(f"[bench] dense-prefix plan: {plan_info}")
+    elif args.prefix != "auto":
+        prefix = [int(args.prefix)] * args.masks
     for i in range(args.warmup):
         one_step(i % args.masks)
     torch.cuda.synchronize()
@@ -279,7 +324,8 @@ def main():
     per_mask = {}
     for s, t in enumerate(step_ms):
         per_mask.setdefault(s % args.masks, []).append(t)
-    per_ratio = sorted([[round(ratios[i], 4), int(Ms[i]), round(float(np.median(v)), 4)] for i, v in per_mask.items()])
+    per_ratio = sorted([[round(ratios[i], 4), int(Ms[i]), round(float(np.median(v)), 4), prefix[i]]
+                        for i, v in per_mask.items()])
 
     # profiled pass: per-kernel event timing over a second timed region
     kernels, roof = {}, None
@@ -358,7 +404,8 @@ def main():
         "config": {"workload": f"{shape.name}: {DESCR[key]}", "global_batch": shape.batch,
                    "seq_len": shape.n_tokens, "parallelism": "none (1 GPU)",
                    "masks": args.masks, "mean_masked_rows": round(float(np.mean(Ms)), 1)},
-        "per_mask": {"columns": ["ratio", "masked_rows", "median_ms"], "rows": per_ratio},
+        "per_mask": {"columns": ["ratio", "masked_rows", "median_ms", "dense_prefix"], "rows": per_ratio},
+        "prefix_plan": plan_info or None,
         "roofline": roof,
         "kernels": kernels,
         "cpu_baseline": cpu,

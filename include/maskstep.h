@@ -94,13 +94,18 @@ typedef enum { MS_KV_DEVICE = 0, MS_KV_HOST_PINNED = 1 } ms_kv_kind;
  *                     HBM; it is also the working buffer, so the masked rows
  *                     are overwritten with fresh K/V during the step.
  *  MS_KV_HOST_PINNED: layer[l] is a pinned host [B][N][2][d] buffer (image
- *                     tokens); slot[0], slot[1] are device [B][T][2][d]
- *                     buffers that layers alternate through (layer l uses
- *                     slot[l % 2]); loads run on the copy stream. */
+ *                     tokens). slots[0..n_slots-1] are device [B][T][2][d]
+ *                     buffers; the j-th cached layer of the step uses
+ *                     slots[j % n_slots], and its load (on the copy stream)
+ *                     waits until the compute stream has finished with the
+ *                     layer that used the slot before. With n_slots >= the
+ *                     number of cached layers every load starts at once
+ *                     (MI355X's HBM holds a whole stack's K/V easily). */
 typedef struct {
     int32_t kind;
     const void* const* layer;   /* [n_layers] */
-    void* slot[2];
+    int32_t n_slots;            /* MS_KV_HOST_PINNED only, >= 1 */
+    void* const* slots;         /* [n_slots], MS_KV_HOST_PINNED only */
 } ms_kv_source;
 
 typedef struct ms_step ms_step;   /* opaque host object, one per mask set */
@@ -111,6 +116,7 @@ typedef struct {
     int32_t n_segments;  /* packed segments (one per request, two with dual_stream) */
     int32_t n_qtiles;    /* attention query tiles */
     int32_t text_rows;   /* packed rows that use the text weight set */
+    int32_t dense_prefix;/* blocks computed over every token (mask_step_set_dense_prefix) */
 } ms_step_info;
 
 /* Bytes of device workspace a step over `batch` requests needs (worst case,
@@ -134,6 +140,27 @@ ms_status mask_step_get_info(const ms_step* step, ms_step_info* info);
  * [n_segments + 1] (packed offset of each segment). Valid until destroy. */
 ms_status mask_step_index(const ms_step* step, const int32_t** d_rows, const int32_t** d_inv,
                           const int32_t** d_seg_start);
+
+/* Bubble-free pipeline loading (Sec. 4.2, Alg. 1). A block may skip its
+ * cache and compute every token instead; with K/V caching that is possible
+ * only while every earlier block did the same (only then do the unmasked
+ * tokens' hidden states exist), so the choice is a prefix: blocks [0, k)
+ * over every token (no cache read, fresh K/V of all tokens in a workspace
+ * buffer), blocks [k, n_layers) with the cache. mask_stack_forward follows
+ * the step's current k (0 after init). The first call with k > 0 enqueues,
+ * on `stream`, the construction of the every-token row layout in the
+ * workspace. */
+ms_status mask_step_set_dense_prefix(ms_step* step, int32_t k, void* stream);
+
+/* Alg. 1's latency model over the prefix choices: with per-block load time
+ * load_ms (cached activations of one block over the copy link), compute
+ * time cached_ms (masked rows only) and full_ms (every token), a cached
+ * block's load follows the previous load and its compute waits for it; a
+ * full block needs no load. Returns in *k_out the prefix length with the
+ * smallest modelled latency (the smallest such k on ties) and that latency
+ * in *latency_ms_out (may be NULL). Host-only. */
+ms_status mask_plan_dense_prefix(int32_t n_layers, double load_ms, double cached_ms, double full_ms,
+                                 int32_t* k_out, double* latency_ms_out);
 
 /* Row gather ("extract the matrix of masked tokens", Sec. 3.1):
  * d_xm[m] = d_x[rows[m]]; d_x [B][T][d], d_xm [M][d] (may be NULL: the
@@ -171,9 +198,10 @@ ms_status mask_scatter_rows(ms_step* step, const void* d_xm, const void* d_ycach
 ms_status cache_prefetch_layer(ms_step* step, int32_t layer, const void* h_kv, void* d_slot,
                                void* copy_stream, void* wait_event, void* signal_event);
 
-/* The whole step: gather, the n_layers blocks, final scatter, with the cache
- * read from HBM or streamed per layer from pinned host memory on copy_stream
- * two layers ahead of the compute stream (Fig. 8 middle). `w` holds n_layers
+/* The whole step: gather, the n_layers blocks (the first k of them over every
+ * token, see mask_step_set_dense_prefix), final scatter, with the cache read
+ * from HBM or streamed per layer from pinned host memory on copy_stream
+ * through the slot ring, ahead of the compute stream (Fig. 8). `w` holds n_layers
  * weight sets ([n_layers][2] when dual_stream: image, text). d_x [B][T][d]
  * holds the current hidden states (only masked rows and text rows are read);
  * d_y [B][T][d] receives the output; it may equal d_ycache. With the

@@ -17,6 +17,9 @@ hipError_t launch_compact(const uint8_t* mask, int B, int N, int n_text, int dua
                           int32_t* rows, int32_t* inv, int32_t* seg_start, int32_t* seg_req,
                           int32_t* cu_tiles, hipStream_t s);
 
+// p[0..n) = v (device bytes).
+hipError_t launch_fill_u8(void* p, uint8_t v, size_t n, hipStream_t s);
+
 // a2: xm[m] = x[rows[m]].
 hipError_t launch_gather(const void* x, const int32_t* rows, void* xm, int M, int row_bytes,
                          hipStream_t s);

@@ -54,7 +54,10 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-    size_t rows, inv, seg_start, seg_req, cu_tiles, xm, a, q, o, h, u, part_o, part_ml, gemm_part, total;
+    size_t rows, inv, seg_start, seg_req, cu_tiles;              // masked-row packing
+    size_t rows_d, inv_d, seg_start_d, seg_req_d, cu_tiles_d;    // every-token packing
+    size_t ones;                                                 // all-ones mask [B][N]
+    size_t xm, a, q, o, h, u, kv_dense, part_o, part_ml, gemm_part, total;
 };
 
 // Attention key-range split: enough workgroups to give every CU two to three,
@@ -91,7 +94,8 @@ ms_status validate_desc(const ms_model_desc* d) {
 
 Layout make_layout(const ms_model_desc& d, int32_t B) {
     Layout L{};
-    const size_t T = (size_t)d.n_text + (size_t)d.grid_h * d.grid_w;
+    const size_t N = (size_t)d.grid_h * d.grid_w;
+    const size_t T = (size_t)d.n_text + N;
     const size_t BT = (size_t)B * T;
     const size_t e = elt_bytes(d.dtype);
     const size_t dm = d.d_model, f = (size_t)d.mlp_mult * d.d_model;
@@ -102,12 +106,19 @@ Layout make_layout(const ms_model_desc& d, int32_t B) {
     L.seg_start = take((ms::kMaxSegments + 1) * 4);
     L.seg_req = take(ms::kMaxSegments * 4);
     L.cu_tiles = take((ms::kMaxSegments + 1) * 4);
+    L.rows_d = take(BT * 4);
+    L.inv_d = take(BT * 4);
+    L.seg_start_d = take((ms::kMaxSegments + 1) * 4);
+    L.seg_req_d = take(ms::kMaxSegments * 4);
+    L.cu_tiles_d = take((ms::kMaxSegments + 1) * 4);
+    L.ones = take((size_t)B * N);
     L.xm = take(BT * dm * e);
     L.a = take(BT * dm * e);
     L.q = take(BT * dm * e);
     L.o = take(BT * dm * e);
     L.h = take(BT * dm * e);
     L.u = take(BT * f * e);
+    L.kv_dense = take(BT * 2 * dm * e);
     L.part_o = take(attn_part_rows(d, B) * dm * 4);
     L.part_ml = take(attn_part_rows(d, B) * (size_t)d.n_heads * 2 * 4);
     L.gemm_part = take(ms::kGemmPartFloats * 4);
@@ -117,6 +128,14 @@ Layout make_layout(const ms_model_desc& d, int32_t B) {
 
 struct Span {
     int b, n0, n1;   // image rows [n0, n1) of request b
+};
+
+// One packed-row layout of the step: the masked rows, or every token (dense blocks).
+struct Packing {
+    int32_t *rows = nullptr, *inv = nullptr, *segs = nullptr, *segreq = nullptr, *cutiles = nullptr;
+    std::vector<int32_t> seg_start;   // host copy
+    int M = 0, nseg = 0, n_qtiles = 0, n_qtiles_fast = 0, text_rows = 0;
+    int attn_nsplit = 1, attn_tps = 1;
 };
 
 // Kernel timing: event pairs around launches of the selected classes.
@@ -157,39 +176,77 @@ class ProfScope {
 struct ms_step {
     ms_model_desc desc;
     int B = 0, T = 0, N = 0, d = 0, f = 0, hd = 0, elt = 0;
-    int M = 0, nseg = 0, n_qtiles = 0, text_rows = 0;
-    int n_qtiles_fast = 0, attn_nsplit = 1, attn_tps = 1;
     bool all_masked = false;
     char* ws = nullptr;
     Layout lay{};
-    std::vector<int32_t> seg_start;
+    Packing mp;                 // masked rows
+    Packing dp;                 // every token (dense-prefix blocks), built on first use
+    bool dense_ready = false;
+    int dense_prefix = 0;
     std::vector<Span> spans;
-    hipEvent_t ev_copied[2] = {nullptr, nullptr};
-    hipEvent_t ev_consumed[2] = {nullptr, nullptr};
+    std::vector<hipEvent_t> ev_copied, ev_consumed;
     hipEvent_t ev_start = nullptr;
 
-    int32_t* rows() const { return reinterpret_cast<int32_t*>(ws + lay.rows); }
-    int32_t* inv() const { return reinterpret_cast<int32_t*>(ws + lay.inv); }
-    int32_t* segs() const { return reinterpret_cast<int32_t*>(ws + lay.seg_start); }
-    int32_t* segreq() const { return reinterpret_cast<int32_t*>(ws + lay.seg_req); }
-    int32_t* cutiles() const { return reinterpret_cast<int32_t*>(ws + lay.cu_tiles); }
+    int M() const { return mp.M; }
     void* buf(size_t off) const { return ws + off; }
+    template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
 };
 
 namespace {
 
 void destroy_events(ms_step* s) {
-    for (int i = 0; i < 2; ++i) {
-        if (s->ev_copied[i]) (void)hipEventDestroy(s->ev_copied[i]);
-        if (s->ev_consumed[i]) (void)hipEventDestroy(s->ev_consumed[i]);
-    }
+    for (hipEvent_t e : s->ev_copied) (void)hipEventDestroy(e);
+    for (hipEvent_t e : s->ev_consumed) (void)hipEventDestroy(e);
+    s->ev_copied.clear();
+    s->ev_consumed.clear();
     if (s->ev_start) (void)hipEventDestroy(s->ev_start);
+    s->ev_start = nullptr;
+}
+
+ms_status ensure_events(ms_step* s, int n) {
+    while ((int)s->ev_copied.size() < n) {
+        hipEvent_t a = nullptr, b = nullptr;
+        hipError_t e = hipEventCreateWithFlags(&a, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&b, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            if (a) (void)hipEventDestroy(a);
+            return fail(MS_EHIP, "event creation: %s", hipGetErrorString(e));
+        }
+        s->ev_copied.push_back(a);
+        s->ev_consumed.push_back(b);
+    }
+    return MS_OK;
+}
+
+// Host-side tables of a packing from its segment starts: query tiles and the
+// attention key-range split.
+void finish_packing(Packing& p, const ms_model_desc& desc, int batch, int T, int hd) {
+    p.M = p.seg_start[p.nseg];
+    p.n_qtiles = 0;
+    p.n_qtiles_fast = 0;
+    for (int i = 0; i < p.nseg; ++i) {
+        const int len = p.seg_start[i + 1] - p.seg_start[i];
+        p.n_qtiles += (len + ms::kQTile - 1) / ms::kQTile;
+        p.n_qtiles_fast += (len + ms::kFastQTile - 1) / ms::kFastQTile;
+    }
+    const int ntiles = (T + 63) / 64;
+    const int base = std::max(1, p.n_qtiles_fast * desc.n_heads);
+    int target = kAttnTargetGroups;
+    if (const char* ev = std::getenv("MS_ATTN_SPLIT_TARGET")) target = std::max(1, std::atoi(ev));
+    int ns = std::min(ntiles, std::max(1, (target + base - 1) / base));
+    if (p.M > 0) ns = std::min(ns, std::max(1, (int)(attn_part_rows(desc, batch) / p.M)));
+    if (!ms::attention_fast_path(desc.dtype, hd)) ns = 1;
+    const int tps = (ntiles + ns - 1) / ns;
+    p.attn_tps = tps;
+    p.attn_nsplit = (ntiles + tps - 1) / tps;
 }
 
 void plan_spans(ms_step* s, const std::vector<uint8_t>& mask) {
     s->spans.clear();
     const size_t row_bytes = 2ull * s->d * s->elt;
-    const int gap_rows = (int)std::max<size_t>(1, kGapMergeBytes / row_bytes);
+    size_t gap_bytes = kGapMergeBytes;
+    if (const char* v = std::getenv("MS_COPY_GAP_BYTES")) gap_bytes = (size_t)std::atoll(v);   // tuning knob
+    const int gap_rows = (int)(gap_bytes / row_bytes);
     for (int b = 0; b < s->B; ++b) {
         const uint8_t* m = mask.data() + (size_t)b * s->N;
         int n = 0;
@@ -199,7 +256,7 @@ void plan_spans(ms_step* s, const std::vector<uint8_t>& mask) {
             if (n >= s->N) break;
             int n0 = n;
             while (n < s->N && !m[n]) ++n;
-            if (cur.n0 >= 0 && n0 - cur.n1 <= gap_rows) {
+            if (cur.n0 >= 0 && n0 - cur.n1 <= gap_rows && gap_rows > 0) {
                 cur.n1 = n;
             } else {
                 if (cur.n0 >= 0) s->spans.push_back(cur);
@@ -208,6 +265,32 @@ void plan_spans(ms_step* s, const std::vector<uint8_t>& mask) {
         }
         if (cur.n0 >= 0) s->spans.push_back(cur);
     }
+}
+
+// The every-token packing (dense-prefix blocks): compaction of an all-ones mask.
+ms_status build_dense_packing(ms_step* s, hipStream_t st) {
+    if (s->dense_ready) return MS_OK;
+    const bool split = s->desc.dual_stream && s->desc.n_text > 0;
+    Packing& p = s->dp;
+    p.rows = s->at<int32_t>(s->lay.rows_d);
+    p.inv = s->at<int32_t>(s->lay.inv_d);
+    p.segs = s->at<int32_t>(s->lay.seg_start_d);
+    p.segreq = s->at<int32_t>(s->lay.seg_req_d);
+    p.cutiles = s->at<int32_t>(s->lay.cu_tiles_d);
+    p.nseg = split ? 2 * s->B : s->B;
+    p.text_rows = split ? s->B * s->desc.n_text : 0;
+    p.seg_start.assign(p.nseg + 1, 0);
+    for (int i = 0; i < p.nseg; ++i) {
+        const int len = split ? (i < s->B ? s->desc.n_text : s->N) : s->T;
+        p.seg_start[i + 1] = p.seg_start[i] + len;
+    }
+    finish_packing(p, s->desc, s->B, s->T, s->hd);
+    MS_HIP(ms::launch_fill_u8(s->buf(s->lay.ones), 1, (size_t)s->B * s->N, st));
+    MS_HIP(ms::launch_compact(static_cast<const uint8_t*>(s->buf(s->lay.ones)), s->B, s->N,
+                              s->desc.n_text, split ? 1 : 0, p.rows, p.inv, p.segs, p.segreq,
+                              p.cutiles, st));
+    s->dense_ready = true;
+    return MS_OK;
 }
 
 ms_status check_weights(const ms_step* s, const ms_layer_weights* w) {
@@ -239,14 +322,15 @@ hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, int cls, hipStream_t st) {
     return ms::launch_gemm_reduce(s->desc.dtype, g, st);
 }
 
-ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* kv, hipStream_t st) {
-    if (s->M == 0) return MS_OK;
+ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w, void* xm, void* kv,
+                        hipStream_t st) {
+    if (pk.M == 0) return MS_OK;
     const int dt = s->desc.dtype;
     const bool dual = s->desc.dual_stream && s->desc.n_text > 0;
     const ms_layer_weights& wi = w[0];
     const ms_layer_weights& wt = dual ? w[1] : w[0];
-    const int M = s->M, d = s->d, f = s->f, e = s->elt;
-    const int msplit = s->text_rows;
+    const int M = pk.M, d = s->d, f = s->f, e = s->elt;
+    const int msplit = pk.text_rows;
     char* a = static_cast<char*>(s->buf(s->lay.a));
     char* q = static_cast<char*>(s->buf(s->lay.q));
     char* o = static_cast<char*>(s->buf(s->lay.o));
@@ -270,7 +354,7 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
         g.bias = r.w->b_qkv;
         g.C = q + (size_t)r.r0 * d * e;
         g.kv = kv;
-        g.rows = s->rows() + r.r0;
+        g.rows = pk.rows + r.r0;
         g.M = r.r1 - r.r0; g.N = 3 * d; g.K = d;
         g.lda = d; g.ldc = d; g.d = d;
         g.epilogue = ms::kEpiQKV;
@@ -278,14 +362,14 @@ ms_status block_forward(ms_step* s, const ms_layer_weights* w, void* xm, void* k
     }
     ms::AttnDesc ad{};
     ad.q = q; ad.kv = kv; ad.o = o;
-    ad.seg_start = s->segs(); ad.seg_req = s->segreq(); ad.cu_tiles = s->cutiles();
-    ad.nseg = s->nseg; ad.T = s->T; ad.d = d; ad.hd = s->hd;
-    ad.n_qtiles = s->n_qtiles; ad.n_heads = s->desc.n_heads;
+    ad.seg_start = pk.segs; ad.seg_req = pk.segreq; ad.cu_tiles = pk.cutiles;
+    ad.nseg = pk.nseg; ad.T = s->T; ad.d = d; ad.hd = s->hd;
+    ad.n_qtiles = pk.n_qtiles; ad.n_heads = s->desc.n_heads;
     ad.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)s->hd));
     ad.M = M;
-    ad.n_qtiles_fast = s->n_qtiles_fast;
-    ad.nsplit = s->attn_nsplit;
-    ad.tiles_per_split = s->attn_tps;
+    ad.n_qtiles_fast = pk.n_qtiles_fast;
+    ad.nsplit = pk.attn_nsplit;
+    ad.tiles_per_split = pk.attn_tps;
     ad.part_o = static_cast<float*>(s->buf(s->lay.part_o));
     ad.part_ml = static_cast<float*>(s->buf(s->lay.part_ml));
     {
@@ -415,52 +499,38 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
     s->ws = static_cast<char*>(d_ws);
     s->lay = lay;
     const bool split = desc->dual_stream && desc->n_text > 0;
-    s->nseg = split ? 2 * batch : batch;
-    s->text_rows = split ? batch * desc->n_text : 0;
+    Packing& p = s->mp;
+    p.rows = s->at<int32_t>(lay.rows);
+    p.inv = s->at<int32_t>(lay.inv);
+    p.segs = s->at<int32_t>(lay.seg_start);
+    p.segreq = s->at<int32_t>(lay.seg_req);
+    p.cutiles = s->at<int32_t>(lay.cu_tiles);
+    p.nseg = split ? 2 * batch : batch;
+    p.text_rows = split ? batch * desc->n_text : 0;
 
     hipStream_t hs = static_cast<hipStream_t>(stream);
     auto bail = [&](ms_status code) { destroy_events(s); delete s; return code; };
     hipError_t e;
     {
-        ProfScope p(MS_K_COMPACT, hs);
-        e = ms::launch_compact(d_mask, batch, s->N, desc->n_text, split ? 1 : 0, s->rows(), s->inv(),
-                               s->segs(), s->segreq(), s->cutiles(), hs);
+        ProfScope prof(MS_K_COMPACT, hs);
+        e = ms::launch_compact(d_mask, batch, s->N, desc->n_text, split ? 1 : 0, p.rows, p.inv,
+                               p.segs, p.segreq, p.cutiles, hs);
     }
     if (e != hipSuccess) return bail(fail(MS_EHIP, "compaction launch: %s", hipGetErrorString(e)));
-    s->seg_start.assign(s->nseg + 1, 0);
+    p.seg_start.assign(p.nseg + 1, 0);
     std::vector<uint8_t> hmask((size_t)batch * s->N);
-    e = hipMemcpyAsync(s->seg_start.data(), s->segs(), (s->nseg + 1) * sizeof(int32_t),
+    e = hipMemcpyAsync(p.seg_start.data(), p.segs, (p.nseg + 1) * sizeof(int32_t),
                        hipMemcpyDeviceToHost, hs);
     if (e == hipSuccess)
         e = hipMemcpyAsync(hmask.data(), d_mask, hmask.size(), hipMemcpyDeviceToHost, hs);
     if (e == hipSuccess) e = hipStreamSynchronize(hs);
     if (e != hipSuccess) return bail(fail(MS_EHIP, "compaction readback: %s", hipGetErrorString(e)));
-    s->M = s->seg_start[s->nseg];
-    s->n_qtiles = 0;
-    for (int i = 0; i < s->nseg; ++i)
-        s->n_qtiles += (s->seg_start[i + 1] - s->seg_start[i] + ms::kQTile - 1) / ms::kQTile;
-    s->all_masked = s->M == batch * s->T;
-    s->n_qtiles_fast = 0;
-    for (int i = 0; i < s->nseg; ++i)
-        s->n_qtiles_fast += (s->seg_start[i + 1] - s->seg_start[i] + ms::kFastQTile - 1) / ms::kFastQTile;
-    {
-        const int ntiles = (s->T + 63) / 64;
-        const int base = std::max(1, s->n_qtiles_fast * desc->n_heads);
-        int target = kAttnTargetGroups;
-        if (const char* ev = std::getenv("MS_ATTN_SPLIT_TARGET")) target = std::max(1, std::atoi(ev));
-        int ns = std::min(ntiles, std::max(1, (target + base - 1) / base));
-        if (s->M > 0) ns = std::min(ns, std::max(1, (int)(attn_part_rows(*desc, batch) / s->M)));
-        if (!ms::attention_fast_path(desc->dtype, s->hd)) ns = 1;
-        const int tps = (ntiles + ns - 1) / ns;
-        s->attn_tps = tps;
-        s->attn_nsplit = (ntiles + tps - 1) / tps;
-    }
+    finish_packing(p, *desc, batch, s->T, s->hd);
+    s->all_masked = p.M == batch * s->T;
     plan_spans(s, hmask);
-    for (int i = 0; i < 2 && e == hipSuccess; ++i) {
-        e = hipEventCreateWithFlags(&s->ev_copied[i], hipEventDisableTiming);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&s->ev_consumed[i], hipEventDisableTiming);
-    }
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&s->ev_start, hipEventDisableTiming);
+    st = ensure_events(s, 2);
+    if (st != MS_OK) return bail(st);
+    e = hipEventCreateWithFlags(&s->ev_start, hipEventDisableTiming);
     if (e != hipSuccess) return bail(fail(MS_EHIP, "event creation: %s", hipGetErrorString(e)));
     *out = s;
     return ok();
@@ -469,19 +539,60 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
 ms_status mask_step_get_info(const ms_step* s, ms_step_info* info) {
     if (!s || !info) return fail(MS_EINVAL, "NULL argument");
     info->batch = s->B;
-    info->rows = s->M;
-    info->n_segments = s->nseg;
-    info->n_qtiles = s->n_qtiles;
-    info->text_rows = s->text_rows;
+    info->rows = s->mp.M;
+    info->n_segments = s->mp.nseg;
+    info->n_qtiles = s->mp.n_qtiles;
+    info->text_rows = s->mp.text_rows;
+    info->dense_prefix = s->dense_prefix;
     return ok();
 }
 
 ms_status mask_step_index(const ms_step* s, const int32_t** d_rows, const int32_t** d_inv,
                           const int32_t** d_seg_start) {
     if (!s) return fail(MS_ESTATE, "no step context");
-    if (d_rows) *d_rows = s->rows();
-    if (d_inv) *d_inv = s->inv();
-    if (d_seg_start) *d_seg_start = s->segs();
+    if (d_rows) *d_rows = s->mp.rows;
+    if (d_inv) *d_inv = s->mp.inv;
+    if (d_seg_start) *d_seg_start = s->mp.segs;
+    return ok();
+}
+
+ms_status mask_step_set_dense_prefix(ms_step* s, int32_t k, void* stream) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (k < 0 || k > s->desc.n_layers) return fail(MS_EINVAL, "dense prefix %d outside 0..n_layers", k);
+    if (k > 0) {
+        ms_status st = build_dense_packing(s, static_cast<hipStream_t>(stream));
+        if (st != MS_OK) return st;
+    }
+    s->dense_prefix = k;
+    return ok();
+}
+
+ms_status mask_plan_dense_prefix(int32_t n_layers, double load_ms, double cached_ms, double full_ms,
+                                 int32_t* k_out, double* latency_ms_out) {
+    if (n_layers < 1 || !k_out) return fail(MS_EINVAL, "need n_layers >= 1 and k_out");
+    if (!(load_ms >= 0) || !(cached_ms >= 0) || !(full_ms >= 0)) return fail(MS_EINVAL, "negative or NaN cost");
+    // Alg. 1's clocks for the choice "first k blocks over every token, the rest with the cache":
+    // a full block needs no load (comp += full); a cached block's load follows the previous load
+    // and its compute waits for it (comp = max(load, comp) + cached).
+    int best_k = 0;
+    double best = 0.0;
+    for (int k = 0; k <= n_layers; ++k) {
+        double comp = 0.0, load = 0.0;
+        for (int i = 0; i < n_layers; ++i) {
+            if (i < k) {
+                comp += full_ms;
+            } else {
+                load += load_ms;
+                comp = std::max(load, comp) + cached_ms;
+            }
+        }
+        if (k == 0 || comp < best - 1e-12) {
+            best = comp;
+            best_k = k;
+        }
+    }
+    *k_out = best_k;
+    if (latency_ms_out) *latency_ms_out = best;
     return ok();
 }
 
@@ -491,7 +602,7 @@ ms_status mask_gather_rows(ms_step* s, const void* d_x, void* d_xm, void* stream
     void* xm = d_xm ? d_xm : s->buf(s->lay.xm);
     if (!aligned16(d_x) || !aligned16(xm)) return fail(MS_EALIGN, "x / xm not 16-byte aligned");
     ProfScope p(MS_K_GATHER, static_cast<hipStream_t>(stream));
-    MS_HIP(ms::launch_gather(d_x, s->rows(), xm, s->M, s->d * s->elt, static_cast<hipStream_t>(stream)));
+    MS_HIP(ms::launch_gather(d_x, s->mp.rows, xm, s->mp.M, s->d * s->elt, static_cast<hipStream_t>(stream)));
     return ok();
 }
 
@@ -504,7 +615,7 @@ ms_status mask_block_forward(ms_step* s, int32_t layer, const ms_layer_weights* 
     if (!aligned16(xm) || !aligned16(d_kv)) return fail(MS_EALIGN, "xm / kv not 16-byte aligned");
     ms_status st = check_weights(s, w);
     if (st != MS_OK) return st;
-    st = block_forward(s, w, xm, d_kv, static_cast<hipStream_t>(stream));
+    st = block_forward(s, s->mp, w, xm, d_kv, static_cast<hipStream_t>(stream));
     return st == MS_OK ? ok() : st;
 }
 
@@ -516,7 +627,7 @@ ms_status mask_scatter_rows(ms_step* s, const void* d_xm, const void* d_ycache, 
     const void* xm = d_xm ? d_xm : s->buf(s->lay.xm);
     if (!aligned16(d_y) || !aligned16(xm) || !aligned16(d_ycache)) return fail(MS_EALIGN, "pointer not 16-byte aligned");
     ProfScope p(MS_K_SCATTER, static_cast<hipStream_t>(stream));
-    MS_HIP(ms::launch_scatter(xm, s->rows(), s->inv(), d_ycache, d_y, s->M, s->B * s->T,
+    MS_HIP(ms::launch_scatter(xm, s->mp.rows, s->mp.inv, d_ycache, d_y, s->mp.M, s->B * s->T,
                               s->d * s->elt, static_cast<hipStream_t>(stream)));
     return ok();
 }
@@ -543,7 +654,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
     if (kv->kind != MS_KV_DEVICE && kv->kind != MS_KV_HOST_PINNED) return fail(MS_EINVAL, "unknown kv kind %d", kv->kind);
     if (!kv->layer) return fail(MS_EINVAL, "kv->layer is NULL");
     const int L = s->desc.n_layers;
-    const int nsets = (s->desc.dual_stream && s->desc.n_text > 0) ? 2 : 1;
+    const int k = s->dense_prefix;
     const int wstride = s->desc.dual_stream ? 2 : 1;
     for (int l = 0; l < L; ++l) {
         if (!kv->layer[l]) return fail(MS_EINVAL, "kv->layer[%d] is NULL", l);
@@ -551,63 +662,92 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         ms_status st = check_weights(s, w + (size_t)l * wstride);
         if (st != MS_OK) return st;
     }
-    (void)nsets;
     const bool pinned = kv->kind == MS_KV_HOST_PINNED;
+    const int n_slots = pinned ? kv->n_slots : 0;
     if (pinned) {
-        for (int i = 0; i < 2; ++i) {
-            if (!kv->slot[i] && (i == 0 || L > 1)) return fail(MS_EINVAL, "kv->slot[%d] is NULL", i);
-            if (kv->slot[i] && !aligned16(kv->slot[i])) return fail(MS_EALIGN, "kv->slot[%d] not aligned", i);
+        if (n_slots < 1 || !kv->slots) return fail(MS_EINVAL, "pinned K/V needs n_slots >= 1 device slots");
+        for (int i = 0; i < n_slots; ++i) {
+            if (!kv->slots[i]) return fail(MS_EINVAL, "kv->slots[%d] is NULL", i);
+            if (!aligned16(kv->slots[i])) return fail(MS_EALIGN, "kv->slots[%d] not 16-byte aligned", i);
         }
-        if (!s->all_masked && s->M > 0) {
-            ms_status st = check_pinned(kv->layer[0]);
+        if (!s->all_masked && s->mp.M > 0 && k < L) {
+            ms_status st = check_pinned(kv->layer[k]);
             if (st != MS_OK) return st;
         }
+        ms_status st = ensure_events(s, n_slots);
+        if (st != MS_OK) return st;
     }
     if (!aligned16(d_x) || !aligned16(d_y) || !aligned16(d_ycache)) return fail(MS_EALIGN, "pointer not 16-byte aligned");
 
     hipStream_t cs = static_cast<hipStream_t>(compute_stream);
     hipStream_t ps = static_cast<hipStream_t>(copy_stream);
     void* xm = s->buf(s->lay.xm);
-    if (s->M > 0) {
-        {
-            ProfScope p(MS_K_GATHER, cs);
-            MS_HIP(ms::launch_gather(d_x, s->rows(), xm, s->M, s->d * s->elt, cs));
-        }
-        const bool stream_cache = pinned && !s->all_masked;
+    const Packing& mp = s->mp;
+    if (mp.M > 0) {
+        const int n_cached = L - k;
+        const bool stream_cache = pinned && !s->all_masked && n_cached > 0;
         const bool serialize = stream_cache && (env_flag("MS_SERIALIZE") || ps == cs);
         if (stream_cache && !serialize) {
-            // the copy stream must not overwrite a slot an earlier call still reads
+            // the copy stream must not overwrite a slot an earlier call still reads; the first
+            // n_slots cached layers then load from the start, under the dense prefix if any
             MS_HIP(hipEventRecord(s->ev_start, cs));
             MS_HIP(hipStreamWaitEvent(ps, s->ev_start, 0));
-            for (int l = 0; l < std::min(L, 2); ++l) {
-                ms_status st = prefetch_signal(s, kv->layer[l], kv->slot[l], ps, nullptr, s->ev_copied[l]);
+            for (int j = 0; j < std::min(n_slots, n_cached); ++j) {
+                ms_status st = prefetch_signal(s, kv->layer[k + j], kv->slots[j], ps, nullptr, s->ev_copied[j]);
                 if (st != MS_OK) return st;
             }
         }
-        for (int l = 0; l < L; ++l) {
+        if (k > 0) {
+            // dense prefix: every token, fresh K/V into the workspace buffer, no cache read
+            const Packing& dp = s->dp;
+            void* kvd = s->buf(s->lay.kv_dense);
+            {
+                ProfScope p(MS_K_GATHER, cs);
+                MS_HIP(ms::launch_gather(d_x, dp.rows, xm, dp.M, s->d * s->elt, cs));
+            }
+            for (int l = 0; l < k; ++l) {
+                ms_status st = block_forward(s, dp, w + (size_t)l * wstride, xm, kvd, cs);
+                if (st != MS_OK) return st;
+            }
+            // hidden states of every token back in token order, then the masked rows
+            void* flat = s->buf(s->lay.o);
+            {
+                ProfScope p(MS_K_SCATTER, cs);
+                MS_HIP(ms::launch_scatter(xm, dp.rows, dp.inv, flat, flat, dp.M, s->B * s->T,
+                                          s->d * s->elt, cs));
+            }
+            ProfScope p(MS_K_GATHER, cs);
+            MS_HIP(ms::launch_gather(flat, mp.rows, xm, mp.M, s->d * s->elt, cs));
+        } else {
+            ProfScope p(MS_K_GATHER, cs);
+            MS_HIP(ms::launch_gather(d_x, mp.rows, xm, mp.M, s->d * s->elt, cs));
+        }
+        for (int l = k; l < L; ++l) {
+            const int j = l - k;
             void* kvbuf = const_cast<void*>(kv->layer[l]);
             if (pinned) {
-                kvbuf = kv->slot[l % 2];
+                kvbuf = kv->slots[j % n_slots];
                 if (serialize) {
                     ms_status st = prefetch(s, kv->layer[l], kvbuf, cs, nullptr);
                     if (st != MS_OK) return st;
                 } else if (stream_cache) {
-                    MS_HIP(hipStreamWaitEvent(cs, s->ev_copied[l % 2], 0));
+                    MS_HIP(hipStreamWaitEvent(cs, s->ev_copied[j % n_slots], 0));
                 }
             }
-            ms_status st = block_forward(s, w + (size_t)l * wstride, xm, kvbuf, cs);
+            ms_status st = block_forward(s, mp, w + (size_t)l * wstride, xm, kvbuf, cs);
             if (st != MS_OK) return st;
-            if (stream_cache && !serialize && l + 2 < L) {
-                MS_HIP(hipEventRecord(s->ev_consumed[l % 2], cs));
-                st = prefetch_signal(s, kv->layer[l + 2], kv->slot[l % 2], ps, s->ev_consumed[l % 2],
-                                     s->ev_copied[l % 2]);
+            if (stream_cache && !serialize && j + n_slots < n_cached) {
+                const int sl = j % n_slots;
+                MS_HIP(hipEventRecord(s->ev_consumed[sl], cs));
+                st = prefetch_signal(s, kv->layer[l + n_slots], kv->slots[sl], ps, s->ev_consumed[sl],
+                                     s->ev_copied[sl]);
                 if (st != MS_OK) return st;
             }
         }
     }
     {
         ProfScope p(MS_K_SCATTER, cs);
-        MS_HIP(ms::launch_scatter(xm, s->rows(), s->inv(), d_ycache, d_y, s->M, s->B * s->T,
+        MS_HIP(ms::launch_scatter(xm, mp.rows, mp.inv, d_ycache, d_y, mp.M, s->B * s->T,
                                   s->d * s->elt, cs));
     }
     return ok();

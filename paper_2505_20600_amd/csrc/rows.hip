@@ -51,6 +51,11 @@ __global__ __launch_bounds__(kCopyThreads) void merge_kernel(
     }
 }
 
+__global__ __launch_bounds__(kCopyThreads) void fill_kernel(uint8_t* __restrict__ p, uint8_t v, long n) {
+    const long stride = (long)gridDim.x * blockDim.x;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
 int copy_grid(long total) {
     long blocks = (total + kCopyThreads - 1) / kCopyThreads;
     if (blocks > 256 * 16) blocks = 256 * 16;
@@ -120,6 +125,13 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
 }
 
 }  // namespace
+
+hipError_t launch_fill_u8(void* p, uint8_t v, size_t n, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_kernel, dim3(copy_grid((long)n)), dim3(kCopyThreads), 0, s,
+                       static_cast<uint8_t*>(p), v, (long)n);
+    return hipGetLastError();
+}
 
 hipError_t launch_gather(const void* x, const int32_t* rows, void* xm, int M, int row_bytes,
                          hipStream_t s) {

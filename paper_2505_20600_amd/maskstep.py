@@ -39,12 +39,13 @@ class LayerWeights(C.Structure):
 
 
 class KVSource(C.Structure):
-    _fields_ = [("kind", C.c_int32), ("layer", C.POINTER(C.c_void_p)), ("slot", C.c_void_p * 2)]
+    _fields_ = [("kind", C.c_int32), ("layer", C.POINTER(C.c_void_p)), ("n_slots", C.c_int32),
+                ("slots", C.POINTER(C.c_void_p))]
 
 
 class StepInfo(C.Structure):
     _fields_ = [("batch", C.c_int32), ("rows", C.c_int32), ("n_segments", C.c_int32),
-                ("n_qtiles", C.c_int32), ("text_rows", C.c_int32)]
+                ("n_qtiles", C.c_int32), ("text_rows", C.c_int32), ("dense_prefix", C.c_int32)]
 
 
 class MaskStepError(RuntimeError):
@@ -77,6 +78,9 @@ def load() -> C.CDLL:
             "mask_stack_forward": (i32, [vp, C.POINTER(LayerWeights), vp, vp, C.POINTER(KVSource),
                                          vp, vp, vp]),
             "mask_step_destroy": (None, [vp]),
+            "mask_step_set_dense_prefix": (i32, [vp, i32, vp]),
+            "mask_plan_dense_prefix": (i32, [i32, C.c_double, C.c_double, C.c_double, C.POINTER(i32),
+                                             C.POINTER(C.c_double)]),
             "mask_profiler_start": (i32, [C.c_uint32, i32]),
             "ms_linear": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, sz, vp]),
             "mask_profiler_stop": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
@@ -92,6 +96,7 @@ def load() -> C.CDLL:
 EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask_step_init",
             "mask_step_get_info", "mask_step_index", "mask_gather_rows", "mask_block_forward",
             "mask_scatter_rows", "cache_prefetch_layer", "mask_stack_forward", "mask_step_destroy",
+            "mask_step_set_dense_prefix", "mask_plan_dense_prefix",
             "mask_profiler_start", "mask_profiler_stop", "ms_linear")
 
 MS_EPI_BIAS, MS_EPI_BIAS_RESID, MS_EPI_BIAS_GELU = 0, 1, 2
@@ -149,6 +154,14 @@ def _stream(s) -> int | None:
     if isinstance(s, int):
         return s
     return s.cuda_stream
+
+
+def mask_plan_dense_prefix(n_layers: int, load_ms: float, cached_ms: float, full_ms: float):
+    """(k, modelled latency) of the best dense prefix under Alg. 1's latency model."""
+    k = C.c_int32()
+    lat = C.c_double()
+    _check(load().mask_plan_dense_prefix(n_layers, load_ms, cached_ms, full_ms, C.byref(k), C.byref(lat)))
+    return k.value, lat.value
 
 
 def model_desc(shape, max_batch: int | None = None) -> ModelDesc:
@@ -249,13 +262,18 @@ class MaskStep:
         _check(self._lib.cache_prefetch_layer(self.handle, layer, _ptr(h_kv), _ptr(d_slot),
                                               _stream(copy_stream), ev(wait_event), ev(signal_event)))
 
-    def stack_forward(self, weights_c, x, ycache, kv_layers, y, *, pinned: bool = False, slots=(None, None),
+    def set_dense_prefix(self, k: int, stream=None):
+        _check(self._lib.mask_step_set_dense_prefix(self.handle, k, _stream(stream)))
+
+    def stack_forward(self, weights_c, x, ycache, kv_layers, y, *, pinned: bool = False, slots=(),
                       stream=None, copy_stream=None):
-        """``weights_c`` from weights_array(); ``kv_layers``: [L] tensors (device or pinned host)."""
+        """``weights_c`` from weights_array(); ``kv_layers``: [L] tensors (device or pinned host);
+        ``slots``: device [B][T][2][d] buffers the pinned layers stream through."""
         L = len(kv_layers)
         ptrs = (C.c_void_p * L)(*[_ptr(t) for t in kv_layers])
+        sl = (C.c_void_p * max(1, len(slots)))(*[_ptr(t) for t in slots])
         src = KVSource(MS_KV_HOST_PINNED if pinned else MS_KV_DEVICE, C.cast(ptrs, C.POINTER(C.c_void_p)),
-                       (C.c_void_p * 2)(_ptr(slots[0]), _ptr(slots[1])))
+                       len(slots) if pinned else 0, C.cast(sl, C.POINTER(C.c_void_p)))
         cs = _stream(stream)
         ps = _stream(copy_stream) if copy_stream is not None else cs
         _check(self._lib.mask_stack_forward(self.handle, weights_c, _ptr(x), _ptr(ycache), C.byref(src),

@@ -81,7 +81,7 @@ def new_step(shape, mask_np, stream=None):
 
 
 def run_stack(shape, mask, x, kv_cache, y_cache, weights, *, pinned=False, serialize=False,
-              aliased=False, poison_cache=False):
+              aliased=False, poison_cache=False, n_slots=2, dense_prefix=0):
     """One step through mask_stack_forward; returns (y, working kv per layer or None, step)."""
     dw = dev_weights(weights, shape)
     wc = MS.weights_array(dw)
@@ -97,14 +97,16 @@ def run_stack(shape, mask, x, kv_cache, y_cache, weights, *, pinned=False, seria
             t.copy_(torch.as_tensor(np.ascontiguousarray(img, np.float32)).to(tdtype(shape)))
             host.append(t)
         slots = [torch.full((shape.batch, shape.n_tokens, 2, shape.d_model), float("nan"),
-                            dtype=tdtype(shape), device=DEV) for _ in range(2)]
+                            dtype=tdtype(shape), device=DEV) for _ in range(n_slots)]
         kv_layers = host
     else:
         kv_layers = [to_dev(kv_cache[l], shape) for l in range(L)]
         if poison_cache:
             for t in kv_layers:
                 t.fill_(float("nan"))
-        slots = (None, None)
+        slots = ()
+    if dense_prefix:
+        step.set_dense_prefix(dense_prefix)
     y = d_yc if aliased else torch.empty((shape.batch, shape.n_tokens, shape.d_model),
                                          dtype=tdtype(shape), device=DEV)
     cs = torch.cuda.current_stream()

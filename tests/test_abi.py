@@ -105,6 +105,25 @@ def test_calls_without_a_step_context_fail_cleanly():
     lib.mask_step_destroy(None)  # no-op
 
 
+def test_planner_matches_the_oracle_planner():
+    """mask_plan_dense_prefix (host-only) against Alg. 1's recurrences evaluated in the oracle."""
+    import numpy as np
+    import oracle
+    g = np.random.default_rng(5)
+    for _ in range(300):
+        n = int(g.integers(1, 30))
+        L, cw = float(g.uniform(0.05, 5)), float(g.uniform(0.01, 2))
+        cwo = cw + float(g.uniform(0, 6))
+        k, lat = MS.mask_plan_dense_prefix(n, L, cw, cwo)
+        k_ref, lat_ref = oracle.best_dense_prefix(n, L, cw, cwo)
+        assert k == k_ref
+        assert abs(lat - lat_ref) <= 1e-9 * max(1.0, lat_ref)
+    with pytest.raises(MS.MaskStepError):
+        MS.mask_plan_dense_prefix(0, 1.0, 1.0, 1.0)
+    with pytest.raises(MS.MaskStepError):
+        MS.mask_plan_dense_prefix(4, -1.0, 1.0, 1.0)
+
+
 def test_error_message_is_per_call():
     lib = MS.load()
     assert lib.mask_workspace_bytes(C.byref(_desc(d_model=100)), 1) == 0

@@ -266,7 +266,7 @@ def test_streamed_repeated_steps_are_identical():
         t.copy_(torch.as_tensor(np.ascontiguousarray(kv[l], np.float32)).to(torch.bfloat16))
         host.append(t)
     slots = [torch.empty((shape.batch, shape.n_tokens, 2, shape.d_model), dtype=torch.bfloat16,
-                         device=G.DEV) for _ in range(2)]
+                         device=G.DEV) for _ in range(3)]
     d_x, d_yc = G.to_dev(xt, shape), G.to_dev(yc, shape)
     copy = torch.cuda.Stream()
     outs = []
@@ -322,3 +322,46 @@ def test_attention_split_and_unsplit_match_oracle(hd_shape, monkeypatch):
         G.assert_close(y, y_ref, "bf16", f"{shape.name} split target {target}")
         outs.append(y)
     G.assert_close(outs[1], outs[0], "bf16", "split vs unsplit")
+
+
+# ------------------------------------------------------------------ dense prefix (bubble-free pipeline)
+
+PREFIX_SHAPE = W.ModelShape("prefix", 4, 256, 2, 4, 16, 16, dtype="bf16", batch=2)
+PREFIX_DUAL = W.ModelShape("prefix_dual", 3, 256, 2, 4, 8, 16, n_text=16, dual_stream=True, dtype="bf16",
+                           batch=2)
+
+
+@pytest.mark.parametrize("shape", [PREFIX_SHAPE, PREFIX_DUAL], ids=lambda s: s.name)
+def test_dense_prefix_matches_oracle_and_streaming_is_exact(shape):
+    """Blocks [0, k) over every token, the rest cached: resident, streamed through 1, 2 or
+    n_layers slots, pipelined or serialized — identical bits, and the oracle within tolerance."""
+    ws, xt, kv, yc = _inputs(shape, 70, std=0.03)
+    mask = np.stack([W.ellipse_mask(shape.grid_h, shape.grid_w, r, W.rng(7, 3, b)) for b, r in
+                     enumerate((0.3, 0.12))])
+    x = W.edited_hidden(shape, 70, xt, mask)
+    for k in (1, 2, shape.n_layers):
+        y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, dense_prefix=k)
+        y_res, _, step = G.run_stack(shape, mask, x, kv, yc, ws, dense_prefix=k)
+        assert step.info().dense_prefix == k
+        G.assert_close(y_res, y_ref, "bf16", f"{shape.name} dense prefix {k}")
+        for n_slots in (1, 2, shape.n_layers):
+            y_pipe, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, n_slots=n_slots, dense_prefix=k)
+            np.testing.assert_array_equal(y_pipe, y_res, err_msg=f"k={k} slots={n_slots}")
+        y_ser, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, serialize=True, dense_prefix=k)
+        np.testing.assert_array_equal(y_ser, y_res)
+    # the prefix reads no cache of its blocks: poisoning them changes nothing
+    poisoned = kv.copy()
+    poisoned[:2] = np.nan
+    y_a, _, _ = G.run_stack(shape, mask, x, poisoned, yc, ws, dense_prefix=2)
+    y_b, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, dense_prefix=2)
+    np.testing.assert_array_equal(y_a, y_b)
+
+
+def test_dense_prefix_own_cache_reproduces_dense():
+    shape = PREFIX_SHAPE.replace(batch=1)
+    ws = W.stack_weights(shape, 71, random_ln=True, std=0.03)
+    xt = W.template_hidden(shape, 71)
+    y_dense, kv_dense = oracle.dense_stack(xt, ws, shape)
+    mask = np.stack([W.ellipse_mask(16, 16, 0.25, W.rng(7, 3, 9))])
+    y, _, _ = G.run_stack(shape, mask, xt, kv_dense, y_dense, ws, pinned=True, n_slots=4, dense_prefix=2)
+    G.assert_close(y, y_dense, "bf16", "own cache with a dense prefix")
