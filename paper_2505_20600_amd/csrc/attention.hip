@@ -226,10 +226,16 @@ struct FastCfg {
     static constexpr int NK32 = HD / 32;                  // 32-deep QK^T steps
     static constexpr bool K16 = (HD % 32) != 0;           // one extra 16-deep step
     static constexpr int HDQ = NK32 * 32 + (K16 ? 16 : 0);
-    static constexpr int NHS = (HD + 15) / 16;            // 16-row subtiles of O^T
+    // O^T rows: head_dim rows, then rows of ones in V^T whose O^T rows
+    // accumulate the softmax denominator (sum of the bf16 probabilities) on
+    // the matrix cores. head_dim 72 uses its zero-padding rows 72..79 for it;
+    // 64 and 128 get one extra 16-row subtile.
+    static constexpr bool SUM_IN_PAD = (HD % 16) != 0;
+    static constexpr int NHS = (HD + 15) / 16 + (SUM_IN_PAD ? 0 : 1);
     static constexpr int HDV = NHS * 16;
+    static constexpr int SUMROW = SUM_IN_PAD ? HD : NHS * 16 - 16;  // first ones row
     static constexpr int KL = HDQ + 8;                    // K row stride in LDS (elements)
-    static constexpr int VL = kKeyTile + 4;               // V^T row stride in LDS (elements)
+    static constexpr int VL = kKeyTile + 8;               // V^T row stride in LDS (elements)
     static constexpr int CH = HD / 8;                     // 16-byte chunks per key row
     static constexpr int KITEMS = kKeyTile * CH;          // K: key x chunk
     static constexpr int VITEMS = (kKeyTile / 2) * CH;    // V: key pair x chunk
@@ -249,8 +255,9 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x4_t a, bf16x4_t b, f32x4_t c) {
 template <int HD>
 __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a) {
     using C = FastCfg<HD>;
-    __shared__ __attribute__((aligned(16))) bf16_t sK[kKeyTile * C::KL];
-    __shared__ __attribute__((aligned(16))) bf16_t sVt[C::HDV * C::VL];
+    // two K / V^T tile buffers: the next tile is stored while the current one is read
+    __shared__ __attribute__((aligned(16))) bf16_t sK[2][kKeyTile * C::KL];
+    __shared__ __attribute__((aligned(16))) bf16_t sVt[2][C::HDV * C::VL];
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
@@ -282,11 +289,15 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
     const int kt1 = min(ntiles_all, kt0 + a.tiles_per_split);
 
     if constexpr (C::HDQ > HD) {
-        for (int i = tid; i < kKeyTile * (C::HDQ - HD); i += kThreads)
-            sK[(i / (C::HDQ - HD)) * C::KL + HD + i % (C::HDQ - HD)] = 0;
+        for (int i = tid; i < 2 * kKeyTile * (C::HDQ - HD); i += kThreads) {
+            const int b = i / (kKeyTile * (C::HDQ - HD)), j = i % (kKeyTile * (C::HDQ - HD));
+            sK[b][(j / (C::HDQ - HD)) * C::KL + HD + j % (C::HDQ - HD)] = 0;
+        }
     }
-    if constexpr (C::HDV > HD) {
-        for (int i = tid; i < (C::HDV - HD) * C::VL; i += kThreads) sVt[HD * C::VL + i] = 0;
+    // V^T rows past head_dim: ones from SUMROW on, zeros before (never written by tiles)
+    for (int i = tid; i < 2 * (C::HDV - HD) * C::VL; i += kThreads) {
+        const int b = i / ((C::HDV - HD) * C::VL), j = i % ((C::HDV - HD) * C::VL);
+        sVt[b][HD * C::VL + j] = (HD + j / C::VL >= C::SUMROW) ? bf16_t(0x3f80) : bf16_t(0);
     }
 
     // Q^T fragments (B operand): query column l16 of block qb, head_dim slots by lane group
@@ -317,7 +328,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
     for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int h = 0; h < C::NHS; ++h) oacc[qb][h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    float m_run[2] = {-INFINITY, -INFINITY};
     const float cs = a.scale_log2;
 
     // Every thread stages both K and V items of the next tile into its own
@@ -363,13 +374,16 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
                     pv[j][e] = ld16(base + offv[j][e] - (keyv[j] + e - min(keyv[j] + e, last)) * 2 * d);
         }
     };
-    auto sstore = [&]() {
+    // V^T rows r hold keys as 32 key pairs; pair p of row r sits at pair slot
+    // p ^ (8 * ((r >> 4) & 3)): 4-key groups stay contiguous for the 8-byte
+    // reads, and the pair-packed stores of one wave cover all 64 banks.
+    auto sstore = [&](int buf) {
 #pragma unroll
         for (int j = 0; j < C::KPT; ++j) {
             const int item = tid + j * kThreads;
             if (C::KITEMS % kThreads == 0 || item < C::KITEMS) {
                 const int key = item / C::CH, c = item % C::CH;
-                st16(&sK[key * C::KL + c * 8], pk[j]);
+                st16(&sK[buf][key * C::KL + c * 8], pk[j]);
             }
         }
 #pragma unroll
@@ -380,16 +394,18 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
                 // V^T[c*8 + e][2kp .. 2kp+1] = (V[2kp][c*8+e], V[2kp+1][c*8+e])
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
+                    const int r = c * 8 + e;
                     const uint32_t w = __builtin_amdgcn_perm(pv[j][1].w[e >> 1], pv[j][0].w[e >> 1],
                                                              (e & 1) ? 0x07060302u : 0x05040100u);
-                    *reinterpret_cast<uint32_t*>(&sVt[(c * 8 + e) * C::VL + 2 * kp]) = w;
+                    const int slot = kp ^ (8 * ((r >> 4) & 3));
+                    *reinterpret_cast<uint32_t*>(&sVt[buf][r * C::VL + 2 * slot]) = w;
                 }
             }
         }
     };
 
     // One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
-    auto compute = [&](int k0, bool tail) {
+    auto compute = [&](int buf, int k0, bool tail) {
         f32x4_t sacc[2][4];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
@@ -397,7 +413,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
             for (int ks = 0; ks < 4; ++ks) sacc[qb][ks] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-            const bf16_t* kr = &sK[(ks * 16 + l16) * C::KL];
+            const bf16_t* kr = &sK[buf][(ks * 16 + l16) * C::KL];
 #pragma unroll
             for (int kc = 0; kc < C::NK32; ++kc) {
                 const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(kr + kc * 32 + grp * 8);
@@ -430,22 +446,15 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
             // rescale the accumulators only when some query's running max grew
             if (__any(m_new > m_run[qb])) {
                 const float corr = fast_exp2((m_run[qb] - m_new) * cs);
-                l_run[qb] *= corr;
 #pragma unroll
                 for (int h = 0; h < C::NHS; ++h) oacc[qb][h] *= corr;
                 m_run[qb] = m_new;
             }
             const float mc = m_run[qb] * cs;
-            float psum = 0.f;
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float p = fast_exp2(fmaf(sacc[qb][ks][r], cs, -mc));
-                    sacc[qb][ks][r] = p;
-                    psum += p;
-                }
-            l_run[qb] += psum;
+                for (int r = 0; r < 4; ++r) sacc[qb][ks][r] = fast_exp2(fmaf(sacc[qb][ks][r], cs, -mc));
         }
         // O^T += V^T P^T; K-slots 0..3 = keys 32c + 4*grp + r, slots 4..7 = keys 32c + 16 + 4*grp + r
 #pragma unroll
@@ -462,9 +471,10 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
             }
 #pragma unroll
             for (int h = 0; h < C::NHS; ++h) {
-                const bf16_t* vr = &sVt[(h * 16 + l16) * C::VL + 32 * c + 4 * grp];
-                const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
-                const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 16);
+                const int x = 8 * (h & 3);   // pair-slot swizzle of rows h*16 .. h*16+15
+                const bf16_t* vrow = &sVt[buf][(h * 16 + l16) * C::VL];
+                const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + 2 * ((16 * c + 2 * grp) ^ x));
+                const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + 2 * ((16 * c + 8 + 2 * grp) ^ x));
                 const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb) oacc[qb][h] = mfma32(vf, pf[qb], oacc[qb][h]);
@@ -472,27 +482,37 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
         }
     };
 
-    // full 64-key tiles first (no masking), then the partial last tile if any
+    // One barrier per tile: tile kt is read from buffer kt & 1 while tile kt+1
+    // is stored into the other buffer (last read during tile kt-1, which every
+    // wave finished before the previous barrier); full 64-key tiles need no
+    // key masking, only a partial last tile does.
     const int kfull = min(kt1, max(kt0, T_ / kKeyTile));
-    if (kt0 < kt1) gload(kt0);
-    for (int kt = kt0; kt < kfull; ++kt) {
-        __syncthreads();
-        sstore();
-        __syncthreads();
-        if (kt + 1 < kt1) gload(kt + 1);
-        compute(kt * kKeyTile, false);
+    if (kt0 < kt1) {
+        gload(kt0);
+        sstore(kt0 & 1);
+        if (kt0 + 1 < kt1) gload(kt0 + 1);
     }
-    for (int kt = kfull; kt < kt1; ++kt) {
+    __syncthreads();
+    for (int kt = kt0; kt < kt1; ++kt) {
+        compute(kt & 1, kt * kKeyTile, kt >= kfull);
+        if (kt + 1 < kt1) {
+            sstore((kt + 1) & 1);
+            if (kt + 2 < kt1) gload(kt + 2);
+        }
         __syncthreads();
-        sstore();
-        __syncthreads();
-        if (kt + 1 < kt1) gload(kt + 1);
-        compute(kt * kKeyTile, true);
     }
 
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        const float l = rows_sum(l_run[qb]);
+        // denominator from the ones rows: subtile SUMROW/16, row SUMROW % 16 + 4*grp + r;
+        // with the ones in the padding rows only lane groups 2-3 hold it (rows 72..79)
+        float l = oacc[qb][C::SUMROW / 16][0];
+        if constexpr (C::SUM_IN_PAD) {
+            // lane groups 0-1 hold V rows there: zero them and add the swapped halves
+            const float t = grp >= 2 ? l : 0.f;
+            auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+            l = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+        }
         const int qrow = row0 + wave * 32 + qb * 16 + l16;
         if (qrow >= row_end) continue;
         if (a.nsplit == 1) {
