@@ -106,6 +106,19 @@ __device__ __forceinline__ void load_lds16(const void* g, void* lds) {
     __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds), 16, 0, 0);
 }
 
+// The same copy issued as an opaque instruction: the compiler does not see the
+// LDS write, so it adds no wait of its own before later LDS reads (of other
+// stages); the caller orders them with wait_vmcnt + barrier_only. `lds` is a
+// wave-uniform LDS byte address. The loads complete in issue order with every
+// other vector-memory load, so the compiler's own vmcnt waits stay correct.
+__device__ __forceinline__ void dma_lds16(const void* g, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(g) : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)(p)));
+}
+
 // s_waitcnt with only the vector-memory counter constrained (<= n, n < 64).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -115,7 +128,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // Workgroup barrier without the memory fence of __syncthreads (callers order
 // their own memory operations with explicit waits).
-__device__ __forceinline__ void barrier_only() { __builtin_amdgcn_s_barrier(); }
+// The empty asm statements keep the compiler from moving memory accesses
+// across the barrier.
+__device__ __forceinline__ void barrier_only() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
 // 2^x with the hardware v_exp_f32 (no denormal-result fix-up: softmax
 // weights below 2^-126 of the running maximum are irrelevant).

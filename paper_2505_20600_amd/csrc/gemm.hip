@@ -176,24 +176,36 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
 // LDS rows are 128 bytes (one K step of 64 bf16) with their eight 16-byte
 // chunks XOR-swizzled by (row >> 1) & 7: each load instruction fills 1 KB
 // (8 rows) contiguously, and the 16-row MFMA fragment reads of one K chunk
-// still touch 16 distinct bank groups.
+// still touch 16 distinct bank groups. The copies are issued as opaque
+// instructions (dma_lds16) and ordered by explicit counter waits: a compiler
+// that sees them must assume each may write the stage being read and drains
+// every load in flight before the first fragment read of each step.
+
+// Waves per workgroup of the direct-to-LDS kernel: 256x256 tiles run eight
+// waves (2 x 4, 128 x 64 outputs each), the other tiles four (2 x 2).
+constexpr int dl_waves(int bm, int bn) { return bm * bn >= 256 * 256 ? 8 : 4; }
+
 template <int BM, int BN, int S, int EPI>
-__global__ __launch_bounds__(kThreads) void gemm_dl_kernel(GemmDesc g) {
+__global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmDesc g) {
+    static_assert(S >= 2 && S <= 4, "stages");
+    constexpr int NW = dl_waves(BM, BN);
+    constexpr int WM = 2, WN = NW / 2;          // wave grid: WM along m, WN along n
     using E = Elt<bf16_t>;
     using frag_t = typename E::frag_t;
     constexpr int BK = 64;
     constexpr int ROWE = 64;                    // elements per LDS row
-    constexpr int IPW = (BM + BN) / 32;         // 1 KB load instructions per wave per stage
-    constexpr int IA = BM / 32;                 // of which for the activation tile
-    constexpr int SM = BM / 32;
-    constexpr int SN = BN / 32;
+    constexpr int IPW = (BM + BN) / (8 * NW);   // 1 KB load instructions per wave per stage
+    constexpr int IA = BM / (8 * NW);           // of which for the activation tile
+    constexpr int SM = BM / WM / 16;            // 16-row MFMA blocks per wave (rows m)
+    constexpr int SN = BN / WN / 16;            // 16-col MFMA blocks per wave (cols n)
+    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "load split");
     __shared__ __attribute__((aligned(1024))) bf16_t sA[S][BM * ROWE];
     __shared__ __attribute__((aligned(1024))) bf16_t sW[S][BN * ROWE];
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
     const int wave = tid / kWave;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % WM, wn = wave / WM;
     const int M = g.M, N = g.N, K = g.K;
     const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
     const int lb = xcd_logical_block(blockIdx.x, tiles_m * tiles_n * g.ksplit);
@@ -206,26 +218,27 @@ __global__ __launch_bounds__(kThreads) void gemm_dl_kernel(GemmDesc g) {
     const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.A);
     const bf16_t* __restrict__ W = static_cast<const bf16_t*>(g.W);
 
-    // per load instruction: this lane's element offset (row * ld + swizzled chunk)
+    // per load instruction: this lane's element offset (row * ld + swizzled
+    // chunk) and the wave's 1 KB destination inside a stage (bytes)
     int goff[IPW];
+    uint32_t ldst[IPW];
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
-        const int blk = i * 4 + wave;                       // 8-row block
+        const int blk = i * NW + wave;                      // 8-row block
         const bool isA = i < IA;
         const int rloc = (isA ? blk : blk - BM / 8) * 8 + lane / 8;
         const int c = (lane % 8) ^ ((rloc >> 1) & 7);
         if (isA) goff[i] = min(m0 + rloc, M - 1) * g.lda + c * 8;
         else goff[i] = min(n0 + rloc, N - 1) * K + c * 8;
+        ldst[i] = isA ? lds_addr(&sA[0][blk * 512]) : lds_addr(&sW[0][(blk - BM / 8) * 512]);
     }
+    constexpr uint32_t kStageA = BM * ROWE * 2, kStageW = BN * ROWE * 2;   // bytes
     auto issue = [&](int kt, int st) {
         const int k0 = kbeg + kt * BK;
 #pragma unroll
         for (int i = 0; i < IPW; ++i) {
-            const int blk = i * 4 + wave;
-            if (i < IA)
-                load_lds16(A + goff[i] + k0, &sA[st][blk * 512]);
-            else
-                load_lds16(W + goff[i] + k0, &sW[st][(blk - BM / 8) * 512]);
+            if (i < IA) dma_lds16(A + goff[i] + k0, ldst[i] + st * kStageA);
+            else dma_lds16(W + goff[i] + k0, ldst[i] + st * kStageW);
         }
     };
 
@@ -244,7 +257,9 @@ __global__ __launch_bounds__(kThreads) void gemm_dl_kernel(GemmDesc g) {
         if (st < nk) issue(st, st);
     for (int kt = 0; kt < nk; ++kt) {
         const int st = kt % S;
-        // stage kt complete: allow the loads of the stages issued after it
+        // stage kt complete (the loads of the later stages may stay in
+        // flight); the barrier also ends every wave's reads of the stage
+        // refilled next, read in step kt - 1
         if (kt + S - 1 <= nk) wait_vmcnt<(S - 2) * IPW>();
         else wait_vmcnt<0>();
         barrier_only();
@@ -255,10 +270,10 @@ __global__ __launch_bounds__(kThreads) void gemm_dl_kernel(GemmDesc g) {
             frag_t fa[SM];
 #pragma unroll
             for (int j = 0; j < SM; ++j)
-                fa[j] = *reinterpret_cast<const frag_t*>(&sA[st][(wm * (BM / 2) + j * 16 + lane % 16) * ROWE + ch]);
+                fa[j] = *reinterpret_cast<const frag_t*>(&sA[st][(wm * (BM / WM) + j * 16 + lane % 16) * ROWE + ch]);
 #pragma unroll
             for (int i = 0; i < SN; ++i) {
-                const frag_t fw = *reinterpret_cast<const frag_t*>(&sW[st][(wn * (BN / 2) + i * 16 + lane % 16) * ROWE + ch]);
+                const frag_t fw = *reinterpret_cast<const frag_t*>(&sW[st][(wn * (BN / WN) + i * 16 + lane % 16) * ROWE + ch]);
 #pragma unroll
                 for (int j = 0; j < SM; ++j) acc[i][j] = E::mma(fw, fa[j], acc[i][j]);
             }
@@ -267,11 +282,11 @@ __global__ __launch_bounds__(kThreads) void gemm_dl_kernel(GemmDesc g) {
 
 #pragma unroll
     for (int i = 0; i < SN; ++i) {
-        const int n = n0 + wn * (BN / 2) + i * 16 + grp * 4;
+        const int n = n0 + wn * (BN / WN) + i * 16 + grp * 4;
         if (n >= N) continue;
 #pragma unroll
         for (int j = 0; j < SM; ++j) {
-            const int m = m0 + wm * (BM / 2) + j * 16 + lane % 16;
+            const int m = m0 + wm * (BM / WM) + j * 16 + lane % 16;
             if (m >= M) continue;
             float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
             if (g.ksplit == 1) {
@@ -315,7 +330,7 @@ hipError_t launch_tile(const GemmDesc& g, hipStream_t s) {
 
 template <int BM, int BN, int S>
 hipError_t launch_dl(const GemmDesc& g, hipStream_t s) {
-    dim3 grid(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM) * g.ksplit), block(kThreads);
+    dim3 grid(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM) * g.ksplit), block(kWave * dl_waves(BM, BN));
     switch (g.epilogue) {
         case kEpiBias: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiBias>), grid, block, 0, s, g); break;
         case kEpiBiasResid: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiBiasResid>), grid, block, 0, s, g); break;
@@ -340,37 +355,57 @@ hipError_t launch_reduce(const GemmDesc& g, hipStream_t s) {
     return hipGetLastError();
 }
 
-long groups(const GemmDesc& g, int bm, int bn) {
-    return (long)((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn);
-}
-
 }  // namespace
 
-// Tile choice measured on MI355X (bf16, 2-stage direct-to-LDS main loop):
-// 128x128 sustains the most per CU once the grid has enough groups to give
-// every CU at least one (and to keep the last round's quantisation small);
-// smaller problems run 64x64 tiles, split over K when even those leave CUs idle.
+// Tile choice from a measured cost table. kStepUs[t][n-1] is the time (us)
+// of one 64-deep K step of a whole grid in which every CU holds n workgroups
+// of tile t (MI355X, bf16, direct-to-LDS main loop, K = 2048). A launch costs
+// about steps x kStepUs[t][n_busiest - 1] with n_busiest = ceil(groups / 256);
+// past n = 8 the last measured slope extends the table. Split-K multiplies
+// the groups, divides the steps and adds the partial-sum pass (HBM-bound).
+namespace {
+constexpr int kTiles[6][2] = {{256, 256}, {256, 128}, {128, 128}, {128, 64}, {64, 128}, {64, 64}};
+constexpr double kStepUs[6][8] = {
+    {2.076, 4.126, 6.211, 8.256, 10.266, 12.650, 15.03, 17.408},   // 256x256 (n = 7 interpolated)
+    {1.388, 3.271, 4.815, 6.303, 7.770, 9.414, 10.95, 12.481},     // 256x128
+    {0.962, 1.309, 2.148, 2.750, 3.642, 4.114, 4.76, 5.404},       // 128x128
+    {0.740, 0.986, 1.312, 2.274, 2.990, 3.599, 4.23, 4.855},       // 128x64
+    {0.714, 0.851, 1.064, 1.656, 1.731, 2.160, 2.51, 2.859},       // 64x128
+    {0.584, 0.657, 0.731, 0.954, 1.482, 1.777, 2.11, 2.447},       // 64x64
+};
+
+double step_us(int t, long n) {
+    if (n <= 8) return kStepUs[t][n - 1];
+    const double slope = (kStepUs[t][7] - kStepUs[t][5]) / 2.0;
+    return kStepUs[t][7] + (double)(n - 8) * slope;
+}
+}  // namespace
+
 GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats) {
     GemmPlan p{64, 64, 1};
     if (dtype != kBF16) return p;   // fp32 path: one tile shape
-    GemmDesc g{};
-    g.M = M; g.N = N;
-    if (groups(g, 128, 128) >= (3 * kCUs) / 2) {
-        p.bm = 128; p.bn = 128;
-    } else {
-        const long grp = groups(g, 64, 64);
-        if (grp < kCUs) {
-            int ks = (int)((2 * kCUs + grp - 1) / grp);
-            ks = std::min(ks, std::max(1, K / 256));
-            while (ks > 1 && (size_t)ks * M * N > part_capacity_floats) --ks;
-            p.ksplit = std::max(1, ks);
+    const int steps = K / 64;
+    double best = 1e30;
+    for (int t = 0; t < 6; ++t) {
+        const int bm = kTiles[t][0], bn = kTiles[t][1];
+        const long grp = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+        for (int ks = 1; ks <= 8 && ks <= steps; ++ks) {
+            if (ks > 1 && (size_t)ks * M * N > part_capacity_floats) break;
+            const int per = (steps + ks - 1) / ks;
+            const long n = (grp * ks + kCUs - 1) / kCUs;
+            double us = per * step_us(t, n);
+            // partial sums: ks float planes read, one bf16 plane written, ~4 TB/s, + a launch
+            if (ks > 1) us += 2.0 + ((double)ks * 4 + 2) * M * N / 4.0e6;
+            if (us < best * 0.97) {   // prefer the earlier (larger, unsplit) choice on near-ties
+                best = us;
+                p.bm = bm; p.bn = bn; p.ksplit = ks;
+            }
         }
     }
     if (const char* f = std::getenv("MS_GEMM_TILE")) {   // tuning override "BMxBN"
         int bm = 0, bn = 0;
         if (std::sscanf(f, "%dx%d", &bm, &bn) == 2) {
-            const int ok[6][2] = {{256, 256}, {256, 128}, {128, 128}, {128, 64}, {64, 128}, {64, 64}};
-            for (const auto& t : ok)
+            for (const auto& t : kTiles)
                 if (t[0] == bm && t[1] == bn) { p.bm = bm; p.bn = bn; p.ksplit = 1; }
         }
     }
