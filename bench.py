@@ -302,22 +302,30 @@ def main():
         one_step(i % args.masks)
     torch.cuda.synchronize()
 
+    def row_layers(i):
+        # rows each block of the step actually computes: every token in the dense-prefix
+        # blocks, the masked rows (plus text rows) in the others
+        k = prefix[i]
+        return k * shape.batch * shape.n_tokens + (shape.n_layers - k) * Ms[i]
+
     def timed(k, per_step=False):
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(k + 1)]
         tot_m = 0
+        tot_rl = 0
         torch.cuda.synchronize()
         w0 = time.perf_counter()
         evs[0].record(stream)
         for s in range(k):
             tot_m += one_step(s % args.masks)
+            tot_rl += row_layers(s % args.masks)
             evs[s + 1].record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - w0
         ms = evs[0].elapsed_time(evs[k])
         steps = [evs[s].elapsed_time(evs[s + 1]) for s in range(k)] if per_step else None
-        return ms, wall, tot_m, steps
+        return ms, wall, tot_m, steps, tot_rl
 
-    ms_total, wall, tot_m, step_ms = timed(args.steps, per_step=True)
+    ms_total, wall, tot_m, step_ms, _ = timed(args.steps, per_step=True)
     log(f"[bench] timed {args.steps} steps: {ms_total:.3f} ms (events), {wall * 1e3:.3f} ms (wall)")
     ms_step = ms_total / args.steps
     value = tot_m / (ms_total / 1e3)
@@ -331,13 +339,13 @@ def main():
     kernels, roof = {}, None
     if not args.no_profile_pass:
         MS.profiler_start(MS.KERNEL_CLASSES, capacity=1 << 16)
-        ms_prof, _, tot_m_prof, _ = timed(args.steps)
+        ms_prof, _, tot_m_prof, _, tot_rl_prof = timed(args.steps)
         prof = MS.profiler_stop()
         log(f"[bench] profiled pass: {ms_prof / args.steps:.4f} ms/step; {prof}")
         d, T, L, f = shape.d_model, shape.n_tokens, shape.n_layers, shape.mlp_mult * shape.d_model
         e = 2 if shape.dtype == "bf16" else 4
         nset = 2 if shape.dual_stream else 1
-        m_sum = tot_m_prof * L                      # masked rows summed over the layers of all steps
+        m_sum = tot_rl_prof                         # computed rows summed over the blocks of all steps
         work = {
             "attention": ("mfma", 4.0 * m_sum * T * d),
             "gemm_qkv": ("mfma", 2.0 * m_sum * d * 3 * d),
@@ -363,7 +371,7 @@ def main():
         kname = {"attention": f"attention_fast_kernel<{hd}>"}.get(dom, dom)
         # algorithmic HBM bytes per launch of the dominant kernel
         n_launch = kernels[dom]["launches"]
-        m_avg = tot_m_prof * L / n_launch
+        m_avg = m_sum / n_launch
         alg_bytes = {"attention": (4 * shape.batch * T * d + 4 * m_avg * d) * e / 2}.get(dom)
         tr = measured_traffic(kname)
         if kind == "mfma":

@@ -282,7 +282,6 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
     }
     if (seg >= a.nseg) return;   // grid larger than the tile count: nothing to do
     const int b = a.seg_req[seg];
-    const bf16_t* __restrict__ kvb = static_cast<const bf16_t*>(a.kv) + (long)b * T_ * 2 * d + head * HD;
 
     const int ntiles_all = (T_ + kKeyTile - 1) / kKeyTile;
     const int kt0 = split * a.tiles_per_split;
@@ -333,46 +332,35 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
 
     // Every thread stages both K and V items of the next tile into its own
     // registers, with no branches around the loads, so the loads stay in
-    // flight while the current tile is computed. Addresses: a uniform tile
-    // base plus fixed 32-bit per-thread offsets; only the last, partial tile
-    // clamps its key index (keys past T are masked out of its scores).
-    int offk[C::KPT], offv[C::VPT][2];
-    int keyk[C::KPT], keyv[C::VPT];
+    // flight while the current tile is computed. Buffer loads: the request's
+    // K/V block is the resource (bounded at its last key), each lane keeps a
+    // fixed byte offset, and the tile advances through the scalar offset;
+    // rows past the last key read as zeros (their scores are masked anyway).
+    const auto rsrc = make_rsrc(static_cast<const bf16_t*>(a.kv) + (long)b * T_ * 2 * d,
+                                (uint32_t)T_ * 2u * (uint32_t)d * 2u);
+    uint32_t offk[C::KPT], offv[C::VPT][2];
 #pragma unroll
     for (int j = 0; j < C::KPT; ++j) {
         const int item = min(tid + j * kThreads, C::KITEMS - 1);
-        keyk[j] = item / C::CH;
-        offk[j] = keyk[j] * 2 * d + (item % C::CH) * 8;
+        offk[j] = 2u * (uint32_t)((item / C::CH) * 2 * d + head * HD + (item % C::CH) * 8);
     }
 #pragma unroll
     for (int j = 0; j < C::VPT; ++j) {
         const int item = min(tid + j * kThreads, C::VITEMS - 1);
-        keyv[j] = 2 * (item / C::CH);
+        const int key = 2 * (item / C::CH);
 #pragma unroll
-        for (int e = 0; e < 2; ++e) offv[j][e] = (keyv[j] + e) * 2 * d + d + (item % C::CH) * 8;
+        for (int e = 0; e < 2; ++e)
+            offv[j][e] = 2u * (uint32_t)((key + e) * 2 * d + d + head * HD + (item % C::CH) * 8);
     }
     vec16 pk[C::KPT], pv[C::VPT][2];
     auto gload = [&](int kt) {
-        const int k0 = kt * kKeyTile;
-        const bf16_t* base = kvb + (long)k0 * 2 * d;
-        if (k0 + kKeyTile <= T_) {
+        const uint32_t soff = (uint32_t)kt * kKeyTile * 2u * (uint32_t)d * 2u;
 #pragma unroll
-            for (int j = 0; j < C::KPT; ++j) pk[j] = ld16(base + offk[j]);
+        for (int j = 0; j < C::KPT; ++j) pk[j] = buf_ld16(rsrc, offk[j], soff);
 #pragma unroll
-            for (int j = 0; j < C::VPT; ++j)
+        for (int j = 0; j < C::VPT; ++j)
 #pragma unroll
-                for (int e = 0; e < 2; ++e) pv[j][e] = ld16(base + offv[j][e]);
-        } else {
-            const int last = T_ - 1 - k0;
-#pragma unroll
-            for (int j = 0; j < C::KPT; ++j)
-                pk[j] = ld16(base + offk[j] - (keyk[j] - min(keyk[j], last)) * 2 * d);
-#pragma unroll
-            for (int j = 0; j < C::VPT; ++j)
-#pragma unroll
-                for (int e = 0; e < 2; ++e)
-                    pv[j][e] = ld16(base + offv[j][e] - (keyv[j] + e - min(keyv[j] + e, last)) * 2 * d);
-        }
+            for (int e = 0; e < 2; ++e) pv[j][e] = buf_ld16(rsrc, offv[j][e], soff);
     };
     // V^T rows r hold keys as 32 key pairs; pair p of row r sits at pair slot
     // p ^ (8 * ((r >> 4) & 3)): 4-key groups stay contiguous for the 8-byte
@@ -493,6 +481,16 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
         if (kt0 + 1 < kt1) gload(kt0 + 1);
     }
     __syncthreads();
+    // The Q fragments are complete here (the first tile's stores waited for
+    // every earlier load). Re-defining them through an empty asm statement
+    // tells the compiler so; otherwise it makes the first MFMA of every tile
+    // wait for all loads in flight, including the next tile's prefetch.
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+        for (int kc = 0; kc < C::NK32; ++kc) asm volatile("" : "+v"(qf[qb][kc]));
+        if constexpr (C::K16) asm volatile("" : "+v"(qf16[qb]));
+    }
     for (int kt = kt0; kt < kt1; ++kt) {
         compute(kt & 1, kt * kKeyTile, kt >= kfull);
         if (kt + 1 < kt1) {

@@ -62,6 +62,16 @@ template <> struct Elt<bf16_t> {
 struct alignas(16) vec16 { uint32_t w[4]; };
 
 __device__ __forceinline__ vec16 ld16(const void* p) { return *reinterpret_cast<const vec16*>(p); }
+
+// Buffer-resource loads: a wave-uniform base with a byte bound, a per-lane
+// byte offset and a scalar byte offset. Reads at or past `bytes` return zeros.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ vec16 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(vec16, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
+}
 __device__ __forceinline__ void st16(void* p, const vec16& v) { *reinterpret_cast<vec16*>(p) = v; }
 
 // Four consecutive elements <-> float4.
