@@ -252,6 +252,17 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x4_t a, bf16x4_t b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s4, a), __builtin_bit_cast(s4, b), c, 0, 0, 0);
 }
 
+// Key pair held by V^T storage slot s (0..31) of a 64-key tile. The PV
+// product takes, in k-slot order, keys 32c + 4g .. 32c + 4g + 3 and then
+// 32c + 16 + 4g .. 32c + 16 + 4g + 3 for lane group g (the layout in which the
+// transposed scores leave each lane's probabilities), so storage slots
+// 16c + 4g + (0, 1) hold pairs 16c + 2g + (0, 1) and slots 16c + 4g + (2, 3)
+// hold pairs 16c + 8 + 2g + (0, 1).
+__device__ __forceinline__ int vt_pair_of_slot(int s) {
+    const int c = s >> 4, g = (s >> 2) & 3, j = s & 3;
+    return 16 * c + (j < 2 ? 2 * g + j : 8 + 2 * g + (j - 2));
+}
+
 template <int HD>
 __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a) {
     using C = FastCfg<HD>;
@@ -347,7 +358,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
 #pragma unroll
     for (int j = 0; j < C::VPT; ++j) {
         const int item = min(tid + j * kThreads, C::VITEMS - 1);
-        const int key = 2 * (item / C::CH);
+        const int key = 2 * vt_pair_of_slot(item / C::CH);
 #pragma unroll
         for (int e = 0; e < 2; ++e)
             offv[j][e] = 2u * (uint32_t)((key + e) * 2 * d + d + head * HD + (item % C::CH) * 8);
@@ -362,9 +373,11 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
 #pragma unroll
             for (int e = 0; e < 2; ++e) pv[j][e] = buf_ld16(rsrc, offv[j][e], soff);
     };
-    // V^T rows r hold keys as 32 key pairs; pair p of row r sits at pair slot
-    // p ^ (8 * ((r >> 4) & 3)): 4-key groups stay contiguous for the 8-byte
-    // reads, and the pair-packed stores of one wave cover all 64 banks.
+    // V^T rows r hold the 64 keys as 32 key pairs in the MFMA k-slot order of
+    // P^T (see vt_pair_of_slot): storage slot s holds pair vt_pair_of_slot(s),
+    // placed at s ^ (8 * ((r >> 4) & 3)). Each lane's 8 keys of one PV step are
+    // then one aligned 16-byte read, and the pair-packed stores of one wave
+    // cover all 64 banks.
     auto sstore = [&](int buf) {
 #pragma unroll
         for (int j = 0; j < C::KPT; ++j) {
@@ -461,9 +474,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
             for (int h = 0; h < C::NHS; ++h) {
                 const int x = 8 * (h & 3);   // pair-slot swizzle of rows h*16 .. h*16+15
                 const bf16_t* vrow = &sVt[buf][(h * 16 + l16) * C::VL];
-                const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + 2 * ((16 * c + 2 * grp) ^ x));
-                const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + 2 * ((16 * c + 8 + 2 * grp) ^ x));
-                const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
+                const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(vrow + 2 * ((16 * c + 4 * grp) ^ x));
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb) oacc[qb][h] = mfma32(vf, pf[qb], oacc[qb][h]);
             }
