@@ -357,59 +357,77 @@ hipError_t launch_reduce(const GemmDesc& g, hipStream_t s) {
 
 }  // namespace
 
-// Tile choice from a measured cost table. kStepUs[t][n-1] is the time (us)
-// of one 64-deep K step of a whole grid in which every CU holds n workgroups
-// of tile t (MI355X, bf16, direct-to-LDS main loop, K = 2048). A launch costs
-// about steps x kStepUs[t][n_busiest - 1] with n_busiest = ceil(groups / 256);
-// past n = 8 the last measured slope extends the table. Split-K multiplies
-// the groups, divides the steps and adds the partial-sum pass (HBM-bound).
+// Tile and stage choice from a measured cost table. Each entry gives the
+// time (us) of one 64-deep K step of a whole grid in which every CU holds n
+// = 1..8 workgroups of that tile and stage count (MI355X, bf16, direct-to-LDS
+// main loop, K = 2048; n = 7 interpolated). A launch costs about steps x
+// time(n_busiest) with n_busiest = ceil(groups / 256); past n = 8 the last
+// measured slope extends the table. More stages pay off when few workgroups
+// share a CU (deeper prefetch), fewer when many do (LDS occupancy). Split-K
+// multiplies the groups, divides the steps and adds the partial-sum pass.
 namespace {
-constexpr int kTiles[6][2] = {{256, 256}, {256, 128}, {128, 128}, {128, 64}, {64, 128}, {64, 64}};
-constexpr double kStepUs[6][8] = {
-    {2.076, 4.126, 6.211, 8.256, 10.266, 12.650, 15.03, 17.408},   // 256x256 (n = 7 interpolated)
-    {1.388, 3.271, 4.815, 6.303, 7.770, 9.414, 10.95, 12.481},     // 256x128
-    {0.962, 1.309, 2.148, 2.750, 3.642, 4.114, 4.76, 5.404},       // 128x128
-    {0.740, 0.986, 1.312, 2.274, 2.990, 3.599, 4.23, 4.855},       // 128x64
-    {0.714, 0.851, 1.064, 1.656, 1.731, 2.160, 2.51, 2.859},       // 64x128
-    {0.584, 0.657, 0.731, 0.954, 1.482, 1.777, 2.11, 2.447},       // 64x64
+struct TileCost {
+    int bm, bn, stages;
+    double us[8];
+};
+constexpr TileCost kCost[] = {
+    {256, 256, 2, {2.089, 4.200, 6.182, 8.226, 10.098, 12.692, 15.092, 17.493}},
+    {256, 128, 2, {1.374, 3.288, 4.830, 6.339, 7.887, 9.361, 10.956, 12.551}},
+    {256, 128, 3, {1.407, 3.010, 4.494, 6.012, 7.518, 9.015, 10.509, 12.004}},
+    {128, 128, 2, {0.973, 1.296, 2.178, 2.738, 3.666, 4.057, 4.707, 5.356}},
+    {128, 128, 3, {0.890, 1.692, 2.503, 3.253, 3.979, 4.765, 5.521, 6.277}},
+    {128, 128, 4, {0.837, 1.682, 2.468, 3.274, 4.051, 4.842, 5.617, 6.393}},
+    {128, 64, 2, {0.742, 0.987, 1.294, 2.259, 2.981, 3.553, 4.182, 4.811}},
+    {128, 64, 3, {0.655, 1.098, 1.930, 2.447, 3.079, 3.592, 4.155, 4.717}},
+    {128, 64, 4, {0.625, 1.414, 2.081, 2.694, 3.291, 3.865, 4.434, 5.003}},
+    {64, 128, 2, {0.708, 0.845, 1.070, 1.661, 1.748, 2.135, 2.515, 2.895}},
+    {64, 128, 3, {0.609, 0.804, 1.282, 1.576, 2.074, 2.343, 2.737, 3.131}},
+    {64, 128, 4, {0.593, 1.113, 1.632, 2.147, 2.693, 3.156, 3.659, 4.162}},
+    {64, 64, 2, {0.586, 0.654, 0.736, 0.938, 1.527, 1.747, 2.089, 2.432}},
+    {64, 64, 3, {0.463, 0.557, 0.818, 1.309, 1.543, 1.854, 2.143, 2.431}},
+    {64, 64, 4, {0.424, 0.566, 0.928, 1.313, 1.654, 1.953, 2.224, 2.494}},
 };
 
-double step_us(int t, long n) {
-    if (n <= 8) return kStepUs[t][n - 1];
-    const double slope = (kStepUs[t][7] - kStepUs[t][5]) / 2.0;
-    return kStepUs[t][7] + (double)(n - 8) * slope;
+double step_us(const TileCost& c, long n) {
+    if (n <= 8) return c.us[n - 1];
+    return c.us[7] + (double)(n - 8) * (c.us[7] - c.us[5]) / 2.0;
 }
 }  // namespace
 
 GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats) {
-    GemmPlan p{64, 64, 1};
+    GemmPlan p{64, 64, 1, 2};
     if (dtype != kBF16) return p;   // fp32 path: one tile shape
     const int steps = K / 64;
     double best = 1e30;
-    for (int t = 0; t < 6; ++t) {
-        const int bm = kTiles[t][0], bn = kTiles[t][1];
-        const long grp = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    for (const TileCost& c : kCost) {
+        const long grp = (long)((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn);
         for (int ks = 1; ks <= 8 && ks <= steps; ++ks) {
             if (ks > 1 && (size_t)ks * M * N > part_capacity_floats) break;
             const int per = (steps + ks - 1) / ks;
             const long n = (grp * ks + kCUs - 1) / kCUs;
-            double us = per * step_us(t, n);
+            double us = per * step_us(c, n);
             // partial sums: ks float planes read, one bf16 plane written, ~4 TB/s, + a launch
             if (ks > 1) us += 2.0 + ((double)ks * 4 + 2) * M * N / 4.0e6;
             if (us < best * 0.97) {   // prefer the earlier (larger, unsplit) choice on near-ties
                 best = us;
-                p.bm = bm; p.bn = bn; p.ksplit = ks;
+                p = GemmPlan{c.bm, c.bn, ks, c.stages};
             }
         }
     }
     if (const char* f = std::getenv("MS_GEMM_TILE")) {   // tuning override "BMxBN"
         int bm = 0, bn = 0;
         if (std::sscanf(f, "%dx%d", &bm, &bn) == 2) {
-            for (const auto& t : kTiles)
-                if (t[0] == bm && t[1] == bn) { p.bm = bm; p.bn = bn; p.ksplit = 1; }
+            for (const TileCost& c : kCost)
+                if (c.bm == bm && c.bn == bn && c.stages == 2) p = GemmPlan{bm, bn, 1, 2};
         }
     }
     return p;
+}
+
+// Largest stage count whose LDS fits next to nothing else (160 KB per CU).
+int max_stages(int bm, int bn) {
+    const int per = (bm + bn) * 64 * 2;
+    return std::min(4, (160 * 1024) / per);
 }
 
 hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
@@ -421,40 +439,36 @@ hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
     const int per = (steps + g.ksplit - 1) / g.ksplit;
     g.kchunk = per * bk;
     g.ksplit = (steps + per - 1) / per;
-    hipError_t e;
-    // main loop: direct-to-LDS with 2 stages (default); tuning knob MS_GEMM_PIPE =
-    // "staged" (register-staged double buffer) or "dl4" (direct-to-LDS, 2-4 stages)
-    static const int pipe = [] {
+    if (dtype != kBF16) return launch_tile<float, 64, 64>(g, s);
+    // main loop: direct-to-LDS (default) or the register-staged double buffer
+    // (tuning knob MS_GEMM_PIPE=staged); MS_GEMM_STAGES overrides the stage count
+    static const bool staged = [] {
         const char* v = std::getenv("MS_GEMM_PIPE");
-        if (!v) return 2;
-        return std::strcmp(v, "staged") == 0 ? 0 : std::strcmp(v, "dl4") == 0 ? 4 : 2;
+        return v && std::strcmp(v, "staged") == 0;
     }();
-    if (dtype == kBF16 && pipe == 2) {
-        if (g.bm == 256 && g.bn == 256) e = launch_dl<256, 256, 2>(g, s);
-        else if (g.bm == 256 && g.bn == 128) e = launch_dl<256, 128, 2>(g, s);
-        else if (g.bm == 128 && g.bn == 128) e = launch_dl<128, 128, 2>(g, s);
-        else if (g.bm == 128 && g.bn == 64) e = launch_dl<128, 64, 2>(g, s);
-        else if (g.bm == 64 && g.bn == 128) e = launch_dl<64, 128, 2>(g, s);
-        else e = launch_dl<64, 64, 2>(g, s);
-    } else if (dtype == kBF16 && pipe == 0) {
-        if (g.bm == 256 && g.bn == 256) e = launch_tile<bf16_t, 256, 256>(g, s);
-        else if (g.bm == 256 && g.bn == 128) e = launch_tile<bf16_t, 256, 128>(g, s);
-        else if (g.bm == 128 && g.bn == 128) e = launch_tile<bf16_t, 128, 128>(g, s);
-        else if (g.bm == 128 && g.bn == 64) e = launch_tile<bf16_t, 128, 64>(g, s);
-        else if (g.bm == 64 && g.bn == 128) e = launch_tile<bf16_t, 64, 128>(g, s);
-        else e = launch_tile<bf16_t, 64, 64>(g, s);
-    } else if (dtype == kBF16) {
-        // direct-to-LDS stages: 256x256 64 KB x 2; 256x128 48 KB x 3; 128x128 32 KB x 4; smaller x 4
-        if (g.bm == 256 && g.bn == 256) e = launch_dl<256, 256, 2>(g, s);
-        else if (g.bm == 256 && g.bn == 128) e = launch_dl<256, 128, 3>(g, s);
-        else if (g.bm == 128 && g.bn == 128) e = launch_dl<128, 128, 4>(g, s);
-        else if (g.bm == 128 && g.bn == 64) e = launch_dl<128, 64, 4>(g, s);
-        else if (g.bm == 64 && g.bn == 128) e = launch_dl<64, 128, 4>(g, s);
-        else e = launch_dl<64, 64, 4>(g, s);
-    } else {
-        e = launch_tile<float, 64, 64>(g, s);
+    static const int force_stages = [] {
+        const char* v = std::getenv("MS_GEMM_STAGES");
+        return v ? std::atoi(v) : 0;
+    }();
+    if (staged) {
+        if (g.bm == 256 && g.bn == 256) return launch_tile<bf16_t, 256, 256>(g, s);
+        if (g.bm == 256 && g.bn == 128) return launch_tile<bf16_t, 256, 128>(g, s);
+        if (g.bm == 128 && g.bn == 128) return launch_tile<bf16_t, 128, 128>(g, s);
+        if (g.bm == 128 && g.bn == 64) return launch_tile<bf16_t, 128, 64>(g, s);
+        if (g.bm == 64 && g.bn == 128) return launch_tile<bf16_t, 64, 128>(g, s);
+        return launch_tile<bf16_t, 64, 64>(g, s);
     }
-    return e;
+    int st = force_stages > 0 ? force_stages : (g.stages > 0 ? g.stages : 2);
+    st = std::max(2, std::min(st, max_stages(g.bm, g.bn)));
+    if (g.bm == 256 && g.bn == 256) return launch_dl<256, 256, 2>(g, s);
+    if (g.bm == 256 && g.bn == 128) return st == 3 ? launch_dl<256, 128, 3>(g, s) : launch_dl<256, 128, 2>(g, s);
+    if (g.bm == 128 && g.bn == 128)
+        return st == 4 ? launch_dl<128, 128, 4>(g, s) : st == 3 ? launch_dl<128, 128, 3>(g, s) : launch_dl<128, 128, 2>(g, s);
+    if (g.bm == 128 && g.bn == 64)
+        return st == 4 ? launch_dl<128, 64, 4>(g, s) : st == 3 ? launch_dl<128, 64, 3>(g, s) : launch_dl<128, 64, 2>(g, s);
+    if (g.bm == 64 && g.bn == 128)
+        return st == 4 ? launch_dl<64, 128, 4>(g, s) : st == 3 ? launch_dl<64, 128, 3>(g, s) : launch_dl<64, 128, 2>(g, s);
+    return st == 4 ? launch_dl<64, 64, 4>(g, s) : st == 3 ? launch_dl<64, 64, 3>(g, s) : launch_dl<64, 64, 2>(g, s);
 }
 
 hipError_t launch_gemm_reduce(int dtype, const GemmDesc& g, hipStream_t s) {

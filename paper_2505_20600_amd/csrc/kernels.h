@@ -49,13 +49,14 @@ struct GemmDesc {
     int d;              // kEpiQKV: model width
     int epilogue;
     int bm, bn;         // output tile (from plan_gemm)
+    int stages;         // LDS stages of the bf16 main loop (0: the tile's default)
     int ksplit;         // K-range splits (1: epilogue fused in the GEMM)
     int kchunk;         // set by launch_gemm
     float* part;        // ksplit > 1: [ksplit][M][N] float32 partials
 };
 
 struct GemmPlan {
-    int bm, bn, ksplit;
+    int bm, bn, ksplit, stages;
 };
 
 // Partial buffer the split-K plan may use (float32 elements).

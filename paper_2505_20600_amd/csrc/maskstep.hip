@@ -310,6 +310,7 @@ hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, int cls, hipStream_t st) {
     const ms::GemmPlan p = ms::plan_gemm(s->desc.dtype, g.M, g.N, g.K, ms::kGemmPartFloats);
     g.bm = p.bm;
     g.bn = p.bn;
+    g.stages = p.stages;
     g.ksplit = p.ksplit;
     g.part = static_cast<float*>(s->buf(s->lay.gemm_part));
     hipError_t e;
@@ -784,6 +785,7 @@ ms_status ms_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* 
         p.bm = tile_m;
         p.bn = tile_n;
         p.ksplit = 1;
+        p.stages = 0;
     }
     if (ksplit > 0) p.ksplit = ksplit;
     if (p.ksplit > 1 && (!d_ws || ws_bytes < (size_t)p.ksplit * M * N * 4))
@@ -794,7 +796,7 @@ ms_status ms_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* 
     g.M = M; g.N = N; g.K = K; g.lda = K; g.ldr = N; g.ldc = N;
     g.epilogue = epilogue == MS_EPI_BIAS ? ms::kEpiBias
                : epilogue == MS_EPI_BIAS_RESID ? ms::kEpiBiasResid : ms::kEpiBiasGelu;
-    g.bm = p.bm; g.bn = p.bn; g.ksplit = p.ksplit;
+    g.bm = p.bm; g.bn = p.bn; g.ksplit = p.ksplit; g.stages = p.stages;
     g.part = static_cast<float*>(d_ws);
     hipStream_t st = static_cast<hipStream_t>(stream);
     MS_HIP(ms::launch_gemm(dtype, g, st));
