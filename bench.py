@@ -368,7 +368,7 @@ def main():
         kind, amount = work[dom]
         t_s = kernels[dom]["ms_total"] / 1e3
         hd = shape.d_model // shape.n_heads
-        kname = {"attention": f"attention_fast_kernel<{hd}>"}.get(dom, dom)
+        kname = {"attention": f"attention_dma_kernel<{hd}, 2>"}.get(dom, dom)
         # algorithmic HBM bytes per launch of the dominant kernel
         n_launch = kernels[dom]["launches"]
         m_avg = m_sum / n_launch

@@ -15,6 +15,8 @@
 // A operand (V^T rows) reads contiguous keys. The pairing of MFMA K-slots to
 // keys only has to agree between the two operands of one instruction, which
 // it does by construction.
+#include <cstdlib>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -208,42 +210,6 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnDesc a) {
     }
 }
 
-// ---------------------------------------------------------------------------
-// bf16 kernel for head_dim 64 / 72 / 128.
-//
-// Workgroup = 128 packed query rows of one segment x one head x one key range;
-// each wave owns 32 queries (two 16-query MFMA column blocks), so every K and
-// V fragment read from LDS feeds two MFMAs. The next 64-key K/V tile is
-// fetched into registers while the current one is computed. V is written to
-// LDS transposed, four keys per 8-byte store. head_dim 72 runs its QK^T
-// contraction as two 32-deep steps plus one zero-padded 16-deep step.
-// Softmax: the scale is folded into one FMA before exp2, probabilities are
-// packed to bf16 by the hardware converter.
-// ---------------------------------------------------------------------------
-
-template <int HD>
-struct FastCfg {
-    static constexpr int NK32 = HD / 32;                  // 32-deep QK^T steps
-    static constexpr bool K16 = (HD % 32) != 0;           // one extra 16-deep step
-    static constexpr int HDQ = NK32 * 32 + (K16 ? 16 : 0);
-    // O^T rows: head_dim rows, then rows of ones in V^T whose O^T rows
-    // accumulate the softmax denominator (sum of the bf16 probabilities) on
-    // the matrix cores. head_dim 72 uses its zero-padding rows 72..79 for it;
-    // 64 and 128 get one extra 16-row subtile.
-    static constexpr bool SUM_IN_PAD = (HD % 16) != 0;
-    static constexpr int NHS = (HD + 15) / 16 + (SUM_IN_PAD ? 0 : 1);
-    static constexpr int HDV = NHS * 16;
-    static constexpr int SUMROW = SUM_IN_PAD ? HD : NHS * 16 - 16;  // first ones row
-    static constexpr int KL = HDQ + 8;                    // K row stride in LDS (elements)
-    static constexpr int VL = kKeyTile + 8;               // V^T row stride in LDS (elements)
-    static constexpr int CH = HD / 8;                     // 16-byte chunks per key row
-    static constexpr int KITEMS = kKeyTile * CH;          // K: key x chunk
-    static constexpr int VITEMS = (kKeyTile / 2) * CH;    // V: key pair x chunk
-    static constexpr int KPT = (KITEMS + kThreads - 1) / kThreads;
-    static constexpr int VPT = (VITEMS + kThreads - 1) / kThreads;
-    static_assert(HD % 8 == 0 && HD % 32 <= 16, "head_dim layout");
-};
-
 __device__ __forceinline__ f32x4_t mfma32(bf16x8_t a, bf16x8_t b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
@@ -252,38 +218,91 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x4_t a, bf16x4_t b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s4, a), __builtin_bit_cast(s4, b), c, 0, 0, 0);
 }
 
-// Key pair held by V^T storage slot s (0..31) of a 64-key tile. The PV
-// product takes, in k-slot order, keys 32c + 4g .. 32c + 4g + 3 and then
-// 32c + 16 + 4g .. 32c + 16 + 4g + 3 for lane group g (the layout in which the
-// transposed scores leave each lane's probabilities), so storage slots
-// 16c + 4g + (0, 1) hold pairs 16c + 2g + (0, 1) and slots 16c + 4g + (2, 3)
-// hold pairs 16c + 8 + 2g + (0, 1).
-__device__ __forceinline__ int vt_pair_of_slot(int s) {
-    const int c = s >> 4, g = (s >> 2) & 3, j = s & 3;
-    return 16 * c + (j < 2 ? 2 * g + j : 8 + 2 * g + (j - 2));
-}
+// ---------------------------------------------------------------------------
+// bf16 kernel for head_dim 64 / 72 / 128.
+//
+// Workgroup = 128 packed query rows of one segment x one head x one key range;
+// each wave owns 32 queries (two 16-query MFMA column blocks), so every K and
+// V fragment read from LDS feeds two MFMAs. Transposed scores S^T = K Q^T
+// leave the probabilities in the B-operand layout of O^T = V^T P^T. K and V
+// tiles of 64 keys go global -> LDS with buffer_load_dwordx4 ... lds (no
+// staging registers, no VALU work to store them) into S stages, in natural
+// [key][head_dim] layout;
+// the PV operand V^T is read with the gfx950 transpose read
+// ds_read_b64_tr_b16: within each 16-lane group, lane i receives element
+// (i & 3) of the 8 bytes addressed by lane 4e + (i >> 2), e = 0..3. Each
+// lane therefore addresses V[key0 + (l16 >> 2)][hd0 + 4 (l16 & 3)] and
+// receives V[key0 + e][hd0 + l16], e = 0..3: four keys of one head_dim row,
+// in the k-slot order of P^T. Rows of 128 / 256 bytes carry their 16-byte
+// chunks XOR-swizzled by dma_swz(row) so both the K fragment reads (16 rows)
+// and the transpose reads (8 rows x 32 bytes per half wave) are conflict-free;
+// 144-byte rows (head_dim 72) need no swizzle. Keys past the end read as
+// zeros (buffer bound). The softmax denominator comes from V^T rows of ones:
+// a constant operand for head_dim 64 / 128, and for head_dim 72 the padding
+// rows 72..79, whose lanes address a small LDS block of ones.
+// ---------------------------------------------------------------------------
 
 template <int HD>
-__global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a) {
-    using C = FastCfg<HD>;
-    // two K / V^T tile buffers: the next tile is stored while the current one is read
-    __shared__ __attribute__((aligned(16))) bf16_t sK[2][kKeyTile * C::KL];
-    __shared__ __attribute__((aligned(16))) bf16_t sVt[2][C::HDV * C::VL];
+struct DmaCfg {
+    static constexpr int NK32 = HD / 32;
+    static constexpr bool K16 = (HD % 32) != 0;
+    static constexpr int ROWB = HD * 2;                 // bytes per K / V row
+    static constexpr bool SWZ = ROWB == 128 || ROWB == 256;
+    static constexpr int TILEB = kKeyTile * ROWB;       // bytes per K (or V) tile
+    static constexpr int KPAD = 16;                     // past the K tile: head_dim 72 reads 8 B beyond a row
+    static constexpr int STAGEB = 2 * TILEB + KPAD;     // K tile, pad, V tile
+    static constexpr int INSTR = TILEB / 1024;          // 1 KB copies per tile
+    static constexpr int NQ = 2 * INSTR;                // copies per stage (K then V)
+    static constexpr int IPW_MIN = NQ / 4;              // copies per wave per stage (fewest)
+    static constexpr int IPW_MAX = (NQ + 3) / 4;
+    static constexpr bool SUM_IN_PAD = (HD % 16) != 0;
+    static constexpr int NHS = (HD + 15) / 16 + (SUM_IN_PAD ? 0 : 1);
+    static constexpr int NREAL = (HD + 15) / 16;        // O^T subtiles with V rows
+    static_assert(TILEB % 1024 == 0, "tile copies");
+};
+
+// 16-byte chunk swizzle of a K / V row (see the kernel comment).
+template <int ROWB>
+__device__ __forceinline__ int dma_swz(int r) {
+    if constexpr (ROWB == 128) return 2 * ((r >> 1) & 3) + ((r >> 3) & 1);
+    else if constexpr (ROWB == 256) return 2 * (r & 7) + ((r >> 3) & 1);
+    else return 0;
+}
+
+// One 16-byte-per-lane buffer load into LDS at `lds` + 16 * lane, issued as an
+// opaque instruction (the caller orders it with wait_vmcnt + barrier_only).
+__device__ __forceinline__ void dma_buf16(u32x4_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc),
+                    "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
+}
+
+typedef const __attribute__((address_space(3))) uint8_t* lds_cptr;
+
+__device__ __forceinline__ bf16x4_t ld_tr16(lds_cptr p) {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    const s4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(p));
+    return __builtin_bit_cast(bf16x4_t, v);
+}
+
+template <int HD, int S>
+__global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) {
+    using C = DmaCfg<HD>;
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[S * C::STAGEB + 16];
+    const uint32_t lds0 = lds_addr(smem);
+    const uint32_t ones_rel = S * C::STAGEB;            // 8 bytes of bf16 ones (head_dim 72)
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
     const int wave = tid / kWave;
     const int grp = lane / 16;
     const int l16 = lane % 16;
-    // 1-D launch, logical order head-major (head, split, query tile), placed so
-    // that each XCD works on a contiguous range of heads and keeps their K/V in L2
     const int total = a.n_qtiles_fast * a.nsplit * a.n_heads;
     const int lb = xcd_logical_block(blockIdx.x, total);
     const int head = lb / (a.nsplit * a.n_qtiles_fast);
     const int split = (lb / a.n_qtiles_fast) % a.nsplit;
     const int T_ = a.T, d = a.d;
 
-    // query tile -> segment (128-row tiles counted per segment)
     int tile = lb % a.n_qtiles_fast, seg = 0, row0 = 0, row_end = 0;
     for (; seg < a.nseg; ++seg) {
         const int r0 = a.seg_start[seg], r1 = a.seg_start[seg + 1];
@@ -291,26 +310,47 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
         if (tile < nt) { row0 = r0 + tile * kFastQTile; row_end = r1; break; }
         tile -= nt;
     }
-    if (seg >= a.nseg) return;   // grid larger than the tile count: nothing to do
+    if (seg >= a.nseg) return;
     const int b = a.seg_req[seg];
-
     const int ntiles_all = (T_ + kKeyTile - 1) / kKeyTile;
     const int kt0 = split * a.tiles_per_split;
     const int kt1 = min(ntiles_all, kt0 + a.tiles_per_split);
+    const int nt = max(0, kt1 - kt0);
 
-    if constexpr (C::HDQ > HD) {
-        for (int i = tid; i < 2 * kKeyTile * (C::HDQ - HD); i += kThreads) {
-            const int b = i / (kKeyTile * (C::HDQ - HD)), j = i % (kKeyTile * (C::HDQ - HD));
-            sK[b][(j / (C::HDQ - HD)) * C::KL + HD + j % (C::HDQ - HD)] = 0;
-        }
-    }
-    // V^T rows past head_dim: ones from SUMROW on, zeros before (never written by tiles)
-    for (int i = tid; i < 2 * (C::HDV - HD) * C::VL; i += kThreads) {
-        const int b = i / ((C::HDV - HD) * C::VL), j = i % ((C::HDV - HD) * C::VL);
-        sVt[b][HD * C::VL + j] = (HD + j / C::VL >= C::SUMROW) ? bf16_t(0x3f80) : bf16_t(0);
-    }
+    // constant LDS: the K pads (finite bytes for the head_dim-72 over-read) and the ones block
+    if (tid < S) *reinterpret_cast<uint4*>(smem + tid * C::STAGEB + C::TILEB) = make_uint4(0u, 0u, 0u, 0u);
+    if (tid == S) *reinterpret_cast<uint2*>(smem + S * C::STAGEB) = make_uint2(0x3f803f80u, 0x3f803f80u);
 
-    // Q^T fragments (B operand): query column l16 of block qb, head_dim slots by lane group
+    // buffer resource over request b's K/V block [T][2][d]
+    u32x4_t rsrc;
+    {
+        const uint64_t base = reinterpret_cast<uint64_t>(static_cast<const bf16_t*>(a.kv) + (long)b * T_ * 2 * d);
+        rsrc[0] = (uint32_t)base;
+        rsrc[1] = (uint32_t)(base >> 32) & 0xffffu;
+        rsrc[2] = (uint32_t)T_ * 4u * (uint32_t)d;
+        rsrc[3] = 0x00020000u;
+    }
+    // per copy of this wave: fixed per-lane global byte offset and LDS destination in a stage
+    uint32_t voff[C::IPW_MAX], ldst[C::IPW_MAX];
+#pragma unroll
+    for (int i = 0; i < C::IPW_MAX; ++i) {
+        const int q = min(i * 4 + wave, C::NQ - 1);
+        const bool isV = q >= C::INSTR;
+        const int pos = (q % C::INSTR) * 1024 + lane * 16;
+        const int r = pos / C::ROWB;
+        const int c = ((pos % C::ROWB) / 16) ^ dma_swz<C::ROWB>(r);
+        voff[i] = (uint32_t)(r * 4 * d + (isV ? 2 * d : 0) + head * C::ROWB + c * 16);
+        ldst[i] = __builtin_amdgcn_readfirstlane((uint32_t)((isV ? C::TILEB + C::KPAD : 0) + (q % C::INSTR) * 1024));
+    }
+    auto issue = [&](int kt, int st) {
+        const uint32_t soff = (uint32_t)kt * kKeyTile * 4u * (uint32_t)d;
+        const uint32_t sbase = lds0 + st * C::STAGEB;
+#pragma unroll
+        for (int i = 0; i < C::IPW_MAX; ++i)
+            if (i * 4 + wave < C::NQ) dma_buf16(rsrc, voff[i], soff, sbase + ldst[i]);
+    };
+
+    // Q^T fragments (B operand)
     bf16x8_t qf[2][C::NK32 > 0 ? C::NK32 : 1];
     bf16x4_t qf16[2];
     const bf16_t* __restrict__ q = static_cast<const bf16_t*>(a.q);
@@ -333,6 +373,22 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
         }
     }
 
+    // fragment read offsets inside a stage (bytes)
+    const int fK = dma_swz<C::ROWB>(l16);
+    uint32_t koff[C::NK32 > 0 ? C::NK32 : 1];
+#pragma unroll
+    for (int kc = 0; kc < C::NK32; ++kc) koff[kc] = l16 * C::ROWB + (((4 * kc + grp) ^ fK) * 16);
+    const uint32_t koff16 = l16 * C::ROWB + C::NK32 * 64 + grp * 8;   // head_dim 72: 16-deep step
+    const int rowA = 4 * grp + (l16 >> 2);
+    const int fV = dma_swz<C::ROWB>(rowA);
+    uint32_t voffh[C::NREAL];
+#pragma unroll
+    for (int h = 0; h < C::NREAL; ++h) {
+        const int hd = 16 * h + 4 * (l16 & 3);
+        voffh[h] = C::TILEB + C::KPAD + rowA * C::ROWB + (((hd / 8) ^ fV) * 16) + (hd % 8) * 2;
+    }
+    const bool ones_lane = C::SUM_IN_PAD && (16 * (C::NREAL - 1) + 4 * (l16 & 3)) >= HD;
+
     f32x4_t oacc[2][C::NHS];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
@@ -340,73 +396,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
         for (int h = 0; h < C::NHS; ++h) oacc[qb][h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float m_run[2] = {-INFINITY, -INFINITY};
     const float cs = a.scale_log2;
+    const bf16x8_t onesf = __builtin_bit_cast(bf16x8_t, make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u));
 
-    // Every thread stages both K and V items of the next tile into its own
-    // registers, with no branches around the loads, so the loads stay in
-    // flight while the current tile is computed. Buffer loads: the request's
-    // K/V block is the resource (bounded at its last key), each lane keeps a
-    // fixed byte offset, and the tile advances through the scalar offset;
-    // rows past the last key read as zeros (their scores are masked anyway).
-    const auto rsrc = make_rsrc(static_cast<const bf16_t*>(a.kv) + (long)b * T_ * 2 * d,
-                                (uint32_t)T_ * 2u * (uint32_t)d * 2u);
-    uint32_t offk[C::KPT], offv[C::VPT][2];
-#pragma unroll
-    for (int j = 0; j < C::KPT; ++j) {
-        const int item = min(tid + j * kThreads, C::KITEMS - 1);
-        offk[j] = 2u * (uint32_t)((item / C::CH) * 2 * d + head * HD + (item % C::CH) * 8);
-    }
-#pragma unroll
-    for (int j = 0; j < C::VPT; ++j) {
-        const int item = min(tid + j * kThreads, C::VITEMS - 1);
-        const int key = 2 * vt_pair_of_slot(item / C::CH);
-#pragma unroll
-        for (int e = 0; e < 2; ++e)
-            offv[j][e] = 2u * (uint32_t)((key + e) * 2 * d + d + head * HD + (item % C::CH) * 8);
-    }
-    vec16 pk[C::KPT], pv[C::VPT][2];
-    auto gload = [&](int kt) {
-        const uint32_t soff = (uint32_t)kt * kKeyTile * 2u * (uint32_t)d * 2u;
-#pragma unroll
-        for (int j = 0; j < C::KPT; ++j) pk[j] = buf_ld16(rsrc, offk[j], soff);
-#pragma unroll
-        for (int j = 0; j < C::VPT; ++j)
-#pragma unroll
-            for (int e = 0; e < 2; ++e) pv[j][e] = buf_ld16(rsrc, offv[j][e], soff);
-    };
-    // V^T rows r hold the 64 keys as 32 key pairs in the MFMA k-slot order of
-    // P^T (see vt_pair_of_slot): storage slot s holds pair vt_pair_of_slot(s),
-    // placed at s ^ (8 * ((r >> 4) & 3)). Each lane's 8 keys of one PV step are
-    // then one aligned 16-byte read, and the pair-packed stores of one wave
-    // cover all 64 banks.
-    auto sstore = [&](int buf) {
-#pragma unroll
-        for (int j = 0; j < C::KPT; ++j) {
-            const int item = tid + j * kThreads;
-            if (C::KITEMS % kThreads == 0 || item < C::KITEMS) {
-                const int key = item / C::CH, c = item % C::CH;
-                st16(&sK[buf][key * C::KL + c * 8], pk[j]);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < C::VPT; ++j) {
-            const int item = tid + j * kThreads;
-            if (C::VITEMS % kThreads == 0 || item < C::VITEMS) {
-                const int kp = item / C::CH, c = item % C::CH;
-                // V^T[c*8 + e][2kp .. 2kp+1] = (V[2kp][c*8+e], V[2kp+1][c*8+e])
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int r = c * 8 + e;
-                    const uint32_t w = __builtin_amdgcn_perm(pv[j][1].w[e >> 1], pv[j][0].w[e >> 1],
-                                                             (e & 1) ? 0x07060302u : 0x05040100u);
-                    const int slot = kp ^ (8 * ((r >> 4) & 3));
-                    *reinterpret_cast<uint32_t*>(&sVt[buf][r * C::VL + 2 * slot]) = w;
-                }
-            }
-        }
-    };
-
-    // One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
-    auto compute = [&](int buf, int k0, bool tail) {
+    auto compute = [&](uint32_t sbase, int k0, bool tail) {
         f32x4_t sacc[2][4];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
@@ -414,15 +406,14 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
             for (int ks = 0; ks < 4; ++ks) sacc[qb][ks] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-            const bf16_t* kr = &sK[buf][(ks * 16 + l16) * C::KL];
 #pragma unroll
             for (int kc = 0; kc < C::NK32; ++kc) {
-                const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(kr + kc * 32 + grp * 8);
+                const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(smem + sbase + koff[kc] + ks * 16 * C::ROWB);
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb) sacc[qb][ks] = mfma32(kf, qf[qb][kc], sacc[qb][ks]);
             }
             if constexpr (C::K16) {
-                const bf16x4_t kf = *reinterpret_cast<const bf16x4_t*>(kr + C::NK32 * 32 + grp * 4);
+                const bf16x4_t kf = *reinterpret_cast<const bf16x4_t*>(smem + sbase + koff16 + ks * 16 * C::ROWB);
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb) sacc[qb][ks] = mfma16(kf, qf16[qb], sacc[qb][ks]);
             }
@@ -444,7 +435,6 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
                 mx = fmaxf(fmaxf(mx, fmaxf(sacc[qb][ks][0], sacc[qb][ks][1])), fmaxf(sacc[qb][ks][2], sacc[qb][ks][3]));
             mx = rows_max(mx);
             const float m_new = fmaxf(m_run[qb], mx);
-            // rescale the accumulators only when some query's running max grew
             if (__any(m_new > m_run[qb])) {
                 const float corr = fast_exp2((m_run[qb] - m_new) * cs);
 #pragma unroll
@@ -457,7 +447,13 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) sacc[qb][ks][r] = fast_exp2(fmaf(sacc[qb][ks][r], cs, -mc));
         }
-        // O^T += V^T P^T; K-slots 0..3 = keys 32c + 4*grp + r, slots 4..7 = keys 32c + 16 + 4*grp + r
+        // O^T += V^T P^T; k-slots 0..3 = keys 32c + 4*grp + e, 4..7 = keys 32c + 16 + 4*grp + e
+        uint32_t vbase[C::NREAL];
+#pragma unroll
+        for (int h = 0; h < C::NREAL; ++h) {
+            vbase[h] = lds0 + sbase + voffh[h];
+            asm volatile("" : "+v"(vbase[h]));   // keep the sum: offsets are added per read
+        }
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
             bf16x8_t pf[2];
@@ -472,55 +468,53 @@ __global__ __launch_bounds__(kThreads, 2) void attention_fast_kernel(AttnDesc a)
             }
 #pragma unroll
             for (int h = 0; h < C::NHS; ++h) {
-                const int x = 8 * (h & 3);   // pair-slot swizzle of rows h*16 .. h*16+15
-                const bf16_t* vrow = &sVt[buf][(h * 16 + l16) * C::VL];
-                const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(vrow + 2 * ((16 * c + 4 * grp) ^ x));
+                bf16x8_t vf;
+                if (h >= C::NREAL) {
+                    vf = onesf;
+                } else {
+                    // one base address per head_dim block and tile; the key-block and
+                    // second-half offsets fold into the read instructions
+                    lds_cptr p0 = (lds_cptr)(uintptr_t)vbase[h] + (32 * c) * C::ROWB;
+                    lds_cptr p1 = (lds_cptr)(uintptr_t)vbase[h] + (32 * c + 16) * C::ROWB;
+                    if (h == C::NREAL - 1 && ones_lane) { p0 = (lds_cptr)(uintptr_t)(lds0 + ones_rel); p1 = p0; }
+                    const bf16x4_t lo = ld_tr16(p0), hi = ld_tr16(p1);
+                    vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                }
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb) oacc[qb][h] = mfma32(vf, pf[qb], oacc[qb][h]);
             }
         }
     };
 
-    // One barrier per tile: tile kt is read from buffer kt & 1 while tile kt+1
-    // is stored into the other buffer (last read during tile kt-1, which every
-    // wave finished before the previous barrier); full 64-key tiles need no
-    // key masking, only a partial last tile does.
-    const int kfull = min(kt1, max(kt0, T_ / kKeyTile));
-    if (kt0 < kt1) {
-        gload(kt0);
-        sstore(kt0 & 1);
-        if (kt0 + 1 < kt1) gload(kt0 + 1);
-    }
-    __syncthreads();
-    // The Q fragments are complete here (the first tile's stores waited for
-    // every earlier load). Re-defining them through an empty asm statement
-    // tells the compiler so; otherwise it makes the first MFMA of every tile
-    // wait for all loads in flight, including the next tile's prefetch.
+    // S-stage pipeline: step t reads stage t % S; tiles t + 1 .. t + S - 2 stay in flight
+    for (int t = 0; t < S - 1; ++t)
+        if (t < nt) issue(kt0 + t, t);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
 #pragma unroll
         for (int kc = 0; kc < C::NK32; ++kc) asm volatile("" : "+v"(qf[qb][kc]));
         if constexpr (C::K16) asm volatile("" : "+v"(qf16[qb]));
     }
-    for (int kt = kt0; kt < kt1; ++kt) {
-        compute(kt & 1, kt * kKeyTile, kt >= kfull);
-        if (kt + 1 < kt1) {
-            sstore((kt + 1) & 1);
-            if (kt + 2 < kt1) gload(kt + 2);
-        }
-        __syncthreads();
+    const int kfull = min(kt1, max(kt0, T_ / kKeyTile));
+    for (int t = 0; t < nt; ++t) {
+        if (t + S - 1 <= nt) wait_vmcnt<(S - 2) * C::IPW_MIN>();
+        else wait_vmcnt<0>();
+        barrier_only();
+        if (t + S - 1 < nt) issue(kt0 + t + S - 1, (t + S - 1) % S);
+        const int kt = kt0 + t;
+        compute((t % S) * C::STAGEB, kt * kKeyTile, kt >= kfull);
     }
 
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        // denominator from the ones rows: subtile SUMROW/16, row SUMROW % 16 + 4*grp + r;
-        // with the ones in the padding rows only lane groups 2-3 hold it (rows 72..79)
-        float l = oacc[qb][C::SUMROW / 16][0];
+        float l;
         if constexpr (C::SUM_IN_PAD) {
-            // lane groups 0-1 hold V rows there: zero them and add the swapped halves
-            const float t = grp >= 2 ? l : 0.f;
-            auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+            // rows 72..79 of subtile 4 are the ones rows: lane groups 2-3 hold them
+            const float t0 = grp >= 2 ? oacc[qb][C::NHS - 1][0] : 0.f;
+            auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(t0), __float_as_uint(t0), false, false);
             l = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+        } else {
+            l = oacc[qb][C::NHS - 1][0];
         }
         const int qrow = row0 + wave * 32 + qb * 16 + l16;
         if (qrow >= row_end) continue;
@@ -590,12 +584,9 @@ hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s) {
     if (a.M == 0) return hipSuccess;
     if (attention_fast_path(dtype, a.hd)) {
         dim3 grid(a.n_qtiles_fast * a.n_heads * a.nsplit), block(kThreads);
-        if (a.hd == 64)
-            hipLaunchKernelGGL((attention_fast_kernel<64>), grid, block, 0, s, a);
-        else if (a.hd == 72)
-            hipLaunchKernelGGL((attention_fast_kernel<72>), grid, block, 0, s, a);
-        else
-            hipLaunchKernelGGL((attention_fast_kernel<128>), grid, block, 0, s, a);
+        if (a.hd == 64) hipLaunchKernelGGL((attention_dma_kernel<64, 2>), grid, block, 0, s, a);
+        else if (a.hd == 72) hipLaunchKernelGGL((attention_dma_kernel<72, 2>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((attention_dma_kernel<128, 2>), grid, block, 0, s, a);
         return hipGetLastError();
     }
     dim3 grid(a.n_qtiles, a.n_heads), block(kThreads);
