@@ -242,6 +242,8 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x4_t a, bf16x4_t b, f32x4_t c) {
 // rows 72..79, whose lanes address a small LDS block of ones.
 // ---------------------------------------------------------------------------
 
+constexpr float kRescaleLog2 = 8.0f;   // softmax weights may reach 2^8 before a rescale
+
 template <int HD>
 struct DmaCfg {
     static constexpr int NK32 = HD / 32;
@@ -434,8 +436,12 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
             for (int ks = 0; ks < 4; ++ks)
                 mx = fmaxf(fmaxf(mx, fmaxf(sacc[qb][ks][0], sacc[qb][ks][1])), fmaxf(sacc[qb][ks][2], sacc[qb][ks][3]));
             mx = rows_max(mx);
+            // Rescale only when some query's maximum grew by more than 2^8 (in the
+            // exp2 domain): below that the stale maximum keeps the weights <= 256,
+            // exact in bf16 and fp32 alike, and numerator and denominator share it.
+            // This keeps the accumulators out of VALU work on almost every tile.
             const float m_new = fmaxf(m_run[qb], mx);
-            if (__any(m_new > m_run[qb])) {
+            if (__any((m_new - m_run[qb]) * cs > kRescaleLog2)) {
                 const float corr = fast_exp2((m_run[qb] - m_new) * cs);
 #pragma unroll
                 for (int h = 0; h < C::NHS; ++h) oacc[qb][h] *= corr;
