@@ -400,8 +400,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
     const float cs = a.scale_log2;
     const bf16x8_t onesf = __builtin_bit_cast(bf16x8_t, make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u));
 
-    auto compute = [&](uint32_t sbase, int k0, bool tail) {
-        f32x4_t sacc[2][4];
+    // S^T of one tile (QK^T) into sacc, keys past T masked
+    auto qk = [&](uint32_t sbase, int k0, bool tail, f32x4_t (&sacc)[2][4]) {
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
@@ -429,6 +429,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
                     for (int r = 0; r < 4; ++r)
                         if (k0 + ks * 16 + grp * 4 + r >= T_) sacc[qb][ks][r] = -INFINITY;
         }
+    };
+    // online softmax in place: sacc becomes the weights; running maxima and accumulators updated
+    auto softmax = [&](f32x4_t (&sacc)[2][4]) {
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
             float mx = -INFINITY;
@@ -453,6 +456,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
 #pragma unroll
                 for (int r = 0; r < 4; ++r) sacc[qb][ks][r] = fast_exp2(fmaf(sacc[qb][ks][r], cs, -mc));
         }
+    };
+    // O^T += V^T P^T for one tile
+    auto pv = [&](uint32_t sbase, f32x4_t (&sacc)[2][4]) {
         // O^T += V^T P^T; k-slots 0..3 = keys 32c + 4*grp + e, 4..7 = keys 32c + 16 + 4*grp + e
         uint32_t vbase[C::NREAL];
 #pragma unroll
@@ -462,6 +468,22 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
         }
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
+            // all V^T operands of this 32-key block first, so their reads overlap
+            bf16x8_t vf[C::NHS];
+#pragma unroll
+            for (int h = 0; h < C::NHS; ++h) {
+                if (h >= C::NREAL) {
+                    vf[h] = onesf;
+                } else {
+                    // one base address per head_dim block and tile; the key-block and
+                    // second-half offsets fold into the read instructions
+                    lds_cptr p0 = (lds_cptr)(uintptr_t)vbase[h] + (32 * c) * C::ROWB;
+                    lds_cptr p1 = (lds_cptr)(uintptr_t)vbase[h] + (32 * c + 16) * C::ROWB;
+                    if (h == C::NREAL - 1 && ones_lane) { p0 = (lds_cptr)(uintptr_t)(lds0 + ones_rel); p1 = p0; }
+                    const bf16x4_t lo = ld_tr16(p0), hi = ld_tr16(p1);
+                    vf[h] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                }
+            }
             bf16x8_t pf[2];
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
@@ -473,42 +495,38 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
                 pf[qb] = __builtin_bit_cast(bf16x8_t, w);
             }
 #pragma unroll
-            for (int h = 0; h < C::NHS; ++h) {
-                bf16x8_t vf;
-                if (h >= C::NREAL) {
-                    vf = onesf;
-                } else {
-                    // one base address per head_dim block and tile; the key-block and
-                    // second-half offsets fold into the read instructions
-                    lds_cptr p0 = (lds_cptr)(uintptr_t)vbase[h] + (32 * c) * C::ROWB;
-                    lds_cptr p1 = (lds_cptr)(uintptr_t)vbase[h] + (32 * c + 16) * C::ROWB;
-                    if (h == C::NREAL - 1 && ones_lane) { p0 = (lds_cptr)(uintptr_t)(lds0 + ones_rel); p1 = p0; }
-                    const bf16x4_t lo = ld_tr16(p0), hi = ld_tr16(p1);
-                    vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                }
+            for (int h = 0; h < C::NHS; ++h)
 #pragma unroll
-                for (int qb = 0; qb < 2; ++qb) oacc[qb][h] = mfma32(vf, pf[qb], oacc[qb][h]);
-            }
+                for (int qb = 0; qb < 2; ++qb) oacc[qb][h] = mfma32(vf[h], pf[qb], oacc[qb][h]);
         }
     };
 
+    const int kfull = min(kt1, max(kt0, T_ / kKeyTile));
+    auto fence_q = [&]() {
+        // The Q fragments are complete here. Re-defining them through an empty asm
+        // statement tells the compiler so; otherwise it makes the first MFMA of
+        // every tile wait for all loads in flight, including the next prefetch.
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+            for (int kc = 0; kc < C::NK32; ++kc) asm volatile("" : "+v"(qf[qb][kc]));
+            if constexpr (C::K16) asm volatile("" : "+v"(qf16[qb]));
+        }
+    };
+    f32x4_t sa[2][4];
     // S-stage pipeline: step t reads stage t % S; tiles t + 1 .. t + S - 2 stay in flight
     for (int t = 0; t < S - 1; ++t)
         if (t < nt) issue(kt0 + t, t);
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-        for (int kc = 0; kc < C::NK32; ++kc) asm volatile("" : "+v"(qf[qb][kc]));
-        if constexpr (C::K16) asm volatile("" : "+v"(qf16[qb]));
-    }
-    const int kfull = min(kt1, max(kt0, T_ / kKeyTile));
+    fence_q();
     for (int t = 0; t < nt; ++t) {
         if (t + S - 1 <= nt) wait_vmcnt<(S - 2) * C::IPW_MIN>();
         else wait_vmcnt<0>();
         barrier_only();
         if (t + S - 1 < nt) issue(kt0 + t + S - 1, (t + S - 1) % S);
         const int kt = kt0 + t;
-        compute((t % S) * C::STAGEB, kt * kKeyTile, kt >= kfull);
+        qk((t % S) * C::STAGEB, kt * kKeyTile, kt >= kfull, sa);
+        softmax(sa);
+        pv((t % S) * C::STAGEB, sa);
     }
 
 #pragma unroll
