@@ -19,3 +19,4 @@ from .stack import (  # noqa: F401
     rounder,
 )
 from .planner import best_dense_prefix, greedy_choice, pipeline_latency  # noqa: F401
+from .ycache import dense_inputs, kv_cache_of_inputs, kv_of_inputs, masked_stack_y  # noqa: F401
