@@ -87,9 +87,12 @@ typedef struct {
     const void *w_2, *b_2;       /* [d][f], [d] */
 } ms_layer_weights;
 
-typedef enum { MS_KV_DEVICE = 0, MS_KV_HOST_PINNED = 1 } ms_kv_kind;
+typedef enum {
+    MS_KV_DEVICE = 0, MS_KV_HOST_PINNED = 1,   /* K/V caching (Sec. 3.1, Fig. 7) */
+    MS_Y_DEVICE = 2, MS_Y_HOST_PINNED = 3      /* Y caching (Sec. 3.1, Fig. 5 bottom) */
+} ms_kv_kind;
 
-/* Where the per-layer cached K/V come from.
+/* Where the per-layer cache comes from.
  *  MS_KV_DEVICE:      layer[l] is a device [B][T][2][d] buffer, resident in
  *                     HBM; it is also the working buffer, so the masked rows
  *                     are overwritten with fresh K/V during the step.
@@ -100,12 +103,19 @@ typedef enum { MS_KV_DEVICE = 0, MS_KV_HOST_PINNED = 1 } ms_kv_kind;
  *                     waits until the compute stream has finished with the
  *                     layer that used the slot before. With n_slots >= the
  *                     number of cached layers every load starts at once
- *                     (MI355X's HBM holds a whole stack's K/V easily). */
+ *                     (MI355X's HBM holds a whole stack's K/V easily).
+ *  MS_Y_DEVICE:       layer[l] is a device [B][N][d] buffer: block l's cached
+ *                     input hidden state of the image tokens (only unmasked
+ *                     rows are read). Each cached block recomputes the K/V of
+ *                     the unmasked tokens from it (mask_recompute_kv) into the
+ *                     workspace; half the cache bytes of the K/V kinds.
+ *  MS_Y_HOST_PINNED:  layer[l] is a pinned host [B][N][d] buffer; slots are
+ *                     device [B][N][d] buffers used as for MS_KV_HOST_PINNED. */
 typedef struct {
     int32_t kind;
     const void* const* layer;   /* [n_layers] */
-    int32_t n_slots;            /* MS_KV_HOST_PINNED only, >= 1 */
-    void* const* slots;         /* [n_slots], MS_KV_HOST_PINNED only */
+    int32_t n_slots;            /* host-pinned kinds only, >= 1 */
+    void* const* slots;         /* [n_slots], host-pinned kinds only */
 } ms_kv_source;
 
 typedef struct ms_step ms_step;   /* opaque host object, one per mask set */
@@ -198,10 +208,26 @@ ms_status mask_scatter_rows(ms_step* step, const void* d_xm, const void* d_ycach
 ms_status cache_prefetch_layer(ms_step* step, int32_t layer, const void* h_kv, void* d_slot,
                                void* copy_stream, void* wait_event, void* signal_event);
 
+/* The same block-wise loading for Y caching: the unmasked image rows of
+ * layer `layer`'s cached block input, h_yin [B][N][d] (pinned) -> d_slot
+ * [B][N][d] at the same rows (copy-engine copies of merged runs, as above). */
+ms_status cache_prefetch_inputs(ms_step* step, int32_t layer, const void* h_yin, void* d_slot,
+                                void* copy_stream, void* wait_event, void* signal_event);
+
+/* Y caching (Sec. 3.1, Fig. 5 bottom: the unmasked tokens are replenished from
+ * the cached activations): writes into the working K/V d_kv [B][T][2][d] the
+ * K and V of every unmasked image token, computed from its cached block
+ * input d_yin [B][N][d] with the block's LN1 and the K/V columns of its QKV
+ * projection (image weight set, w[0]). Run it before mask_block_forward, which
+ * then fills the masked rows. `w` as for mask_block_forward. Asynchronous on
+ * `stream`; nothing is written when no token is unmasked. */
+ms_status mask_recompute_kv(ms_step* step, int32_t layer, const ms_layer_weights* w, const void* d_yin,
+                            void* d_kv, void* stream);
+
 /* The whole step: gather, the n_layers blocks (the first k of them over every
- * token, see mask_step_set_dense_prefix), final scatter, with the cache read
- * from HBM or streamed per layer from pinned host memory on copy_stream
- * through the slot ring, ahead of the compute stream (Fig. 8). `w` holds n_layers
+ * token, see mask_step_set_dense_prefix), final scatter, with the cache (any
+ * ms_kv_kind) read from HBM or streamed per layer from pinned host memory on
+ * copy_stream through the slot ring, ahead of the compute stream (Fig. 8). `w` holds n_layers
  * weight sets ([n_layers][2] when dual_stream: image, text). d_x [B][T][d]
  * holds the current hidden states (only masked rows and text rows are read);
  * d_y [B][T][d] receives the output; it may equal d_ycache. With the

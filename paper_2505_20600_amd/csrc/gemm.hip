@@ -56,7 +56,7 @@ __device__ __forceinline__ void epilogue_store(const GemmDesc& g, int m, int n, 
             store4<T>(static_cast<T*>(g.C) + (long)m * g.ldc + n, v);
         } else {
             const long tok = g.rows[m];
-            store4<T>(static_cast<T*>(g.kv) + tok * 2 * g.d + (n - g.d), v);
+            store4<T>(static_cast<T*>(g.kv) + tok * g.kvld + (n - g.d), v);
         }
     } else {
         store4<T>(static_cast<T*>(g.C) + (long)m * g.ldc + n, v);

@@ -29,10 +29,11 @@ hipError_t launch_scatter(const void* xm, const int32_t* rows, const int32_t* in
                           const void* ycache, void* y, int M, int total_rows, int row_bytes,
                           hipStream_t s);
 
-// a3 / a8: y = LN(x) row-wise; rows [0, m_split) use (g1, b1), the rest (g0, b0).
+// a3 / a8: y[i] = LN(x[idx ? idx[i] : i]) row-wise; rows [0, m_split) use (g1, b1),
+// the rest (g0, b0).
 hipError_t launch_layernorm(int dtype, const void* x, const void* g0, const void* b0,
                             const void* g1, const void* b1, int m_split, void* y, int M, int d,
-                            float eps, hipStream_t s);
+                            float eps, hipStream_t s, const int32_t* idx = nullptr);
 
 enum Epilogue { kEpiBias = 0, kEpiBiasResid = 1, kEpiBiasGelu = 2, kEpiQKV = 3 };
 
@@ -41,12 +42,13 @@ struct GemmDesc {
     const void* W;      // [N][K] weights
     const void* bias;   // [N]
     const void* R;      // [M][N] residual (kEpiBiasResid), row stride ldr
-    void* C;            // [M][N] output, row stride ldc (kEpiQKV: Q columns [0, d))
-    void* kv;           // kEpiQKV: [B*T][2][d] working K/V
+    void* C;            // [M][N] output, row stride ldc (kEpiQKV: columns [0, d) only)
+    void* kv;           // kEpiQKV: columns [d, N) of packed row m go to kv + rows[m] * kvld
     const int32_t* rows;// kEpiQKV: flat token row of each packed row
+    int kvld;           // kEpiQKV: row stride of kv (elements)
     int M, N, K;
     int lda, ldr, ldc;
-    int d;              // kEpiQKV: model width
+    int d;              // kEpiQKV: columns that go to C (d for Q|K|V, 0 for K|V only)
     int epilogue;
     int bm, bn;         // output tile (from plan_gemm)
     int stages;         // LDS stages of the bf16 main loop (0: the tile's default)

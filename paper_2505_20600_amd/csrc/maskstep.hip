@@ -20,7 +20,7 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 1;
+constexpr int32_t kAbiVersion = 2;
 constexpr int kMaxBatch = 64;
 // Host-to-device copy spans are merged across masked gaps of at most this
 // many bytes: a gap costs less PCIe time than one more copy submission.
@@ -57,6 +57,7 @@ struct Layout {
     size_t rows, inv, seg_start, seg_req, cu_tiles;              // masked-row packing
     size_t rows_d, inv_d, seg_start_d, seg_req_d, cu_tiles_d;    // every-token packing
     size_t ones;                                                 // all-ones mask [B][N]
+    size_t u_src, u_tok;                                         // unmasked image rows (Y caching)
     size_t xm, a, q, o, h, u, kv_dense, part_o, part_ml, gemm_part, total;
 };
 
@@ -112,6 +113,8 @@ Layout make_layout(const ms_model_desc& d, int32_t B) {
     L.seg_req_d = take(ms::kMaxSegments * 4);
     L.cu_tiles_d = take((ms::kMaxSegments + 1) * 4);
     L.ones = take((size_t)B * N);
+    L.u_src = take((size_t)B * N * 4);
+    L.u_tok = take((size_t)B * N * 4);
     L.xm = take(BT * dm * e);
     L.a = take(BT * dm * e);
     L.q = take(BT * dm * e);
@@ -184,6 +187,9 @@ struct ms_step {
     bool dense_ready = false;
     int dense_prefix = 0;
     std::vector<Span> spans;
+    // unmasked image rows: index into a [B][N] input cache and flat token row (Y caching)
+    int U = 0;
+    std::vector<int32_t> h_usrc, h_utok;
     std::vector<hipEvent_t> ev_copied, ev_consumed;
     hipEvent_t ev_start = nullptr;
 
@@ -357,7 +363,7 @@ ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w
         g.kv = kv;
         g.rows = pk.rows + r.r0;
         g.M = r.r1 - r.r0; g.N = 3 * d; g.K = d;
-        g.lda = d; g.ldc = d; g.d = d;
+        g.lda = d; g.ldc = d; g.d = d; g.kvld = 2 * d;
         g.epilogue = ms::kEpiQKV;
         MS_HIP(run_gemm(s, g, MS_K_GEMM_QKV, st));
     }
@@ -416,15 +422,44 @@ ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w
     return MS_OK;
 }
 
-ms_status prefetch(ms_step* s, const void* h_kv, void* d_slot, hipStream_t cs, hipEvent_t wait) {
+// Y caching (Sec. 3.1, Fig. 5 bottom): K/V of the unmasked image tokens from
+// their cached block input y_in [B][N][d]: LayerNorm of the gathered rows,
+// then the K/V columns of the QKV projection, written to their token rows of
+// the working K/V [B][T][2][d]. Image weights (unmasked tokens are image tokens).
+ms_status recompute_kv(ms_step* s, const ms_layer_weights* w, const void* y_in, void* kv, hipStream_t st) {
+    if (s->U == 0) return MS_OK;
+    const int d = s->d, e = s->elt;
+    void* a = s->buf(s->lay.u);
+    {
+        ProfScope p(MS_K_LAYERNORM, st);
+        MS_HIP(ms::launch_layernorm(s->desc.dtype, y_in, w->ln1_g, w->ln1_b, w->ln1_g, w->ln1_b, 0, a, s->U, d,
+                                    s->desc.ln_eps, st, s->at<int32_t>(s->lay.u_src)));
+    }
+    ms::GemmDesc g{};
+    g.A = a;
+    g.W = static_cast<const char*>(w->w_qkv) + (size_t)d * d * e;
+    g.bias = static_cast<const char*>(w->b_qkv) + (size_t)d * e;
+    g.kv = kv; g.rows = s->at<int32_t>(s->lay.u_tok);
+    g.M = s->U; g.N = 2 * d; g.K = d; g.lda = d; g.ldc = 2 * d; g.d = 0; g.kvld = 2 * d;
+    g.epilogue = ms::kEpiQKV;
+    MS_HIP(run_gemm(s, g, MS_K_GEMM_QKV, st));
+    return MS_OK;
+}
+
+// Loads the unmasked image rows of one block's cache from pinned host memory:
+// K/V rows [B][N][2][d] -> slot [B][T][2][d] at n_text + n, or (y) block
+// input rows [B][N][d] -> slot [B][N][d] in place.
+ms_status prefetch(ms_step* s, const void* h_kv, void* d_slot, hipStream_t cs, hipEvent_t wait,
+                   bool y = false) {
     if (wait) MS_HIP(hipStreamWaitEvent(cs, wait, 0));
     ProfScope p(MS_K_COPY, cs);
-    const size_t row_bytes = 2ull * s->d * s->elt;
+    const size_t row_bytes = (y ? 1ull : 2ull) * s->d * s->elt;
+    const size_t drows = y ? (size_t)s->N : (size_t)s->T, dtext = y ? 0 : (size_t)s->desc.n_text;
     const char* src = static_cast<const char*>(h_kv);
     char* dst = static_cast<char*>(d_slot);
     for (const Span& sp : s->spans) {
         const size_t so = ((size_t)sp.b * s->N + sp.n0) * row_bytes;
-        const size_t dof = ((size_t)sp.b * s->T + s->desc.n_text + sp.n0) * row_bytes;
+        const size_t dof = ((size_t)sp.b * drows + dtext + sp.n0) * row_bytes;
         MS_HIP(hipMemcpyAsync(dst + dof, src + so, (size_t)(sp.n1 - sp.n0) * row_bytes,
                               hipMemcpyHostToDevice, cs));
     }
@@ -432,8 +467,8 @@ ms_status prefetch(ms_step* s, const void* h_kv, void* d_slot, hipStream_t cs, h
 }
 
 ms_status prefetch_signal(ms_step* s, const void* h_kv, void* d_slot, hipStream_t cs, hipEvent_t wait,
-                          hipEvent_t signal) {
-    ms_status st = prefetch(s, h_kv, d_slot, cs, wait);
+                          hipEvent_t signal, bool y = false) {
+    ms_status st = prefetch(s, h_kv, d_slot, cs, wait, y);
     if (st != MS_OK) return st;
     if (signal) MS_HIP(hipEventRecord(signal, cs));
     return MS_OK;
@@ -529,6 +564,19 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
     finish_packing(p, *desc, batch, s->T, s->hd);
     s->all_masked = p.M == batch * s->T;
     plan_spans(s, hmask);
+    for (int b = 0; b < batch; ++b)
+        for (int n = 0; n < s->N; ++n)
+            if (!hmask[(size_t)b * s->N + n]) {
+                s->h_usrc.push_back(b * s->N + n);
+                s->h_utok.push_back(b * s->T + desc->n_text + n);
+            }
+    s->U = (int)s->h_usrc.size();
+    if (s->U > 0) {
+        e = hipMemcpyAsync(s->buf(lay.u_src), s->h_usrc.data(), s->U * sizeof(int32_t), hipMemcpyHostToDevice, hs);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(s->buf(lay.u_tok), s->h_utok.data(), s->U * sizeof(int32_t), hipMemcpyHostToDevice, hs);
+        if (e != hipSuccess) return bail(fail(MS_EHIP, "unmasked-row upload: %s", hipGetErrorString(e)));
+    }
     st = ensure_events(s, 2);
     if (st != MS_OK) return bail(st);
     e = hipEventCreateWithFlags(&s->ev_start, hipEventDisableTiming);
@@ -646,14 +694,40 @@ ms_status cache_prefetch_layer(ms_step* s, int32_t layer, const void* h_kv, void
     return st == MS_OK ? ok() : st;
 }
 
+ms_status cache_prefetch_inputs(ms_step* s, int32_t layer, const void* h_yin, void* d_slot,
+                                void* copy_stream, void* wait_event, void* signal_event) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (layer < 0 || layer >= s->desc.n_layers) return fail(MS_EINVAL, "layer %d out of range", layer);
+    if (!h_yin || !d_slot) return fail(MS_EINVAL, "h_yin or slot is NULL");
+    if (!aligned16(h_yin) || !aligned16(d_slot)) return fail(MS_EALIGN, "h_yin / slot not 16-byte aligned");
+    ms_status st = check_pinned(h_yin);
+    if (st != MS_OK) return st;
+    st = prefetch_signal(s, h_yin, d_slot, static_cast<hipStream_t>(copy_stream),
+                         static_cast<hipEvent_t>(wait_event), static_cast<hipEvent_t>(signal_event), true);
+    return st == MS_OK ? ok() : st;
+}
+
+ms_status mask_recompute_kv(ms_step* s, int32_t layer, const ms_layer_weights* w, const void* d_yin,
+                            void* d_kv, void* stream) {
+    if (!s) return fail(MS_ESTATE, "no step context");
+    if (layer < 0 || layer >= s->desc.n_layers) return fail(MS_EINVAL, "layer %d out of range", layer);
+    if (!w || !d_kv || (!d_yin && s->U > 0)) return fail(MS_EINVAL, "NULL argument");
+    if (!aligned16(d_yin) || !aligned16(d_kv)) return fail(MS_EALIGN, "pointer not 16-byte aligned");
+    ms_status st = check_weights(s, w);
+    if (st != MS_OK) return st;
+    st = recompute_kv(s, w, d_yin, d_kv, static_cast<hipStream_t>(stream));
+    return st == MS_OK ? ok() : st;
+}
+
 ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* d_x,
                              const void* d_ycache, const ms_kv_source* kv, void* d_y,
                              void* compute_stream, void* copy_stream) {
     if (!s) return fail(MS_ESTATE, "no step context");
     if (!w || !d_x || !kv || !d_y) return fail(MS_EINVAL, "NULL argument");
     if (!d_ycache && !s->all_masked) return fail(MS_EINVAL, "y_cache may be NULL only when every token is masked");
-    if (kv->kind != MS_KV_DEVICE && kv->kind != MS_KV_HOST_PINNED) return fail(MS_EINVAL, "unknown kv kind %d", kv->kind);
+    if (kv->kind < MS_KV_DEVICE || kv->kind > MS_Y_HOST_PINNED) return fail(MS_EINVAL, "unknown kv kind %d", kv->kind);
     if (!kv->layer) return fail(MS_EINVAL, "kv->layer is NULL");
+    const bool ycache = kv->kind == MS_Y_DEVICE || kv->kind == MS_Y_HOST_PINNED;
     const int L = s->desc.n_layers;
     const int k = s->dense_prefix;
     const int wstride = s->desc.dual_stream ? 2 : 1;
@@ -663,10 +737,10 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         ms_status st = check_weights(s, w + (size_t)l * wstride);
         if (st != MS_OK) return st;
     }
-    const bool pinned = kv->kind == MS_KV_HOST_PINNED;
+    const bool pinned = kv->kind == MS_KV_HOST_PINNED || kv->kind == MS_Y_HOST_PINNED;
     const int n_slots = pinned ? kv->n_slots : 0;
     if (pinned) {
-        if (n_slots < 1 || !kv->slots) return fail(MS_EINVAL, "pinned K/V needs n_slots >= 1 device slots");
+        if (n_slots < 1 || !kv->slots) return fail(MS_EINVAL, "a pinned cache needs n_slots >= 1 device slots");
         for (int i = 0; i < n_slots; ++i) {
             if (!kv->slots[i]) return fail(MS_EINVAL, "kv->slots[%d] is NULL", i);
             if (!aligned16(kv->slots[i])) return fail(MS_EALIGN, "kv->slots[%d] not 16-byte aligned", i);
@@ -694,7 +768,8 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             MS_HIP(hipEventRecord(s->ev_start, cs));
             MS_HIP(hipStreamWaitEvent(ps, s->ev_start, 0));
             for (int j = 0; j < std::min(n_slots, n_cached); ++j) {
-                ms_status st = prefetch_signal(s, kv->layer[k + j], kv->slots[j], ps, nullptr, s->ev_copied[j]);
+                ms_status st = prefetch_signal(s, kv->layer[k + j], kv->slots[j], ps, nullptr, s->ev_copied[j],
+                                               ycache);
                 if (st != MS_OK) return st;
             }
         }
@@ -725,15 +800,23 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         }
         for (int l = k; l < L; ++l) {
             const int j = l - k;
-            void* kvbuf = const_cast<void*>(kv->layer[l]);
+            void* src = const_cast<void*>(kv->layer[l]);
             if (pinned) {
-                kvbuf = kv->slots[j % n_slots];
+                src = kv->slots[j % n_slots];
                 if (serialize) {
-                    ms_status st = prefetch(s, kv->layer[l], kvbuf, cs, nullptr);
+                    ms_status st = prefetch(s, kv->layer[l], src, cs, nullptr, ycache);
                     if (st != MS_OK) return st;
                 } else if (stream_cache) {
                     MS_HIP(hipStreamWaitEvent(cs, s->ev_copied[j % n_slots], 0));
                 }
+            }
+            // K/V variant: the cache is the working K/V; Y variant: the unmasked
+            // K/V are recomputed from the cached block input into the workspace
+            void* kvbuf = src;
+            if (ycache) {
+                kvbuf = s->buf(s->lay.kv_dense);
+                ms_status st = recompute_kv(s, w + (size_t)l * wstride, src, kvbuf, cs);
+                if (st != MS_OK) return st;
             }
             ms_status st = block_forward(s, mp, w + (size_t)l * wstride, xm, kvbuf, cs);
             if (st != MS_OK) return st;
@@ -741,7 +824,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 const int sl = j % n_slots;
                 MS_HIP(hipEventRecord(s->ev_consumed[sl], cs));
                 st = prefetch_signal(s, kv->layer[l + n_slots], kv->slots[sl], ps, s->ev_consumed[sl],
-                                     s->ev_copied[sl]);
+                                     s->ev_copied[sl], ycache);
                 if (st != MS_OK) return st;
             }
         }

@@ -71,7 +71,7 @@ template <typename T>
 __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
     const T* __restrict__ x, const T* __restrict__ g0, const T* __restrict__ b0,
     const T* __restrict__ g1, const T* __restrict__ b1, int m_split, T* __restrict__ y, int M,
-    int d, float eps) {
+    int d, float eps, const int32_t* __restrict__ idx) {
     constexpr int V = 16 / sizeof(T);   // elements per 16-byte vector
     const int lane = threadIdx.x % kWave;
     const int row = blockIdx.x * kLnWaves + threadIdx.x / kWave;
@@ -79,7 +79,7 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
     const T* gam = row < m_split ? g1 : g0;
     const T* bet = row < m_split ? b1 : b0;
     const int nvec = d / V;
-    const T* xr = x + (long)row * d;
+    const T* xr = x + (long)(idx ? idx[row] : row) * d;
     float v[kLnMaxVecPerLane][V];
     float s = 0.f;
 #pragma unroll
@@ -167,7 +167,7 @@ hipError_t launch_scatter(const void* xm, const int32_t* rows, const int32_t* in
 
 hipError_t launch_layernorm(int dtype, const void* x, const void* g0, const void* b0,
                             const void* g1, const void* b1, int m_split, void* y, int M, int d,
-                            float eps, hipStream_t s) {
+                            float eps, hipStream_t s, const int32_t* idx) {
     if (M == 0) return hipSuccess;
     dim3 grid((M + kLnWaves - 1) / kLnWaves), block(kLnWaves * kWave);
     if (dtype == kBF16) {
@@ -175,13 +175,13 @@ hipError_t launch_layernorm(int dtype, const void* x, const void* g0, const void
                            static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(g0),
                            static_cast<const bf16_t*>(b0), static_cast<const bf16_t*>(g1),
                            static_cast<const bf16_t*>(b1), m_split, static_cast<bf16_t*>(y), M, d,
-                           eps);
+                           eps, idx);
     } else {
         hipLaunchKernelGGL(layernorm_kernel<float>, grid, block, 0, s,
                            static_cast<const float*>(x), static_cast<const float*>(g0),
                            static_cast<const float*>(b0), static_cast<const float*>(g1),
                            static_cast<const float*>(b1), m_split, static_cast<float*>(y), M, d,
-                           eps);
+                           eps, idx);
     }
     return hipGetLastError();
 }

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libmaskstep.so")
 
 MS_OK, MS_EINVAL, MS_ESHAPE, MS_EDTYPE, MS_EALIGN, MS_ENOTPINNED, MS_EWORKSPACE, MS_ESTATE, MS_EHIP = range(9)
 MS_FP32, MS_BF16 = 0, 1
-MS_KV_DEVICE, MS_KV_HOST_PINNED = 0, 1
+MS_KV_DEVICE, MS_KV_HOST_PINNED, MS_Y_DEVICE, MS_Y_HOST_PINNED = 0, 1, 2, 3
 
 STATUS_NAMES = {0: "MS_OK", 1: "MS_EINVAL", 2: "MS_ESHAPE", 3: "MS_EDTYPE", 4: "MS_EALIGN",
                 5: "MS_ENOTPINNED", 6: "MS_EWORKSPACE", 7: "MS_ESTATE", 8: "MS_EHIP"}
@@ -75,6 +75,8 @@ def load() -> C.CDLL:
             "mask_block_forward": (i32, [vp, i32, C.POINTER(LayerWeights), vp, vp, vp]),
             "mask_scatter_rows": (i32, [vp, vp, vp, vp, vp]),
             "cache_prefetch_layer": (i32, [vp, i32, vp, vp, vp, vp, vp]),
+            "cache_prefetch_inputs": (i32, [vp, i32, vp, vp, vp, vp, vp]),
+            "mask_recompute_kv": (i32, [vp, i32, C.POINTER(LayerWeights), vp, vp, vp]),
             "mask_stack_forward": (i32, [vp, C.POINTER(LayerWeights), vp, vp, C.POINTER(KVSource),
                                          vp, vp, vp]),
             "mask_step_destroy": (None, [vp]),
@@ -95,7 +97,8 @@ def load() -> C.CDLL:
 
 EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask_step_init",
             "mask_step_get_info", "mask_step_index", "mask_gather_rows", "mask_block_forward",
-            "mask_scatter_rows", "cache_prefetch_layer", "mask_stack_forward", "mask_step_destroy",
+            "mask_scatter_rows", "cache_prefetch_layer", "cache_prefetch_inputs", "mask_recompute_kv",
+            "mask_stack_forward", "mask_step_destroy",
             "mask_step_set_dense_prefix", "mask_plan_dense_prefix",
             "mask_profiler_start", "mask_profiler_stop", "ms_linear")
 
@@ -262,17 +265,29 @@ class MaskStep:
         _check(self._lib.cache_prefetch_layer(self.handle, layer, _ptr(h_kv), _ptr(d_slot),
                                               _stream(copy_stream), ev(wait_event), ev(signal_event)))
 
+    def prefetch_inputs(self, layer: int, h_yin, d_slot, copy_stream, wait_event=None, signal_event=None):
+        ev = lambda e: None if e is None else (e if isinstance(e, int) else e.cuda_event)
+        _check(self._lib.cache_prefetch_inputs(self.handle, layer, _ptr(h_yin), _ptr(d_slot),
+                                               _stream(copy_stream), ev(wait_event), ev(signal_event)))
+
+    def recompute_kv(self, layer: int, weights_c, y_in, kv, stream=None):
+        """K/V of the unmasked image tokens from their cached block input (Y caching)."""
+        _check(self._lib.mask_recompute_kv(self.handle, layer, weights_c, _ptr(y_in), _ptr(kv), _stream(stream)))
+
     def set_dense_prefix(self, k: int, stream=None):
         _check(self._lib.mask_step_set_dense_prefix(self.handle, k, _stream(stream)))
 
     def stack_forward(self, weights_c, x, ycache, kv_layers, y, *, pinned: bool = False, slots=(),
-                      stream=None, copy_stream=None):
-        """``weights_c`` from weights_array(); ``kv_layers``: [L] tensors (device or pinned host);
-        ``slots``: device [B][T][2][d] buffers the pinned layers stream through."""
+                      stream=None, copy_stream=None, inputs: bool = False):
+        """``weights_c`` from weights_array(); ``kv_layers``: [L] tensors (device or pinned host),
+        per-layer K/V [B][T|N][2][d], or with ``inputs`` the cached block inputs [B][N][d]
+        (Y caching); ``slots``: device buffers the pinned layers stream through."""
         L = len(kv_layers)
         ptrs = (C.c_void_p * L)(*[_ptr(t) for t in kv_layers])
         sl = (C.c_void_p * max(1, len(slots)))(*[_ptr(t) for t in slots])
-        src = KVSource(MS_KV_HOST_PINNED if pinned else MS_KV_DEVICE, C.cast(ptrs, C.POINTER(C.c_void_p)),
+        kind = (MS_Y_HOST_PINNED if pinned else MS_Y_DEVICE) if inputs else \
+               (MS_KV_HOST_PINNED if pinned else MS_KV_DEVICE)
+        src = KVSource(kind, C.cast(ptrs, C.POINTER(C.c_void_p)),
                        len(slots) if pinned else 0, C.cast(sl, C.POINTER(C.c_void_p)))
         cs = _stream(stream)
         ps = _stream(copy_stream) if copy_stream is not None else cs

@@ -81,8 +81,12 @@ def new_step(shape, mask_np, stream=None):
 
 
 def run_stack(shape, mask, x, kv_cache, y_cache, weights, *, pinned=False, serialize=False,
-              aliased=False, poison_cache=False, n_slots=2, dense_prefix=0):
-    """One step through mask_stack_forward; returns (y, working kv per layer or None, step)."""
+              aliased=False, poison_cache=False, n_slots=2, dense_prefix=0, inputs=False):
+    """One step through mask_stack_forward; returns (y, working kv per layer or None, step).
+    With ``inputs`` the cache is Y caching's per-layer block inputs ``[L][B][N][d]``."""
+    if inputs:
+        return _run_stack_y(shape, mask, x, kv_cache, y_cache, weights, pinned=pinned, serialize=serialize,
+                            n_slots=n_slots, dense_prefix=dense_prefix)
     dw = dev_weights(weights, shape)
     wc = MS.weights_array(dw)
     d_x = to_dev(x, shape)
@@ -116,3 +120,29 @@ def run_stack(shape, mask, x, kv_cache, y_cache, weights, *, pinned=False, seria
     torch.cuda.synchronize()
     kv_out = None if pinned else [to_np(t) for t in kv_layers]
     return to_np(y), kv_out, step
+
+
+def _run_stack_y(shape, mask, x, yin, y_cache, weights, *, pinned, serialize, n_slots, dense_prefix):
+    dw = dev_weights(weights, shape)
+    wc = MS.weights_array(dw)
+    d_x = to_dev(x, shape)
+    d_yc = to_dev(y_cache, shape) if y_cache is not None else None
+    step = new_step(shape, mask)
+    L = shape.n_layers
+    layers = []
+    for l in range(L):
+        t = torch.as_tensor(np.ascontiguousarray(yin[l], np.float32)).to(tdtype(shape))
+        layers.append(t.pin_memory() if pinned else t.to(DEV))
+    slots = ()
+    if pinned:
+        slots = [torch.full((shape.batch, shape.n_image, shape.d_model), float("nan"), dtype=tdtype(shape),
+                            device=DEV) for _ in range(n_slots)]
+    if dense_prefix:
+        step.set_dense_prefix(dense_prefix)
+    y = torch.empty((shape.batch, shape.n_tokens, shape.d_model), dtype=tdtype(shape), device=DEV)
+    cs = torch.cuda.current_stream()
+    copy = cs if serialize else torch.cuda.Stream()
+    step.stack_forward(wc, d_x, d_yc, layers, y, pinned=pinned, slots=slots, stream=cs, copy_stream=copy,
+                       inputs=True)
+    torch.cuda.synchronize()
+    return to_np(y), None, step

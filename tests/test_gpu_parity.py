@@ -365,3 +365,65 @@ def test_dense_prefix_own_cache_reproduces_dense():
     mask = np.stack([W.ellipse_mask(16, 16, 0.25, W.rng(7, 3, 9))])
     y, _, _ = G.run_stack(shape, mask, xt, kv_dense, y_dense, ws, pinned=True, n_slots=4, dense_prefix=2)
     G.assert_close(y, y_dense, "bf16", "own cache with a dense prefix")
+
+
+# ------------------------------------------------------------------ Y caching (Sec. 3.1, Fig. 5 bottom)
+
+Y_SHAPE = W.ModelShape("ycache", 4, 256, 2, 4, 16, 16, dtype="bf16", batch=2)
+Y_DUAL = W.ModelShape("ycache_dual", 3, 256, 2, 4, 8, 16, n_text=16, dual_stream=True, dtype="bf16", batch=2)
+
+
+def _y_inputs(shape, cfg):
+    ws = W.stack_weights(shape, cfg, random_ln=True, std=0.03)
+    xt = W.template_hidden(shape, cfg)
+    yin = oracle.dense_inputs(xt, ws, shape)          # the template's cached block inputs
+    yc, _ = oracle.dense_stack(xt, ws, shape)
+    return ws, xt, yin, yc
+
+
+@pytest.mark.parametrize("shape", [Y_SHAPE, Y_DUAL], ids=lambda s: s.name)
+def test_y_cache_matches_oracle_resident_and_streamed(shape):
+    ws, xt, yin, yc = _y_inputs(shape, 60)
+    mask = np.stack([W.ellipse_mask(shape.grid_h, shape.grid_w, r, W.rng(3, 6, b)) for b, r in
+                     enumerate((0.3, 0.1))])
+    x = W.edited_hidden(shape, 60, xt, mask)
+    ref = oracle.masked_stack_y(x, mask, yin, yc, ws, shape)
+    y_res, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True)
+    G.assert_close(y_res, ref, "bf16", f"{shape.name} Y cache resident")
+    for serialize in (False, True):
+        y_pin, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True, pinned=True, serialize=serialize)
+        np.testing.assert_array_equal(y_pin, y_res)
+    # unmasked rows of the output are the cached final state, bit for bit
+    yc_b = G.to_np(G.to_dev(yc, shape))
+    for b in range(shape.batch):
+        keep = np.concatenate([np.zeros(shape.n_text, bool), mask[b] == 0])
+        np.testing.assert_array_equal(y_res[b, keep], yc_b[b, keep])
+
+
+def test_y_cache_reads_no_recomputed_row_and_no_prefix_cache():
+    shape = Y_SHAPE
+    ws, xt, yin, yc = _y_inputs(shape, 61)
+    mask = _random_mask(shape, 0.25, 12)
+    x = W.edited_hidden(shape, 61, xt, mask)
+    for k in (0, 2):
+        ref, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True, dense_prefix=k)
+        poisoned = yin.copy()
+        poisoned[:k] = np.nan
+        for b in range(shape.batch):
+            poisoned[:, b, mask[b] != 0] = np.nan
+        y, _, _ = G.run_stack(shape, mask, x, poisoned, yc, ws, inputs=True, dense_prefix=k, pinned=True)
+        np.testing.assert_array_equal(y, ref)
+        G.assert_close(ref, oracle.masked_stack_y(x, mask, yin, yc, ws, shape, dense_prefix=k), "bf16",
+                       f"Y cache, dense prefix {k}")
+
+
+def test_y_cache_own_cache_is_dense_and_all_masked_reads_nothing():
+    shape = Y_DUAL
+    ws, xt, yin, yc = _y_inputs(shape, 62)
+    mask = _random_mask(shape, 0.3, 13)
+    y_dense = yc                                         # own cache: the current input is the template
+    y, _, _ = G.run_stack(shape, mask, xt, yin, yc, ws, inputs=True)
+    G.assert_close(y, y_dense, "bf16", "Y own cache vs dense")
+    ones = np.ones_like(mask)
+    y1, _, _ = G.run_stack(shape, ones, xt, np.full_like(yin, np.nan), None, ws, inputs=True)
+    G.assert_close(y1, y_dense, "bf16", "all masked, Y cache never read")
