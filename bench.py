@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--masks", type=int, default=8, help="distinct seeded mask sets cycled over the steps")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cache", default="kv", choices=("kv", "y"),
+                   help="kv: per-layer K/V cache (Fig. 7); y: per-layer cached block inputs (Fig. 5 bottom)")
     p.add_argument("--no-profile-pass", action="store_true")
     p.add_argument("--prefix", default="auto",
                    help="dense-prefix blocks for streamed caches: 'auto' (Alg. 1 planner on measured "
@@ -65,7 +67,7 @@ def parse():
 # ----------------------------------------------------------------------------- inputs
 
 
-def make_inputs(key, shape, n_masks, torch, W):
+def make_inputs(key, shape, n_masks, torch, W, cache="kv"):
     cfg = W.CONFIG_IDS[key]
     dev = "cuda:0"
     tdt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
@@ -94,7 +96,7 @@ def make_inputs(key, shape, n_masks, torch, W):
 
         for _ in range(shape.n_layers):
             weights.append((one(), one()) if shape.dual_stream else one())
-    masks, xs, ratios = [], [], []
+    masks, xs, ratios, unmasked = [], [], [], []
     xt = W.template_hidden(shape, cfg)
     for i in range(n_masks):
         if key == "c3":
@@ -103,15 +105,19 @@ def make_inputs(key, shape, n_masks, torch, W):
             m = W.workload_mask(key, shape, mask_id=i)
         masks.append(torch.as_tensor(m).to(dev))
         ratios.append(float(m.mean()))
+        unmasked.append(int((np.asarray(m) == 0).sum()))
         xs.append(torch.as_tensor(W.edited_hidden(shape, cfg, xt, m)).to(dev).to(tdt))
     g = torch.Generator(device=dev)
     g.manual_seed(2000 + cfg)
     B, T, N, d = shape.batch, shape.n_tokens, shape.n_image, shape.d_model
     pinned = key in ("c3", "c5")
     kv_layers = []
+    # K/V caching: per-layer K/V ([B][T][2][d] resident, [B][N][2][d] image rows in pinned host
+    # memory); Y caching: per-layer block inputs of the image tokens, [B][N][d], hidden-state scale
+    row_shape = (B, N, d) if cache == "y" else ((B, N, 2, d) if pinned else (B, T, 2, d))
+    scale = 1.0 if cache == "y" else 0.5
     for _ in range(shape.n_layers):
-        rows = N if pinned else T
-        t = (torch.randn((B, rows, 2, d), generator=g, device=dev) * 0.5).to(tdt)
+        t = (torch.randn(row_shape, generator=g, device=dev) * scale).to(tdt)
         if pinned:
             h = torch.empty(t.shape, dtype=tdt, pin_memory=True)
             h.copy_(t)
@@ -120,9 +126,10 @@ def make_inputs(key, shape, n_masks, torch, W):
         else:
             kv_layers.append(t)
     # one device slot per layer: every cached layer's load can start at once
-    slots = [torch.empty((B, T, 2, d), dtype=tdt, device=dev) for _ in range(shape.n_layers)] if pinned else []
+    slot_shape = (B, N, d) if cache == "y" else (B, T, 2, d)
+    slots = [torch.empty(slot_shape, dtype=tdt, device=dev) for _ in range(shape.n_layers)] if pinned else []
     ycache = torch.randn((B, T, d), generator=g, device=dev).to(tdt)
-    return weights, masks, xs, ratios, kv_layers, slots, ycache, pinned
+    return weights, masks, xs, ratios, kv_layers, slots, ycache, pinned, unmasked
 
 
 # ----------------------------------------------------------------------------- measured HBM traffic
@@ -237,7 +244,9 @@ def main():
     shape = W.CONFIGS[key]
     torch.cuda.set_device(0)
     t0 = time.perf_counter()
-    weights, masks, xs, ratios, kv_layers, slots, ycache, pinned = make_inputs(key, shape, args.masks, torch, W)
+    weights, masks, xs, ratios, kv_layers, slots, ycache, pinned, unmasked = make_inputs(
+        key, shape, args.masks, torch, W, args.cache)
+    yc_mode = args.cache == "y"
     log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f} s; ratios {np.round(ratios, 3).tolist()}")
     wc = MS.weights_array(weights)
     desc = MS.model_desc(shape)
@@ -254,7 +263,7 @@ def main():
         if prefix[i]:
             st.set_dense_prefix(prefix[i], stream)
         st.stack_forward(wc, xs[i], ycache, kv_layers, y, pinned=pinned, slots=slots, stream=stream,
-                         copy_stream=copy_stream)
+                         copy_stream=copy_stream, inputs=yc_mode)
         m = st.info().rows
         st.close()
         return m
@@ -276,7 +285,8 @@ def main():
         L = shape.n_layers
         for i in range(args.masks):
             st = MS.MaskStep(desc, shape.batch, masks[i], ws, stream)
-            run = lambda: st.stack_forward(wc, xs[i], ycache, slots, y, pinned=False, stream=stream)
+            run = lambda: st.stack_forward(wc, xs[i], ycache, slots, y, pinned=False, stream=stream,
+                                           inputs=yc_mode)
             run()
             cached_ms = min(timed_once(run) for _ in range(2)) / L
             st.set_dense_prefix(L, stream)
@@ -285,7 +295,7 @@ def main():
             st.set_dense_prefix(0, stream)
             MS.profiler_start(("copy",))
             st.stack_forward(wc, xs[i], ycache, kv_layers, y, pinned=True, slots=slots, stream=stream,
-                             copy_stream=copy_stream)
+                             copy_stream=copy_stream, inputs=yc_mode)
             torch.cuda.synchronize()
             prof = MS.profiler_stop()
             load_ms = prof["copy"][0] / max(1, prof["copy"][1]) if "copy" in prof else 0.0
@@ -308,24 +318,30 @@ def main():
         k = prefix[i]
         return k * shape.batch * shape.n_tokens + (shape.n_layers - k) * Ms[i]
 
+    def unmasked_layers(i):
+        # Y caching: unmasked rows whose K/V each cached block recomputes
+        return (shape.n_layers - prefix[i]) * unmasked[i] if yc_mode else 0
+
     def timed(k, per_step=False):
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(k + 1)]
         tot_m = 0
         tot_rl = 0
+        tot_ul = 0
         torch.cuda.synchronize()
         w0 = time.perf_counter()
         evs[0].record(stream)
         for s in range(k):
             tot_m += one_step(s % args.masks)
             tot_rl += row_layers(s % args.masks)
+            tot_ul += unmasked_layers(s % args.masks)
             evs[s + 1].record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - w0
         ms = evs[0].elapsed_time(evs[k])
         steps = [evs[s].elapsed_time(evs[s + 1]) for s in range(k)] if per_step else None
-        return ms, wall, tot_m, steps, tot_rl
+        return ms, wall, tot_m, steps, tot_rl, tot_ul
 
-    ms_total, wall, tot_m, step_ms, _ = timed(args.steps, per_step=True)
+    ms_total, wall, tot_m, step_ms, _, _ = timed(args.steps, per_step=True)
     log(f"[bench] timed {args.steps} steps: {ms_total:.3f} ms (events), {wall * 1e3:.3f} ms (wall)")
     ms_step = ms_total / args.steps
     value = tot_m / (ms_total / 1e3)
@@ -339,7 +355,7 @@ def main():
     kernels, roof = {}, None
     if not args.no_profile_pass:
         MS.profiler_start(MS.KERNEL_CLASSES, capacity=1 << 16)
-        ms_prof, _, tot_m_prof, _, tot_rl_prof = timed(args.steps)
+        ms_prof, _, tot_m_prof, _, tot_rl_prof, u_sum = timed(args.steps)
         prof = MS.profiler_stop()
         log(f"[bench] profiled pass: {ms_prof / args.steps:.4f} ms/step; {prof}")
         d, T, L, f = shape.d_model, shape.n_tokens, shape.n_layers, shape.mlp_mult * shape.d_model
@@ -348,11 +364,11 @@ def main():
         m_sum = tot_rl_prof                         # computed rows summed over the blocks of all steps
         work = {
             "attention": ("mfma", 4.0 * m_sum * T * d),
-            "gemm_qkv": ("mfma", 2.0 * m_sum * d * 3 * d),
+            "gemm_qkv": ("mfma", 2.0 * m_sum * d * 3 * d + 2.0 * u_sum * d * 2 * d),
             "gemm_out": ("mfma", 2.0 * m_sum * d * d),
             "gemm_up": ("mfma", 2.0 * m_sum * d * f),
             "gemm_down": ("mfma", 2.0 * m_sum * f * d),
-            "layernorm": ("hbm", 2.0 * 2 * m_sum * d * e),
+            "layernorm": ("hbm", 2.0 * 2 * m_sum * d * e + 2.0 * u_sum * d * e),
             "gather": ("hbm", 2.0 * tot_m_prof * d * e),
         }
         prof.pop("_dropped", None)
@@ -411,7 +427,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{shape.name}: {DESCR[key]}", "global_batch": shape.batch,
                    "seq_len": shape.n_tokens, "parallelism": "none (1 GPU)",
-                   "masks": args.masks, "mean_masked_rows": round(float(np.mean(Ms)), 1)},
+                   "masks": args.masks, "mean_masked_rows": round(float(np.mean(Ms)), 1),
+                   "cache": "per-layer K/V (Fig. 7)" if args.cache == "kv" else
+                            "per-layer block inputs, K/V recomputed (Fig. 5 bottom)"},
         "per_mask": {"columns": ["ratio", "masked_rows", "median_ms", "dense_prefix"], "rows": per_ratio},
         "prefix_plan": plan_info or None,
         "roofline": roof,
