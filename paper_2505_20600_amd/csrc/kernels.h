@@ -82,10 +82,11 @@ struct AttnDesc {
     int nseg, T, d, hd, n_qtiles, n_heads;
     float scale_log2;     // log2(e) / sqrt(hd)
     // bf16 path: 128-row query tiles, keys split over `nsplit` workgroups of
-    // `tiles_per_split` 64-key tiles; partials (unnormalised O, running max
-    // and sum) go to part_o [nsplit][M][d] / part_ml [nsplit][M][n_heads].
+    // `tiles_per_split` 64-key tiles; partials (O normalised by its own key
+    // range's sum, in bf16, and that range's running max and sum) go to
+    // part_o [nsplit][M][d] / part_ml [nsplit][M][n_heads].
     int M, n_qtiles_fast, nsplit, tiles_per_split;
-    float* part_o;
+    uint16_t* part_o;     // bf16
     float* part_ml;
 };
 

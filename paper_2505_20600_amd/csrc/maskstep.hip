@@ -122,7 +122,7 @@ Layout make_layout(const ms_model_desc& d, int32_t B) {
     L.h = take(BT * dm * e);
     L.u = take(BT * f * e);
     L.kv_dense = take(BT * 2 * dm * e);
-    L.part_o = take(attn_part_rows(d, B) * dm * 4);
+    L.part_o = take(attn_part_rows(d, B) * dm * 2);   // bf16
     L.part_ml = take(attn_part_rows(d, B) * (size_t)d.n_heads * 2 * 4);
     L.gemm_part = take(ms::kGemmPartFloats * 4);
     L.total = off;
@@ -377,7 +377,7 @@ ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w
     ad.n_qtiles_fast = pk.n_qtiles_fast;
     ad.nsplit = pk.attn_nsplit;
     ad.tiles_per_split = pk.attn_tps;
-    ad.part_o = static_cast<float*>(s->buf(s->lay.part_o));
+    ad.part_o = static_cast<uint16_t*>(s->buf(s->lay.part_o));
     ad.part_ml = static_cast<float*>(s->buf(s->lay.part_ml));
     {
         ProfScope p(MS_K_ATTENTION, st);

@@ -63,9 +63,20 @@ int copy_grid(long total) {
 }
 
 // LayerNorm: one wave per row, the row held in registers (two-pass mean and
-// variance in float32), 16-byte vectors.
+// variance in float32), 16-byte vectors. The affine parameters are loaded
+// with the row, so their latency overlaps the row's.
 constexpr int kLnWaves = 4;
 constexpr int kLnMaxVecPerLane = 8;
+
+template <typename T>
+__device__ __forceinline__ float vec_elt(const vec16& v, int e) {
+    if constexpr (sizeof(T) == 2) {
+        const uint32_t w = v.w[e >> 1];
+        return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    } else {
+        return __uint_as_float(v.w[e]);
+    }
+}
 
 template <typename T>
 __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
@@ -80,6 +91,16 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
     const T* bet = row < m_split ? b1 : b0;
     const int nvec = d / V;
     const T* xr = x + (long)(idx ? idx[row] : row) * d;
+    vec16 xv[kLnMaxVecPerLane], gv[kLnMaxVecPerLane], bv[kLnMaxVecPerLane];
+#pragma unroll
+    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+        const int c = lane + i * kWave;
+        if (c < nvec) {
+            xv[i] = ld16(xr + c * V);
+            gv[i] = ld16(gam + c * V);
+            bv[i] = ld16(bet + c * V);
+        }
+    }
     float v[kLnMaxVecPerLane][V];
     float s = 0.f;
 #pragma unroll
@@ -87,9 +108,10 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
-            for (int e = 0; e < V; e += 4) load4<T>(xr + c * V + e, &v[i][e]);
-#pragma unroll
-            for (int e = 0; e < V; ++e) s += v[i][e];
+            for (int e = 0; e < V; ++e) {
+                v[i][e] = vec_elt<T>(xv[i], e);
+                s += v[i][e];
+            }
         }
     }
     const float mean = wave_sum(s) / d;
@@ -113,11 +135,10 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
         if (c < nvec) {
 #pragma unroll
             for (int e = 0; e < V; e += 4) {
-                float gg[4], bb[4], o[4];
-                load4<T>(gam + c * V + e, gg);
-                load4<T>(bet + c * V + e, bb);
+                float o[4];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) o[k] = (v[i][e + k] - mean) * rstd * gg[k] + bb[k];
+                for (int k = 0; k < 4; ++k)
+                    o[k] = (v[i][e + k] - mean) * rstd * vec_elt<T>(gv[i], e + k) + vec_elt<T>(bv[i], e + k);
                 store4<T>(yr + c * V + e, o);
             }
         }

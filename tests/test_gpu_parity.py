@@ -301,6 +301,28 @@ def test_full_size_stack_sampled_request(cfg_key, ratio):
     np.testing.assert_array_equal(y[0, keep], yc[0, keep])
 
 
+@pytest.mark.parametrize("cfg_key,n_layers,pinned", [("c4", 28, False), ("c5", 2, True)])
+def test_full_size_batched_stack_sampled_request(cfg_key, n_layers, pinned):
+    """The batched workloads at full width, token count and batch, with the workload's own
+    mask draw (per-request ratios; c5 with its text rows and the streamed host cache).
+
+    Every request runs through the packed path; the request with the fewest recomputed
+    rows is checked against the oracle (requests attend only within themselves). c4 runs
+    all 28 layers; c5 two of its 19 (full-width layers), so that the oracle and the input
+    generation stay within seconds.
+    """
+    shape = W.CONFIGS[cfg_key].replace(n_layers=n_layers)
+    ws, xt, kv, yc = _inputs(shape, W.CONFIG_IDS[cfg_key], random_ln=False)
+    mask = W.workload_mask(cfg_key, shape)
+    x = W.edited_hidden(shape, W.CONFIG_IDS[cfg_key], xt, mask)
+    y, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=pinned)
+    b = int(np.argmin(mask.sum(1)))
+    toks, xm_ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, b=b)
+    G.assert_close(y[b, toks], xm_ref, "bf16", f"{cfg_key} full size, request {b}")
+    keep = np.setdiff1d(np.arange(shape.n_tokens), toks)
+    np.testing.assert_array_equal(y[b, keep], yc[b, keep])
+
+
 # ------------------------------------------------------------------ attention key-range split
 
 @pytest.mark.parametrize("hd_shape", [
