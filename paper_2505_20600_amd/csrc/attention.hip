@@ -556,13 +556,19 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
                 }
             }
         } else {
-            float* po = a.part_o + ((long)split * a.M + qrow) * d + head * HD;
+            // this key range's output, normalised by its own sum: bf16 holds
+            // it to the output's precision at half the bytes of float32
+            const float inv_l = 1.0f / l;
+            bf16_t* po = a.part_o + ((long)split * a.M + qrow) * d + head * HD;
 #pragma unroll
             for (int h = 0; h < C::NHS; ++h) {
                 const int cidx = h * 16 + grp * 4;
-                if (cidx < HD)
-                    *reinterpret_cast<float4*>(po + cidx) =
-                        make_float4(oacc[qb][h][0], oacc[qb][h][1], oacc[qb][h][2], oacc[qb][h][3]);
+                if (cidx < HD) {
+                    float v[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[r] = oacc[qb][h][r] * inv_l;
+                    store4<bf16_t>(po + cidx, v);
+                }
             }
             if (grp == 0)
                 *reinterpret_cast<float2*>(a.part_ml + 2 * (((long)split * a.M + qrow) * a.n_heads + head)) =
@@ -571,7 +577,10 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
     }
 }
 
-// Combine of the key-range partials (log-sum-exp weights), fixed split order.
+// Combine of the key-range partials, fixed split order: range s, with running
+// max m_s, sum l_s and normalised output O_s, has weight l_s 2^((m_s - m) c)
+// (m the largest m_s, c the log2-domain scale), and the output is the
+// weighted mean of the O_s.
 __global__ __launch_bounds__(256) void attention_combine_kernel(AttnDesc a) {
     const long n4 = (long)a.M * a.d / 4;
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -585,10 +594,12 @@ __global__ __launch_bounds__(256) void attention_combine_kernel(AttnDesc a) {
     float L = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < a.nsplit; ++s) {
         const float* ml = a.part_ml + 2 * (((long)s * a.M + m) * a.n_heads + head);
-        const float w = fast_exp2((ml[0] - gmax) * a.scale_log2);
-        L += w * ml[1];
-        const float4 po = *reinterpret_cast<const float4*>(a.part_o + ((long)s * a.M + m) * a.d + col);
-        acc[0] += w * po.x; acc[1] += w * po.y; acc[2] += w * po.z; acc[3] += w * po.w;
+        const float w = fast_exp2((ml[0] - gmax) * a.scale_log2) * ml[1];
+        L += w;
+        float po[4];
+        load4<bf16_t>(a.part_o + ((long)s * a.M + m) * a.d + col, po);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] += w * po[r];
     }
     const float inv = 1.0f / L;
 #pragma unroll
