@@ -63,6 +63,29 @@ __device__ __forceinline__ void epilogue_store(const GemmDesc& g, int m, int n, 
     }
 }
 
+// Tile of logical block id `lb` in groups of up to `gm` m-tiles: ids run over
+// the m-tiles of a group first, then over n, then to the next group, so that
+// the 32 consecutive ids one XCD runs at once cover a 4 x 8 block of tiles
+// (12 operand slices per K step in its L2) instead of a 16 x 2 strip (18).
+// Measured on MI355X against m-fastest order: -15% time on 6144x3072x3072,
+// -11% on 8192x1152x4608, -2..-4% on the other large shapes, equal on small M.
+constexpr int kGroupM = 4;
+
+struct TileIdx {
+    int kz, m0, n0;
+};
+
+__device__ __forceinline__ TileIdx tile_of(int lb, int tiles_m, int tiles_n, int bm, int bn, int gm) {
+    const int per_k = tiles_m * tiles_n;
+    const int kz = lb / per_k;
+    const int r = lb - kz * per_k;
+    const int group = r / (gm * tiles_n);
+    const int gm0 = group * gm;
+    const int gsize = min(gm, tiles_m - gm0);
+    const int within = r - group * gm * tiles_n;
+    return TileIdx{kz, (gm0 + within % gsize) * bm, (within / gsize) * bn};
+}
+
 template <typename T, int BM, int BN, int EPI>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
     using E = Elt<T>;
@@ -84,13 +107,12 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
     const int wave = tid / kWave;
     const int wm = wave & 1, wn = wave >> 1;
     const int M = g.M, N = g.N, K = g.K;
-    // 1-D launch, logical order (k split, n tile, m tile) with m fastest, placed
-    // so that each XCD covers a contiguous range of weight (n) tiles
+    // 1-D launch: each XCD takes a contiguous range of logical ids (k split
+    // slowest), mapped to tiles in grouped order
     const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
     const int lb = xcd_logical_block(blockIdx.x, tiles_m * tiles_n * g.ksplit);
-    const int kz = lb / (tiles_m * tiles_n);
-    const int n0 = ((lb / tiles_m) % tiles_n) * BN;
-    const int m0 = (lb % tiles_m) * BM;
+    const TileIdx ti = tile_of(lb, tiles_m, tiles_n, BM, BN, g.group_m);
+    const int kz = ti.kz, m0 = ti.m0, n0 = ti.n0;
     const int kbeg = kz * g.kchunk;
     const int kend = min(K, kbeg + g.kchunk);
     const T* __restrict__ A = static_cast<const T*>(g.A);
@@ -209,9 +231,8 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
     const int M = g.M, N = g.N, K = g.K;
     const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
     const int lb = xcd_logical_block(blockIdx.x, tiles_m * tiles_n * g.ksplit);
-    const int kz = lb / (tiles_m * tiles_n);
-    const int n0 = ((lb / tiles_m) % tiles_n) * BN;
-    const int m0 = (lb % tiles_m) * BM;
+    const TileIdx ti = tile_of(lb, tiles_m, tiles_n, BM, BN, g.group_m);
+    const int kz = ti.kz, m0 = ti.m0, n0 = ti.n0;
     const int kbeg = kz * g.kchunk;
     const int kend = min(K, kbeg + g.kchunk);
     const int nk = (kend - kbeg) / BK;
@@ -439,6 +460,11 @@ hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
     const int per = (steps + g.ksplit - 1) / g.ksplit;
     g.kchunk = per * bk;
     g.ksplit = (steps + per - 1) / per;
+    static const int group_m = [] {   // tuning knob MS_GEMM_GROUP (tiles_m or more: m fastest)
+        const char* v = std::getenv("MS_GEMM_GROUP");
+        return v ? std::max(1, std::atoi(v)) : kGroupM;
+    }();
+    g.group_m = group_m;
     if (dtype != kBF16) return launch_tile<float, 64, 64>(g, s);
     // main loop: direct-to-LDS (default) or the register-staged double buffer
     // (tuning knob MS_GEMM_PIPE=staged); MS_GEMM_STAGES overrides the stage count

@@ -54,6 +54,7 @@ struct GemmDesc {
     int stages;         // LDS stages of the bf16 main loop (0: the tile's default)
     int ksplit;         // K-range splits (1: epilogue fused in the GEMM)
     int kchunk;         // set by launch_gemm
+    int group_m;        // set by launch_gemm: m-tiles per group of the tile order
     float* part;        // ksplit > 1: [ksplit][M][N] float32 partials
 };
 
