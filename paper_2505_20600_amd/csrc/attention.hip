@@ -271,14 +271,6 @@ __device__ __forceinline__ int dma_swz(int r) {
     else return 0;
 }
 
-// One 16-byte-per-lane buffer load into LDS at `lds` + 16 * lane, issued as an
-// opaque instruction (the caller orders it with wait_vmcnt + barrier_only).
-__device__ __forceinline__ void dma_buf16(u32x4_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc),
-                    "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
-}
-
 typedef const __attribute__((address_space(3))) uint8_t* lds_cptr;
 
 __device__ __forceinline__ bf16x4_t ld_tr16(lds_cptr p) {
@@ -324,14 +316,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
     if (tid == S) *reinterpret_cast<uint2*>(smem + S * C::STAGEB) = make_uint2(0x3f803f80u, 0x3f803f80u);
 
     // buffer resource over request b's K/V block [T][2][d]
-    u32x4_t rsrc;
-    {
-        const uint64_t base = reinterpret_cast<uint64_t>(static_cast<const bf16_t*>(a.kv) + (long)b * T_ * 2 * d);
-        rsrc[0] = (uint32_t)base;
-        rsrc[1] = (uint32_t)(base >> 32) & 0xffffu;
-        rsrc[2] = (uint32_t)T_ * 4u * (uint32_t)d;
-        rsrc[3] = 0x00020000u;
-    }
+    const u32x4_t rsrc = raw_rsrc(static_cast<const bf16_t*>(a.kv) + (long)b * T_ * 2 * d, (uint32_t)T_ * 4u * (uint32_t)d);
     // per copy of this wave: fixed per-lane global byte offset and LDS destination in a stage
     uint32_t voff[C::IPW_MAX], ldst[C::IPW_MAX];
 #pragma unroll

@@ -125,6 +125,27 @@ __device__ __forceinline__ void dma_lds16(const void* g, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                  :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(g) : "memory", "m0");
 }
+// Buffer resource (four SGPRs) over `bytes` bytes from `base`, raw addressing:
+// loads at or past `bytes` (per-lane offset plus scalar offset) return zeros.
+__device__ __forceinline__ u32x4_t raw_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    u32x4_t r;
+    r[0] = (uint32_t)b;
+    r[1] = (uint32_t)(b >> 32) & 0xffffu;
+    r[2] = bytes;
+    r[3] = 0x00020000u;
+    return r;
+}
+
+// One 16-byte-per-lane buffer load into LDS at `lds` + 16 * lane (gfx950
+// buffer_load_dwordx4 ... lds), issued as an opaque instruction like
+// dma_lds16; `soff` and `lds` are wave-uniform.
+__device__ __forceinline__ void dma_buf16(u32x4_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc),
+                    "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)(p)));
 }

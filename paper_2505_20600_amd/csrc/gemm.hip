@@ -381,7 +381,7 @@ hipError_t launch_reduce(const GemmDesc& g, hipStream_t s) {
 // Tile and stage choice from a measured cost table. Each entry gives the
 // time (us) of one 64-deep K step of a whole grid in which every CU holds n
 // = 1..8 workgroups of that tile and stage count (MI355X, bf16, direct-to-LDS
-// main loop, K = 2048; n = 7 interpolated). A launch costs about steps x
+// main loop, grouped tile order, K = 2048; n = 7 interpolated). A launch costs about steps x
 // time(n_busiest) with n_busiest = ceil(groups / 256); past n = 8 the last
 // measured slope extends the table. More stages pay off when few workgroups
 // share a CU (deeper prefetch), fewer when many do (LDS occupancy). Split-K
@@ -392,21 +392,21 @@ struct TileCost {
     double us[8];
 };
 constexpr TileCost kCost[] = {
-    {256, 256, 2, {2.089, 4.200, 6.182, 8.226, 10.098, 12.692, 15.092, 17.493}},
-    {256, 128, 2, {1.374, 3.288, 4.830, 6.339, 7.887, 9.361, 10.956, 12.551}},
-    {256, 128, 3, {1.407, 3.010, 4.494, 6.012, 7.518, 9.015, 10.509, 12.004}},
-    {128, 128, 2, {0.973, 1.296, 2.178, 2.738, 3.666, 4.057, 4.707, 5.356}},
-    {128, 128, 3, {0.890, 1.692, 2.503, 3.253, 3.979, 4.765, 5.521, 6.277}},
-    {128, 128, 4, {0.837, 1.682, 2.468, 3.274, 4.051, 4.842, 5.617, 6.393}},
-    {128, 64, 2, {0.742, 0.987, 1.294, 2.259, 2.981, 3.553, 4.182, 4.811}},
-    {128, 64, 3, {0.655, 1.098, 1.930, 2.447, 3.079, 3.592, 4.155, 4.717}},
-    {128, 64, 4, {0.625, 1.414, 2.081, 2.694, 3.291, 3.865, 4.434, 5.003}},
-    {64, 128, 2, {0.708, 0.845, 1.070, 1.661, 1.748, 2.135, 2.515, 2.895}},
-    {64, 128, 3, {0.609, 0.804, 1.282, 1.576, 2.074, 2.343, 2.737, 3.131}},
-    {64, 128, 4, {0.593, 1.113, 1.632, 2.147, 2.693, 3.156, 3.659, 4.162}},
-    {64, 64, 2, {0.586, 0.654, 0.736, 0.938, 1.527, 1.747, 2.089, 2.432}},
-    {64, 64, 3, {0.463, 0.557, 0.818, 1.309, 1.543, 1.854, 2.143, 2.431}},
-    {64, 64, 4, {0.424, 0.566, 0.928, 1.313, 1.654, 1.953, 2.224, 2.494}},
+    {256, 256, 2, {2.053, 3.925, 5.809, 7.690, 9.645, 12.229, 14.984, 17.740}},
+    {256, 128, 2, {1.436, 2.538, 3.676, 4.847, 6.029, 7.196, 8.445, 9.694}},
+    {256, 128, 3, {1.418, 2.668, 3.898, 5.195, 6.433, 7.714, 9.015, 10.317}},
+    {128, 128, 2, {0.942, 1.181, 1.820, 2.194, 2.777, 3.200, 3.716, 4.233}},
+    {128, 128, 3, {0.910, 1.645, 2.386, 3.100, 3.816, 4.524, 5.279, 6.034}},
+    {128, 128, 4, {0.849, 1.601, 2.339, 3.053, 3.749, 4.497, 5.223, 5.948}},
+    {128, 64, 2, {0.611, 0.812, 1.093, 1.613, 1.698, 1.946, 2.243, 2.540}},
+    {128, 64, 3, {0.686, 0.833, 1.313, 1.482, 1.920, 2.162, 2.463, 2.764}},
+    {128, 64, 4, {0.650, 1.166, 1.668, 2.171, 2.670, 3.166, 3.631, 4.096}},
+    {64, 128, 2, {0.754, 0.840, 1.065, 1.581, 1.667, 1.966, 2.266, 2.566}},
+    {64, 128, 3, {0.670, 0.827, 1.288, 1.510, 1.936, 2.176, 2.503, 2.831}},
+    {64, 128, 4, {0.589, 1.122, 1.623, 2.133, 2.603, 3.076, 3.572, 4.068}},
+    {64, 64, 2, {0.422, 0.628, 0.708, 0.943, 1.325, 1.357, 1.520, 1.683}},
+    {64, 64, 3, {0.464, 0.562, 0.771, 1.087, 1.219, 1.483, 1.700, 1.917}},
+    {64, 64, 4, {0.440, 0.579, 0.872, 1.034, 1.358, 1.522, 1.758, 1.994}},
 };
 
 double step_us(const TileCost& c, long n) {
