@@ -19,4 +19,5 @@ from .stack import (  # noqa: F401
     rounder,
 )
 from .planner import best_dense_prefix, greedy_choice, pipeline_latency  # noqa: F401
+from .routing import CostModel, batch_latency, block_costs, calc_cost, fit_linear, route  # noqa: F401
 from .ycache import dense_inputs, kv_cache_of_inputs, kv_of_inputs, masked_stack_y  # noqa: F401
