@@ -61,6 +61,10 @@ def parse():
                         "per-block costs) or a fixed count")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device copy (HBM counter calibration) and exit")
+    p.add_argument("--fit", type=int, default=0, metavar="K",
+                   help="only fit the per-block cost models of Sec. 4.3 on K measured random batches of "
+                        "the workload (compute vs FLOPs, cache load vs bytes), run the routing simulation "
+                        "with them, print one JSON line and exit")
     return p.parse_args()
 
 
@@ -161,6 +165,124 @@ def measured_traffic(kernel: str):
     return None
 
 
+# ----------------------------------------------------------------------------- cost-model fit (Sec. 4.3)
+
+
+def fit_cost_models(key, shape, n_points, torch, MS, W):
+    """Measure per-block latencies of random batches and fit Comp(FLOPs) and Load(bytes).
+
+    Each point is one batch of 1..B requests with log-uniform mask ratios in [3%, 80%]
+    (blob masks): the per-block time of the cached blocks (resident K/V) and of blocks
+    over every token (a dense prefix of all layers) against their Table 1 FLOPs, and
+    the per-layer time of the pinned-host cache prefetch against its bytes. A stack of
+    min(L, 4) layers of the workload's shape is enough: every quantity is per block.
+    """
+    import math
+    from paper_2505_20600_amd import routing
+    L = min(shape.n_layers, 4)
+    fs = shape.replace(n_layers=L)
+    cfg = W.CONFIG_IDS[key]
+    dev = "cuda:0"
+    tdt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    elt = 2 if shape.dtype == "bf16" else 4
+    B, T, N, d = shape.batch, shape.n_tokens, shape.n_image, shape.d_model
+    g = torch.Generator(device=dev)
+    g.manual_seed(3000 + cfg)
+    weights, _, _, _, _, _, _, _, _ = make_inputs(key, fs, 1, torch, W)
+    wc = MS.weights_array(weights)
+    kv_dev = [(torch.randn((B, T, 2, d), generator=g, device=dev) * 0.5).to(tdt) for _ in range(L)]
+    kv_host = []
+    for _ in range(L):
+        h = torch.empty((B, N, 2, d), dtype=tdt, pin_memory=True)
+        h.copy_((torch.randn((B, N, 2, d), generator=g, device=dev) * 0.5).to(tdt))
+        kv_host.append(h)
+    slots = [torch.empty((B, T, 2, d), dtype=tdt, device=dev) for _ in range(L)]
+    x = torch.randn((B, T, d), generator=g, device=dev).to(tdt)
+    yc = torch.randn((B, T, d), generator=g, device=dev).to(tdt)
+    y = torch.empty_like(yc)
+    desc = MS.model_desc(fs)
+    ws = torch.empty(MS.mask_workspace_bytes(desc, B), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    copy_stream = torch.cuda.Stream()
+    unit = MS.CostModel(0.0, 1.0, 0.0, 1.0, 2.0 * d * elt)     # mask_batch_cost in GFLOP and MB
+    rng = np.random.default_rng(np.random.SeedSequence([cfg, 7, 0]))
+
+    def timed(fn, reps=3):
+        ts = []
+        for _ in range(reps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts[1:]))
+
+    comp_pts, load_pts = [], []
+    for i in range(n_points):
+        b = 1 + i % B
+        r = np.exp(rng.uniform(math.log(0.03), math.log(0.80), b))
+        m = np.stack([W.blob_mask(shape.grid_h, shape.grid_w, float(rr), W.rng(cfg, 7, 64 * i + j))
+                      for j, rr in enumerate(r)])
+        counts = [int(v) for v in m.sum(1)]
+        (mb, gf_c, gf_f), _, _ = MS.mask_batch_cost(desc, unit, counts)
+        st = MS.MaskStep(desc, b, torch.as_tensor(m).to(dev), ws, stream)
+        kvs = [t[:b] for t in kv_dev]
+        run = lambda: st.stack_forward(wc, x[:b], yc[:b], kvs, y[:b], stream=stream)
+        t_c = timed(run) / L
+        st.set_dense_prefix(L, stream)
+        t_f = timed(run) / L
+        st.set_dense_prefix(0, stream)
+        hs = [h[:b] for h in kv_host]
+        ss = [sl[:b] for sl in slots]
+        MS.profiler_start(("copy",))
+        for _ in range(3):
+            st.stack_forward(wc, x[:b], yc[:b], hs, y[:b], pinned=True, slots=ss, stream=stream,
+                             copy_stream=copy_stream)
+        torch.cuda.synchronize()
+        prof = MS.profiler_stop()
+        st.close()
+        comp_pts += [[round(gf_c, 4), round(t_c, 5)], [round(gf_f, 4), round(t_f, 5)]]
+        if "copy" in prof and prof["copy"][1] > 0 and mb > 0:
+            load_pts.append([round(mb, 3), round(prof["copy"][0] / prof["copy"][1], 5)])
+        log(f"[fit] batch {b} masked {counts}: cached {t_c:.4f} ms ({gf_c:.1f} GF), full {t_f:.4f} ms "
+            f"({gf_f:.1f} GF), load {load_pts[-1] if load_pts else None}")
+    def fit(pts):
+        xs, ys = [p[0] for p in pts], [p[1] for p in pts]
+        a, b, r2 = MS.mask_fit_linear(xs, ys)
+        if b < 0 or a < 0:
+            # a cost model has no negative part: a negative slope (latency flat in the amount,
+            # e.g. span-merged copies that move nearly every row) keeps the mean, a negative
+            # intercept the line through the origin
+            if b < 0:
+                a, b, r2 = float(np.mean(ys)), 0.0, 0.0
+            else:
+                b = float(np.dot(xs, ys) / np.dot(xs, xs))
+                a = 0.0
+                r2 = 1.0 - float(np.sum((np.asarray(ys) - b * np.asarray(xs)) ** 2) /
+                                 np.sum((np.asarray(ys) - np.mean(ys)) ** 2))
+        return a, b, r2
+
+    c0, c1, c_r2 = fit(comp_pts)
+    l0, l1, l_r2 = fit(load_pts)
+    # routing simulation with the fitted models (host-only): caches streamed from pinned host
+    # memory (the fitted load model) and HBM-resident (no loads)
+    import contextlib
+    import io
+    sims = {}
+    for name, load_args in (("streamed", [str(l0), str(l1)]), ("resident", ["0", "0"])):
+        buf = io.StringIO()
+        with contextlib.redirect_stdout(buf):
+            routing.main(["--workload", key, "--comp", str(c0), str(c1), "--load", *load_args, "--requests", "2000"])
+        sims[name] = json.loads(buf.getvalue())
+    return {
+        "comp": {"ms0": round(c0, 5), "ms_per_gflop": round(c1, 6), "r2": round(c_r2, 5), "points": comp_pts},
+        "load": {"ms0": round(l0, 5), "ms_per_mb": round(l1, 6), "r2": round(l_r2, 5), "points": load_pts},
+        "routing": sims,
+    }
+
+
 # ----------------------------------------------------------------------------- CPU oracle
 
 
@@ -243,6 +365,13 @@ def main():
     key = args.workload
     shape = W.CONFIGS[key]
     torch.cuda.set_device(0)
+    if args.fit:
+        t0 = time.perf_counter()
+        res = fit_cost_models(key, shape, args.fit, torch, MS, W)
+        print(json.dumps({"metric": "per-block cost models (Sec. 4.3): latency vs FLOPs and vs cached bytes",
+                          "workload": f"{shape.name}: {DESCR[key]}", "points": args.fit,
+                          "seconds": round(time.perf_counter() - t0, 1), **res}), flush=True)
+        return
     t0 = time.perf_counter()
     weights, masks, xs, ratios, kv_layers, slots, ycache, pinned, unmasked = make_inputs(
         key, shape, args.masks, torch, W, args.cache)

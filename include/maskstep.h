@@ -172,6 +172,53 @@ ms_status mask_step_set_dense_prefix(ms_step* step, int32_t k, void* stream);
 ms_status mask_plan_dense_prefix(int32_t n_layers, double load_ms, double cached_ms, double full_ms,
                                  int32_t* k_out, double* latency_ms_out);
 
+/* Worker-load estimate (Sec. 4.3): linear regression models, fitted offline,
+ * that map a batch's computation (FLOPs of Table 1 at the requests' mask
+ * ratios) and the bytes of cached activations a block loads to latency:
+ *   Comp(F) = comp_ms0 + comp_ms_per_gflop * F / 1e9    (one block)
+ *   Load(B) = load_ms0 + load_ms_per_mb * B / 1e6       (one block's cache)
+ * Zero work or zero bytes cost nothing (the intercepts apply only to issued
+ * work). cache_bytes_per_token is what one unmasked image token's cache holds
+ * per block: 2 * d_model * element size for K/V caching, d_model * element
+ * size for Y caching. All fields finite and >= 0. */
+typedef struct {
+    double comp_ms0, comp_ms_per_gflop;
+    double load_ms0, load_ms_per_mb;
+    double cache_bytes_per_token;
+} ms_cost_model;
+
+/* Least-squares line y ~ intercept + slope * x over n >= 2 points with some
+ * spread in x (the regression fit of Sec. 4.3), and its coefficient of
+ * determination 1 - SS_res / SS_tot (1 when y is constant and fitted
+ * exactly). x, y: host arrays of n doubles. r2_out may be NULL. Host-only. */
+ms_status mask_fit_linear(const double* x, const double* y, int32_t n, double* intercept_out,
+                          double* slope_out, double* r2_out);
+
+/* Per-block costs of a batch and Alg. 1 over them (Sec. 4.3 with Sec. 4.2):
+ * masked[b] = masked image tokens of request b (0..grid_h*grid_w; text rows,
+ * when the model has them, are always recomputed). costs_out[3] receives
+ * L = Load(sum of unmasked image tokens * cache_bytes_per_token),
+ * C_w = Comp(sum of the cached blocks' FLOPs) and C_wo = Comp(batch * FLOPs
+ * of a block over every token); *k_out and *latency_ms_out the dense prefix
+ * and latency of mask_plan_dense_prefix over them. batch = 0 gives zeros.
+ * Any output may be NULL. Host-only; desc is validated as for
+ * mask_step_init except max_batch. */
+ms_status mask_batch_cost(const ms_model_desc* desc, const ms_cost_model* model, const int32_t* masked,
+                          int32_t batch, double* costs_out, int32_t* k_out, double* latency_ms_out);
+
+/* Mask-aware request routing (Alg. 2): the cost of a worker is the
+ * pipeline latency of its running batch with the new request added
+ * (mask_batch_cost); the request goes to the candidate of least cost, the
+ * first one on ties; candidates are the workers whose running batch holds
+ * fewer than max_batch requests. running_masked holds the masked-token
+ * counts of every worker's running batch back to back (worker 0's first),
+ * batch_sizes[w] how many belong to worker w. *worker_out = -1 (and cost 0)
+ * when no worker has room. cost_ms_out may be NULL. Host-only. */
+ms_status mask_route_request(const ms_model_desc* desc, const ms_cost_model* model,
+                             const int32_t* running_masked, const int32_t* batch_sizes, int32_t n_workers,
+                             int32_t max_batch, int32_t request_masked, int32_t* worker_out,
+                             double* cost_ms_out);
+
 /* Row gather ("extract the matrix of masked tokens", Sec. 3.1):
  * d_xm[m] = d_x[rows[m]]; d_x [B][T][d], d_xm [M][d] (may be NULL: the
  * workspace's own packed-hidden buffer is used). */

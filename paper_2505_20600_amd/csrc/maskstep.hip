@@ -616,13 +616,12 @@ ms_status mask_step_set_dense_prefix(ms_step* s, int32_t k, void* stream) {
     return ok();
 }
 
-ms_status mask_plan_dense_prefix(int32_t n_layers, double load_ms, double cached_ms, double full_ms,
-                                 int32_t* k_out, double* latency_ms_out) {
-    if (n_layers < 1 || !k_out) return fail(MS_EINVAL, "need n_layers >= 1 and k_out");
-    if (!(load_ms >= 0) || !(cached_ms >= 0) || !(full_ms >= 0)) return fail(MS_EINVAL, "negative or NaN cost");
-    // Alg. 1's clocks for the choice "first k blocks over every token, the rest with the cache":
-    // a full block needs no load (comp += full); a cached block's load follows the previous load
-    // and its compute waits for it (comp = max(load, comp) + cached).
+namespace {
+// Alg. 1's clocks for the choice "first k blocks over every token, the rest with the cache":
+// a full block needs no load (comp += full); a cached block's load follows the previous load
+// and its compute waits for it (comp = max(load, comp) + cached). Smallest k on ties.
+void plan_prefix(int32_t n_layers, double load_ms, double cached_ms, double full_ms, int32_t* k_out,
+                 double* latency_out) {
     int best_k = 0;
     double best = 0.0;
     for (int k = 0; k <= n_layers; ++k) {
@@ -641,7 +640,160 @@ ms_status mask_plan_dense_prefix(int32_t n_layers, double load_ms, double cached
         }
     }
     *k_out = best_k;
-    if (latency_ms_out) *latency_ms_out = best;
+    *latency_out = best;
+}
+
+// Algorithmic FLOPs of one block for `rows` recomputed rows of a request (Table 1): the
+// projections and the feed-forward (2 rows d^2 (4 + 2 mlp_mult)) and QK^T and PV over every
+// token (4 rows T d). Exact in double for every model the library accepts.
+double block_flops(const ms_model_desc& d, int64_t rows) {
+    const double D = d.d_model;
+    const double T = (double)d.n_text + (double)d.grid_h * d.grid_w;
+    return 2.0 * (double)rows * D * D * (4 + 2 * d.mlp_mult) + 4.0 * (double)rows * T * D;
+}
+
+bool finite_nonneg(double v) { return std::isfinite(v) && v >= 0.0; }
+
+ms_status check_cost_inputs(const ms_model_desc* desc, const ms_cost_model* m) {
+    if (!desc || !m) return fail(MS_EINVAL, "model description or cost model is NULL");
+    ms_model_desc d = *desc;
+    d.max_batch = 1;   // not used by the cost model
+    const ms_status st = validate_desc(&d);
+    if (st != MS_OK) return st;
+    if (!finite_nonneg(m->comp_ms0) || !finite_nonneg(m->comp_ms_per_gflop) || !finite_nonneg(m->load_ms0) ||
+        !finite_nonneg(m->load_ms_per_mb) || !finite_nonneg(m->cache_bytes_per_token))
+        return fail(MS_EINVAL, "cost model fields must be finite and >= 0");
+    return MS_OK;
+}
+
+// (L, C_w, C_wo) of one block for a validated batch
+void batch_block_costs(const ms_model_desc& d, const ms_cost_model& m, const int32_t* masked, int32_t n,
+                       double out[3]) {
+    const int32_t N = d.grid_h * d.grid_w;
+    const int64_t T = (int64_t)d.n_text + N;
+    double f_cached = 0.0, nbytes = 0.0;
+    for (int32_t b = 0; b < n; ++b) {
+        f_cached += block_flops(d, (int64_t)masked[b] + d.n_text);
+        nbytes += (double)(N - masked[b]) * m.cache_bytes_per_token;
+    }
+    const double f_full = (double)n * block_flops(d, T);
+    out[0] = nbytes == 0.0 ? 0.0 : m.load_ms0 + m.load_ms_per_mb * nbytes / 1e6;
+    out[1] = f_cached == 0.0 ? 0.0 : m.comp_ms0 + m.comp_ms_per_gflop * f_cached / 1e9;
+    out[2] = f_full == 0.0 ? 0.0 : m.comp_ms0 + m.comp_ms_per_gflop * f_full / 1e9;
+}
+
+double batch_latency(const ms_model_desc& d, const ms_cost_model& m, const int32_t* masked, int32_t n,
+                     double costs[3], int32_t* k) {
+    costs[0] = costs[1] = costs[2] = 0.0;
+    *k = 0;
+    if (n == 0) return 0.0;
+    batch_block_costs(d, m, masked, n, costs);
+    double lat = 0.0;
+    plan_prefix(d.n_layers, costs[0], costs[1], costs[2], k, &lat);
+    return lat;
+}
+}  // namespace
+
+ms_status mask_plan_dense_prefix(int32_t n_layers, double load_ms, double cached_ms, double full_ms,
+                                 int32_t* k_out, double* latency_ms_out) {
+    if (n_layers < 1 || !k_out) return fail(MS_EINVAL, "need n_layers >= 1 and k_out");
+    if (!(load_ms >= 0) || !(cached_ms >= 0) || !(full_ms >= 0)) return fail(MS_EINVAL, "negative or NaN cost");
+    double lat = 0.0;
+    plan_prefix(n_layers, load_ms, cached_ms, full_ms, k_out, &lat);
+    if (latency_ms_out) *latency_ms_out = lat;
+    return ok();
+}
+
+ms_status mask_fit_linear(const double* x, const double* y, int32_t n, double* intercept_out, double* slope_out,
+                          double* r2_out) {
+    if (!x || !y || !intercept_out || !slope_out) return fail(MS_EINVAL, "x, y and the outputs must be non-NULL");
+    if (n < 2) return fail(MS_EINVAL, "need at least two points, got %d", n);
+    double xm = 0.0, ym = 0.0;
+    for (int32_t i = 0; i < n; ++i) {
+        if (!std::isfinite(x[i]) || !std::isfinite(y[i])) return fail(MS_EINVAL, "point %d is not finite", i);
+        xm += x[i];
+        ym += y[i];
+    }
+    xm /= n;
+    ym /= n;
+    double sxx = 0.0, sxy = 0.0;
+    for (int32_t i = 0; i < n; ++i) {
+        sxx += (x[i] - xm) * (x[i] - xm);
+        sxy += (x[i] - xm) * (y[i] - ym);
+    }
+    if (!(sxx > 0.0)) return fail(MS_EINVAL, "x has no spread");
+    const double slope = sxy / sxx;
+    const double intercept = ym - slope * xm;
+    double ss_res = 0.0, ss_tot = 0.0;
+    for (int32_t i = 0; i < n; ++i) {
+        const double r = y[i] - (intercept + slope * x[i]);
+        ss_res += r * r;
+        ss_tot += (y[i] - ym) * (y[i] - ym);
+    }
+    *intercept_out = intercept;
+    *slope_out = slope;
+    if (r2_out) *r2_out = ss_tot > 0.0 ? 1.0 - ss_res / ss_tot : (ss_res == 0.0 ? 1.0 : 0.0);
+    return ok();
+}
+
+ms_status mask_batch_cost(const ms_model_desc* desc, const ms_cost_model* model, const int32_t* masked,
+                          int32_t batch, double* costs_out, int32_t* k_out, double* latency_ms_out) {
+    ms_status st = check_cost_inputs(desc, model);
+    if (st != MS_OK) return st;
+    if (batch < 0 || (batch > 0 && !masked)) return fail(MS_EINVAL, "need batch >= 0 and masked[batch]");
+    const int32_t N = desc->grid_h * desc->grid_w;
+    for (int32_t b = 0; b < batch; ++b)
+        if (masked[b] < 0 || masked[b] > N) return fail(MS_EINVAL, "masked[%d] = %d outside 0..%d", b, masked[b], N);
+    double costs[3];
+    int32_t k = 0;
+    const double lat = batch_latency(*desc, *model, masked, batch, costs, &k);
+    if (costs_out) std::memcpy(costs_out, costs, sizeof costs);
+    if (k_out) *k_out = k;
+    if (latency_ms_out) *latency_ms_out = lat;
+    return ok();
+}
+
+ms_status mask_route_request(const ms_model_desc* desc, const ms_cost_model* model, const int32_t* running_masked,
+                             const int32_t* batch_sizes, int32_t n_workers, int32_t max_batch, int32_t request_masked,
+                             int32_t* worker_out, double* cost_ms_out) {
+    ms_status st = check_cost_inputs(desc, model);
+    if (st != MS_OK) return st;
+    if (!worker_out) return fail(MS_EINVAL, "worker_out is NULL");
+    if (n_workers < 0 || (n_workers > 0 && !batch_sizes)) return fail(MS_EINVAL, "need n_workers >= 0 and batch_sizes");
+    if (max_batch < 1) return fail(MS_EINVAL, "max_batch must be >= 1");
+    const int32_t N = desc->grid_h * desc->grid_w;
+    if (request_masked < 0 || request_masked > N)
+        return fail(MS_EINVAL, "request masked count %d outside 0..%d", request_masked, N);
+    int64_t total = 0;
+    for (int32_t w = 0; w < n_workers; ++w) {
+        if (batch_sizes[w] < 0) return fail(MS_EINVAL, "batch_sizes[%d] < 0", w);
+        total += batch_sizes[w];
+    }
+    if (total > 0 && !running_masked) return fail(MS_EINVAL, "running_masked is NULL");
+    for (int64_t i = 0; i < total; ++i)
+        if (running_masked[i] < 0 || running_masked[i] > N)
+            return fail(MS_EINVAL, "running_masked[%lld] outside 0..%d", (long long)i, N);
+    int32_t best = -1;
+    double best_cost = 0.0;
+    std::vector<int32_t> batch;
+    int64_t off = 0;
+    for (int32_t w = 0; w < n_workers; ++w) {
+        const int32_t nb = batch_sizes[w];
+        if (nb < max_batch) {
+            batch.assign(running_masked + off, running_masked + off + nb);
+            batch.push_back(request_masked);
+            double costs[3];
+            int32_t k = 0;
+            const double c = batch_latency(*desc, *model, batch.data(), (int32_t)batch.size(), costs, &k);
+            if (best < 0 || c < best_cost) {
+                best = w;
+                best_cost = c;
+            }
+        }
+        off += nb;
+    }
+    *worker_out = best;
+    if (cost_ms_out) *cost_ms_out = best < 0 ? 0.0 : best_cost;
     return ok();
 }
 

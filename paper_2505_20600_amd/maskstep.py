@@ -43,6 +43,13 @@ class KVSource(C.Structure):
                 ("slots", C.POINTER(C.c_void_p))]
 
 
+class CostModel(C.Structure):
+    """ms_cost_model: per-block Comp(F) = comp_ms0 + comp_ms_per_gflop * F / 1e9 and
+    Load(B) = load_ms0 + load_ms_per_mb * B / 1e6 (Sec. 4.3)."""
+    _fields_ = [("comp_ms0", C.c_double), ("comp_ms_per_gflop", C.c_double), ("load_ms0", C.c_double),
+                ("load_ms_per_mb", C.c_double), ("cache_bytes_per_token", C.c_double)]
+
+
 class StepInfo(C.Structure):
     _fields_ = [("batch", C.c_int32), ("rows", C.c_int32), ("n_segments", C.c_int32),
                 ("n_qtiles", C.c_int32), ("text_rows", C.c_int32), ("dense_prefix", C.c_int32)]
@@ -86,6 +93,12 @@ def load() -> C.CDLL:
             "mask_profiler_start": (i32, [C.c_uint32, i32]),
             "ms_linear": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, sz, vp]),
             "mask_profiler_stop": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
+            "mask_fit_linear": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_double), i32, C.POINTER(C.c_double),
+                                      C.POINTER(C.c_double), C.POINTER(C.c_double)]),
+            "mask_batch_cost": (i32, [C.POINTER(ModelDesc), C.POINTER(CostModel), C.POINTER(i32), i32,
+                                      C.POINTER(C.c_double), C.POINTER(i32), C.POINTER(C.c_double)]),
+            "mask_route_request": (i32, [C.POINTER(ModelDesc), C.POINTER(CostModel), C.POINTER(i32),
+                                         C.POINTER(i32), i32, i32, i32, C.POINTER(i32), C.POINTER(C.c_double)]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -100,7 +113,8 @@ EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask
             "mask_scatter_rows", "cache_prefetch_layer", "cache_prefetch_inputs", "mask_recompute_kv",
             "mask_stack_forward", "mask_step_destroy",
             "mask_step_set_dense_prefix", "mask_plan_dense_prefix",
-            "mask_profiler_start", "mask_profiler_stop", "ms_linear")
+            "mask_profiler_start", "mask_profiler_stop", "ms_linear",
+            "mask_fit_linear", "mask_batch_cost", "mask_route_request")
 
 MS_EPI_BIAS, MS_EPI_BIAS_RESID, MS_EPI_BIAS_GELU = 0, 1, 2
 
@@ -165,6 +179,39 @@ def mask_plan_dense_prefix(n_layers: int, load_ms: float, cached_ms: float, full
     lat = C.c_double()
     _check(load().mask_plan_dense_prefix(n_layers, load_ms, cached_ms, full_ms, C.byref(k), C.byref(lat)))
     return k.value, lat.value
+
+
+def mask_fit_linear(x, y):
+    """(intercept, slope, r2) of the least-squares line y ~ intercept + slope * x."""
+    n = len(x)
+    xa = (C.c_double * max(1, n))(*[float(v) for v in x])
+    ya = (C.c_double * max(1, len(y)))(*[float(v) for v in y])
+    if len(y) != n:
+        raise MaskStepError(MS_EINVAL, "x and y differ in length")
+    a, b, r2 = C.c_double(), C.c_double(), C.c_double()
+    _check(load().mask_fit_linear(xa, ya, n, C.byref(a), C.byref(b), C.byref(r2)))
+    return a.value, b.value, r2.value
+
+
+def mask_batch_cost(desc: ModelDesc, model: CostModel, masked):
+    """((L, C_w, C_wo), dense prefix, latency) of one batch (masked image tokens per request)."""
+    n = len(masked)
+    arr = (C.c_int32 * max(1, n))(*[int(v) for v in masked])
+    costs = (C.c_double * 3)()
+    k, lat = C.c_int32(), C.c_double()
+    _check(load().mask_batch_cost(C.byref(desc), C.byref(model), arr, n, costs, C.byref(k), C.byref(lat)))
+    return (costs[0], costs[1], costs[2]), k.value, lat.value
+
+
+def mask_route_request(desc: ModelDesc, model: CostModel, workers, max_batch: int, request_masked: int):
+    """(worker index or -1, cost) of Alg. 2 for one request; ``workers`` = running batches."""
+    flat = [int(v) for w in workers for v in w]
+    run = (C.c_int32 * max(1, len(flat)))(*flat)
+    sizes = (C.c_int32 * max(1, len(workers)))(*[len(w) for w in workers])
+    w, cost = C.c_int32(), C.c_double()
+    _check(load().mask_route_request(C.byref(desc), C.byref(model), run, sizes, len(workers), max_batch,
+                                     int(request_masked), C.byref(w), C.byref(cost)))
+    return w.value, cost.value
 
 
 def model_desc(shape, max_batch: int | None = None) -> ModelDesc:
