@@ -305,6 +305,8 @@ ms_status mask_profiler_stop(double* total_ms, int64_t* launches, int64_t* dropp
 /* Message of the calling thread's last error ("" if none). */
 const char* mask_last_error(void);
 
+/* Version of this interface: 3 (2 added Y caching's kinds and calls, 3 the
+ * cost-model and routing calls). */
 int32_t mask_abi_version(void);
 
 #ifdef __cplusplus

@@ -20,7 +20,7 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 2;
+constexpr int32_t kAbiVersion = 3;
 constexpr int kMaxBatch = 64;
 // Host-to-device copy spans are merged across masked gaps of at most this
 // many bytes: a gap costs less PCIe time than one more copy submission.
