@@ -110,12 +110,21 @@ typedef enum {
  *                     the unmasked tokens from it (mask_recompute_kv) into the
  *                     workspace; half the cache bytes of the K/V kinds.
  *  MS_Y_HOST_PINNED:  layer[l] is a pinned host [B][N][d] buffer; slots are
- *                     device [B][N][d] buffers used as for MS_KV_HOST_PINNED. */
+ *                     device [B][N][d] buffers used as for MS_KV_HOST_PINNED.
+ * request_layer (host-pinned kinds, may be NULL): when set, it replaces
+ * layer with one pinned buffer per request and layer, entry l * B + b =
+ * request b's [N][2][d] (K/V) or [N][d] (Y) cache of layer l, so that each
+ * request of a continuously re-formed batch keeps its cache where it is.
+ * Entries of requests that recompute nothing (no masked token, no text
+ * rows) are never read and may be NULL: such a request loads no cache, in
+ * either form (step-level continuous batching, Sec. 4.2 "Continuous
+ * Batching": a free batch slot is a request with an empty mask). */
 typedef struct {
     int32_t kind;
     const void* const* layer;   /* [n_layers] */
     int32_t n_slots;            /* host-pinned kinds only, >= 1 */
     void* const* slots;         /* [n_slots], host-pinned kinds only */
+    const void* const* request_layer;   /* host-pinned kinds only: [n_layers * B] or NULL */
 } ms_kv_source;
 
 typedef struct ms_step ms_step;   /* opaque host object, one per mask set */

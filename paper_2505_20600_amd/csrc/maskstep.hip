@@ -247,6 +247,16 @@ void finish_packing(Packing& p, const ms_model_desc& desc, int batch, int T, int
     p.attn_nsplit = (ntiles + tps - 1) / tps;
 }
 
+// A request recomputes rows when it has a masked token or text rows (always
+// recomputed). One that does not needs neither its cache nor any K/V of its
+// unmasked tokens: its output is the cached hidden state.
+bool request_recomputes(const ms_step* s, const uint8_t* m) {
+    if (s->desc.n_text > 0) return true;
+    for (int n = 0; n < s->N; ++n)
+        if (m[n]) return true;
+    return false;
+}
+
 void plan_spans(ms_step* s, const std::vector<uint8_t>& mask) {
     s->spans.clear();
     const size_t row_bytes = 2ull * s->d * s->elt;
@@ -255,6 +265,7 @@ void plan_spans(ms_step* s, const std::vector<uint8_t>& mask) {
     const int gap_rows = (int)(gap_bytes / row_bytes);
     for (int b = 0; b < s->B; ++b) {
         const uint8_t* m = mask.data() + (size_t)b * s->N;
+        if (!request_recomputes(s, m)) continue;   // no query attends over its keys
         int n = 0;
         Span cur{b, -1, -1};
         while (n < s->N) {
@@ -449,26 +460,31 @@ ms_status recompute_kv(ms_step* s, const ms_layer_weights* w, const void* y_in, 
 // Loads the unmasked image rows of one block's cache from pinned host memory:
 // K/V rows [B][N][2][d] -> slot [B][T][2][d] at n_text + n, or (y) block
 // input rows [B][N][d] -> slot [B][N][d] in place.
-ms_status prefetch(ms_step* s, const void* h_kv, void* d_slot, hipStream_t cs, hipEvent_t wait,
-                   bool y = false) {
+// One layer's host cache: a [B][N][row] buffer, or (req non-NULL) request b's
+// own [N][row] buffer at req[b].
+struct HostLayer {
+    const void* base;
+    const void* const* req;
+};
+
+ms_status prefetch(ms_step* s, HostLayer h, void* d_slot, hipStream_t cs, hipEvent_t wait, bool y = false) {
     if (wait) MS_HIP(hipStreamWaitEvent(cs, wait, 0));
     ProfScope p(MS_K_COPY, cs);
     const size_t row_bytes = (y ? 1ull : 2ull) * s->d * s->elt;
     const size_t drows = y ? (size_t)s->N : (size_t)s->T, dtext = y ? 0 : (size_t)s->desc.n_text;
-    const char* src = static_cast<const char*>(h_kv);
     char* dst = static_cast<char*>(d_slot);
     for (const Span& sp : s->spans) {
-        const size_t so = ((size_t)sp.b * s->N + sp.n0) * row_bytes;
+        const char* src = h.req ? static_cast<const char*>(h.req[sp.b]) + (size_t)sp.n0 * row_bytes
+                                : static_cast<const char*>(h.base) + ((size_t)sp.b * s->N + sp.n0) * row_bytes;
         const size_t dof = ((size_t)sp.b * drows + dtext + sp.n0) * row_bytes;
-        MS_HIP(hipMemcpyAsync(dst + dof, src + so, (size_t)(sp.n1 - sp.n0) * row_bytes,
-                              hipMemcpyHostToDevice, cs));
+        MS_HIP(hipMemcpyAsync(dst + dof, src, (size_t)(sp.n1 - sp.n0) * row_bytes, hipMemcpyHostToDevice, cs));
     }
     return MS_OK;
 }
 
-ms_status prefetch_signal(ms_step* s, const void* h_kv, void* d_slot, hipStream_t cs, hipEvent_t wait,
+ms_status prefetch_signal(ms_step* s, HostLayer h, void* d_slot, hipStream_t cs, hipEvent_t wait,
                           hipEvent_t signal, bool y = false) {
-    ms_status st = prefetch(s, h_kv, d_slot, cs, wait, y);
+    ms_status st = prefetch(s, h, d_slot, cs, wait, y);
     if (st != MS_OK) return st;
     if (signal) MS_HIP(hipEventRecord(signal, cs));
     return MS_OK;
@@ -564,12 +580,14 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
     finish_packing(p, *desc, batch, s->T, s->hd);
     s->all_masked = p.M == batch * s->T;
     plan_spans(s, hmask);
-    for (int b = 0; b < batch; ++b)
+    for (int b = 0; b < batch; ++b) {
+        if (!request_recomputes(s, hmask.data() + (size_t)b * s->N)) continue;
         for (int n = 0; n < s->N; ++n)
             if (!hmask[(size_t)b * s->N + n]) {
                 s->h_usrc.push_back(b * s->N + n);
                 s->h_utok.push_back(b * s->T + desc->n_text + n);
             }
+    }
     s->U = (int)s->h_usrc.size();
     if (s->U > 0) {
         e = hipMemcpyAsync(s->buf(lay.u_src), s->h_usrc.data(), s->U * sizeof(int32_t), hipMemcpyHostToDevice, hs);
@@ -841,7 +859,7 @@ ms_status cache_prefetch_layer(ms_step* s, int32_t layer, const void* h_kv, void
     if (!aligned16(h_kv) || !aligned16(d_slot)) return fail(MS_EALIGN, "h_kv / slot not 16-byte aligned");
     ms_status st = check_pinned(h_kv);
     if (st != MS_OK) return st;
-    st = prefetch_signal(s, h_kv, d_slot, static_cast<hipStream_t>(copy_stream),
+    st = prefetch_signal(s, HostLayer{h_kv, nullptr}, d_slot, static_cast<hipStream_t>(copy_stream),
                          static_cast<hipEvent_t>(wait_event), static_cast<hipEvent_t>(signal_event));
     return st == MS_OK ? ok() : st;
 }
@@ -854,7 +872,7 @@ ms_status cache_prefetch_inputs(ms_step* s, int32_t layer, const void* h_yin, vo
     if (!aligned16(h_yin) || !aligned16(d_slot)) return fail(MS_EALIGN, "h_yin / slot not 16-byte aligned");
     ms_status st = check_pinned(h_yin);
     if (st != MS_OK) return st;
-    st = prefetch_signal(s, h_yin, d_slot, static_cast<hipStream_t>(copy_stream),
+    st = prefetch_signal(s, HostLayer{h_yin, nullptr}, d_slot, static_cast<hipStream_t>(copy_stream),
                          static_cast<hipEvent_t>(wait_event), static_cast<hipEvent_t>(signal_event), true);
     return st == MS_OK ? ok() : st;
 }
@@ -878,18 +896,34 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
     if (!w || !d_x || !kv || !d_y) return fail(MS_EINVAL, "NULL argument");
     if (!d_ycache && !s->all_masked) return fail(MS_EINVAL, "y_cache may be NULL only when every token is masked");
     if (kv->kind < MS_KV_DEVICE || kv->kind > MS_Y_HOST_PINNED) return fail(MS_EINVAL, "unknown kv kind %d", kv->kind);
-    if (!kv->layer) return fail(MS_EINVAL, "kv->layer is NULL");
     const bool ycache = kv->kind == MS_Y_DEVICE || kv->kind == MS_Y_HOST_PINNED;
+    const bool pinned = kv->kind == MS_KV_HOST_PINNED || kv->kind == MS_Y_HOST_PINNED;
+    const bool per_req = pinned && kv->request_layer;
+    if (!per_req && !kv->layer) return fail(MS_EINVAL, "kv->layer is NULL");
     const int L = s->desc.n_layers;
     const int k = s->dense_prefix;
     const int wstride = s->desc.dual_stream ? 2 : 1;
+    // requests whose cache is read (those with spans) need a valid host pointer per layer
+    std::vector<uint8_t> reads(s->B, 0);
+    for (const Span& sp : s->spans) reads[sp.b] = 1;
     for (int l = 0; l < L; ++l) {
-        if (!kv->layer[l]) return fail(MS_EINVAL, "kv->layer[%d] is NULL", l);
-        if (!aligned16(kv->layer[l])) return fail(MS_EALIGN, "kv->layer[%d] not 16-byte aligned", l);
+        if (per_req) {
+            for (int b = 0; b < s->B; ++b) {
+                const void* q = kv->request_layer[(size_t)l * s->B + b];
+                if (!reads[b]) continue;
+                if (!q) return fail(MS_EINVAL, "kv->request_layer[%d * B + %d] is NULL", l, b);
+                if (!aligned16(q)) return fail(MS_EALIGN, "kv->request_layer[%d * B + %d] not 16-byte aligned", l, b);
+            }
+        } else {
+            if (!kv->layer[l]) return fail(MS_EINVAL, "kv->layer[%d] is NULL", l);
+            if (!aligned16(kv->layer[l])) return fail(MS_EALIGN, "kv->layer[%d] not 16-byte aligned", l);
+        }
         ms_status st = check_weights(s, w + (size_t)l * wstride);
         if (st != MS_OK) return st;
     }
-    const bool pinned = kv->kind == MS_KV_HOST_PINNED || kv->kind == MS_Y_HOST_PINNED;
+    auto host_layer = [&](int l) {
+        return per_req ? HostLayer{nullptr, kv->request_layer + (size_t)l * s->B} : HostLayer{kv->layer[l], nullptr};
+    };
     const int n_slots = pinned ? kv->n_slots : 0;
     if (pinned) {
         if (n_slots < 1 || !kv->slots) return fail(MS_EINVAL, "a pinned cache needs n_slots >= 1 device slots");
@@ -898,8 +932,11 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             if (!aligned16(kv->slots[i])) return fail(MS_EALIGN, "kv->slots[%d] not 16-byte aligned", i);
         }
         if (!s->all_masked && s->mp.M > 0 && k < L) {
-            ms_status st = check_pinned(kv->layer[k]);
-            if (st != MS_OK) return st;
+            for (int b = 0; b < (per_req ? s->B : 1); ++b) {
+                if (per_req && !reads[b]) continue;
+                ms_status st = check_pinned(per_req ? kv->request_layer[(size_t)k * s->B + b] : kv->layer[k]);
+                if (st != MS_OK) return st;
+            }
         }
         ms_status st = ensure_events(s, n_slots);
         if (st != MS_OK) return st;
@@ -920,7 +957,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             MS_HIP(hipEventRecord(s->ev_start, cs));
             MS_HIP(hipStreamWaitEvent(ps, s->ev_start, 0));
             for (int j = 0; j < std::min(n_slots, n_cached); ++j) {
-                ms_status st = prefetch_signal(s, kv->layer[k + j], kv->slots[j], ps, nullptr, s->ev_copied[j],
+                ms_status st = prefetch_signal(s, host_layer(k + j), kv->slots[j], ps, nullptr, s->ev_copied[j],
                                                ycache);
                 if (st != MS_OK) return st;
             }
@@ -952,11 +989,11 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         }
         for (int l = k; l < L; ++l) {
             const int j = l - k;
-            void* src = const_cast<void*>(kv->layer[l]);
+            void* src = pinned ? nullptr : const_cast<void*>(kv->layer[l]);
             if (pinned) {
                 src = kv->slots[j % n_slots];
                 if (serialize) {
-                    ms_status st = prefetch(s, kv->layer[l], src, cs, nullptr, ycache);
+                    ms_status st = prefetch(s, host_layer(l), src, cs, nullptr, ycache);
                     if (st != MS_OK) return st;
                 } else if (stream_cache) {
                     MS_HIP(hipStreamWaitEvent(cs, s->ev_copied[j % n_slots], 0));
@@ -975,7 +1012,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             if (stream_cache && !serialize && j + n_slots < n_cached) {
                 const int sl = j % n_slots;
                 MS_HIP(hipEventRecord(s->ev_consumed[sl], cs));
-                st = prefetch_signal(s, kv->layer[l + n_slots], kv->slots[sl], ps, s->ev_consumed[sl],
+                st = prefetch_signal(s, host_layer(l + n_slots), kv->slots[sl], ps, s->ev_consumed[sl],
                                      s->ev_copied[sl], ycache);
                 if (st != MS_OK) return st;
             }

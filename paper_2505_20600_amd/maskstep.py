@@ -40,7 +40,7 @@ class LayerWeights(C.Structure):
 
 class KVSource(C.Structure):
     _fields_ = [("kind", C.c_int32), ("layer", C.POINTER(C.c_void_p)), ("n_slots", C.c_int32),
-                ("slots", C.POINTER(C.c_void_p))]
+                ("slots", C.POINTER(C.c_void_p)), ("request_layer", C.POINTER(C.c_void_p))]
 
 
 class CostModel(C.Structure):
@@ -234,7 +234,8 @@ def layer_weights_struct(w: dict) -> LayerWeights:
 
 
 def weights_array(layers) -> C.Array:
-    """[L] (or [L][2] image, text) weight dicts of device tensors -> a C array of structs."""
+    """[L] (or [L][2] image, text) weight dicts of device tensors -> a C array of structs.
+    The array keeps the tensors alive: the structs hold only their addresses."""
     flat = []
     for w in layers:
         if isinstance(w, (tuple, list)):
@@ -242,6 +243,7 @@ def weights_array(layers) -> C.Array:
         else:
             flat.append(w)
     arr = (LayerWeights * len(flat))(*[layer_weights_struct(w) for w in flat])
+    arr._tensors = flat
     return arr
 
 
@@ -325,17 +327,28 @@ class MaskStep:
         _check(self._lib.mask_step_set_dense_prefix(self.handle, k, _stream(stream)))
 
     def stack_forward(self, weights_c, x, ycache, kv_layers, y, *, pinned: bool = False, slots=(),
-                      stream=None, copy_stream=None, inputs: bool = False):
+                      stream=None, copy_stream=None, inputs: bool = False, per_request=None):
         """``weights_c`` from weights_array(); ``kv_layers``: [L] tensors (device or pinned host),
         per-layer K/V [B][T|N][2][d], or with ``inputs`` the cached block inputs [B][N][d]
-        (Y caching); ``slots``: device buffers the pinned layers stream through."""
-        L = len(kv_layers)
-        ptrs = (C.c_void_p * L)(*[_ptr(t) for t in kv_layers])
+        (Y caching); ``slots``: device buffers the pinned layers stream through. With
+        ``pinned``, ``per_request`` may replace ``kv_layers``: [L][B] pinned per-request
+        buffers (or None for requests that recompute nothing)."""
+        if per_request is not None:
+            L = len(per_request)
+            ptrs = (C.c_void_p * 1)()
+            req = (C.c_void_p * max(1, sum(len(r) for r in per_request)))(
+                *[_ptr(t) for r in per_request for t in r])
+            req_p = C.cast(req, C.POINTER(C.c_void_p))
+            layer_p = C.POINTER(C.c_void_p)()
+        else:
+            L = len(kv_layers)
+            ptrs = (C.c_void_p * L)(*[_ptr(t) for t in kv_layers])
+            req_p = C.POINTER(C.c_void_p)()
+            layer_p = C.cast(ptrs, C.POINTER(C.c_void_p))
         sl = (C.c_void_p * max(1, len(slots)))(*[_ptr(t) for t in slots])
         kind = (MS_Y_HOST_PINNED if pinned else MS_Y_DEVICE) if inputs else \
                (MS_KV_HOST_PINNED if pinned else MS_KV_DEVICE)
-        src = KVSource(kind, C.cast(ptrs, C.POINTER(C.c_void_p)),
-                       len(slots) if pinned else 0, C.cast(sl, C.POINTER(C.c_void_p)))
+        src = KVSource(kind, layer_p, len(slots) if pinned else 0, C.cast(sl, C.POINTER(C.c_void_p)), req_p)
         cs = _stream(stream)
         ps = _stream(copy_stream) if copy_stream is not None else cs
         _check(self._lib.mask_stack_forward(self.handle, weights_c, _ptr(x), _ptr(ycache), C.byref(src),
