@@ -167,6 +167,8 @@ SMALL_BF16 = [
     W.ModelShape("hd128_b3", 2, 256, 2, 4, 12, 16, dtype="bf16", batch=3),
     # dual weight streams with text rows always recomputed
     W.ModelShape("dual_txt40_b2", 2, 256, 2, 4, 10, 10, n_text=40, dual_stream=True, dtype="bf16", batch=2),
+    # 2 x 96 text rows: the text / image boundary on a multiple of every tile height
+    W.ModelShape("dual_txt96_b2", 2, 256, 2, 4, 10, 10, n_text=96, dual_stream=True, dtype="bf16", batch=2),
 ]
 
 
