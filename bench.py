@@ -511,7 +511,6 @@ def main():
             "gemm_out": ("mfma", 2.0 * m_sum * d * d),
             "gemm_up": ("mfma", 2.0 * m_sum * d * f),
             "gemm_down": ("mfma", 2.0 * m_sum * f * d),
-            "layernorm": ("hbm", 2.0 * 2 * m_sum * d * e + 2.0 * u_sum * d * e),
             "gather": ("hbm", 2.0 * tot_m_prof * d * e),
         }
         prof.pop("_dropped", None)

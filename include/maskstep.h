@@ -300,7 +300,9 @@ void mask_step_destroy(ms_step* step);
  * stream it is launched on; stop synchronizes those events and returns, per
  * class, the summed milliseconds and the launch count (arrays of
  * MS_K_COUNT entries, either may be NULL). Process-wide; up to `capacity`
- * launches are recorded, further ones are counted in `dropped`. */
+ * launches are recorded, further ones are counted in `dropped`.
+ * MS_K_GEMM_REDUCE (split-K partial sums) includes the LayerNorm that follows
+ * a residual projection when the two run as one kernel. */
 typedef enum {
     MS_K_COMPACT = 0, MS_K_GATHER = 1, MS_K_LAYERNORM = 2, MS_K_GEMM_QKV = 3,
     MS_K_ATTENTION = 4, MS_K_GEMM_OUT = 5, MS_K_GEMM_UP = 6, MS_K_GEMM_DOWN = 7,

@@ -34,6 +34,14 @@ hipError_t launch_scatter(const void* xm, const int32_t* rows, const int32_t* in
 hipError_t launch_layernorm(int dtype, const void* x, const void* g0, const void* b0,
                             const void* g1, const void* b1, int m_split, void* y, int M, int d,
                             float eps, hipStream_t s, const int32_t* idx = nullptr);
+// Split-K sum of a bias + residual projection into C (row stride ldc) fused
+// with LayerNorm of the new C rows into y (row stride ldy), one weight set;
+// part is [ksplit][M][d] float32, N = d. Same results as the split-K sum
+// followed by launch_layernorm.
+hipError_t launch_reduce_layernorm(int dtype, const float* part, int ksplit, const void* bias,
+                                   const void* R, int ldr, void* C, int ldc, const void* g,
+                                   const void* b, void* y, int ldy, int M, int d, float eps,
+                                   hipStream_t s);
 
 enum Epilogue { kEpiBias = 0, kEpiBiasResid = 1, kEpiBiasGelu = 2, kEpiQKV = 3 };
 

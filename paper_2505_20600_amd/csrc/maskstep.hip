@@ -323,7 +323,23 @@ ms_status check_weights(const ms_step* s, const ms_layer_weights* w) {
     return MS_OK;
 }
 
-hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, int cls, hipStream_t st) {
+bool env_flag(const char* name) {
+    const char* v = std::getenv(name);
+    return v && v[0] && std::strcmp(v, "0") != 0;
+}
+
+// LayerNorm of a GEMM's output rows (row stride N) into y (row stride N),
+// one weight set.
+struct LnAfter {
+    const void* g;
+    const void* b;
+    void* y;
+};
+
+// A projection, with the LayerNorm that reads its output when `ln` is given:
+// fused into the split-K sum when the plan splits K (bias + residual
+// epilogue only), else a LayerNorm launch of its own.
+hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, int cls, hipStream_t st, const LnAfter* ln = nullptr) {
     const ms::GemmPlan p = ms::plan_gemm(s->desc.dtype, g.M, g.N, g.K, ms::kGemmPartFloats);
     g.bm = p.bm;
     g.bn = p.bn;
@@ -335,13 +351,27 @@ hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, int cls, hipStream_t st) {
         ProfScope prof(cls, st);
         e = ms::launch_gemm(s->desc.dtype, g, st);
     }
-    if (e != hipSuccess || g.ksplit <= 1) return e;
-    ProfScope prof(MS_K_GEMM_REDUCE, st);
-    return ms::launch_gemm_reduce(s->desc.dtype, g, st);
+    if (e != hipSuccess) return e;
+    if (g.ksplit > 1) {
+        ProfScope prof(MS_K_GEMM_REDUCE, st);
+        if (ln && g.epilogue == ms::kEpiBiasResid && !env_flag("MS_NO_LN_FUSE"))
+            return ms::launch_reduce_layernorm(s->desc.dtype, g.part, g.ksplit, g.bias, g.R, g.ldr, g.C,
+                                               g.ldc, ln->g, ln->b, ln->y, g.N, g.M, g.N, s->desc.ln_eps, st);
+        e = ms::launch_gemm_reduce(s->desc.dtype, g, st);
+        if (e != hipSuccess) return e;
+    }
+    if (!ln) return hipSuccess;
+    ProfScope prof(MS_K_LAYERNORM, st);
+    return ms::launch_layernorm(s->desc.dtype, g.C, ln->g, ln->b, ln->g, ln->b, 0, ln->y, g.M, g.N,
+                                s->desc.ln_eps, st);
 }
 
+// One block over the packed rows. `a_ready`: the scratch row buffer already
+// holds LayerNorm 1 of xm (the previous block computed it); `next`: weights
+// of the block that follows on the same rows, whose LayerNorm 1 this block
+// then leaves in the scratch buffer.
 ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w, void* xm, void* kv,
-                        hipStream_t st) {
+                        hipStream_t st, const ms_layer_weights* next = nullptr, bool a_ready = false) {
     if (pk.M == 0) return MS_OK;
     const int dt = s->desc.dtype;
     const bool dual = s->desc.dual_stream && s->desc.n_text > 0;
@@ -356,14 +386,16 @@ ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w
     char* u = static_cast<char*>(s->buf(s->lay.u));
     char* x = static_cast<char*>(xm);
 
-    {
+    if (!a_ready) {
         ProfScope p(MS_K_LAYERNORM, st);
         MS_HIP(ms::launch_layernorm(dt, x, wi.ln1_g, wi.ln1_b, wt.ln1_g, wt.ln1_b, msplit, a, M, d,
                                     s->desc.ln_eps, st));
     }
-    // row ranges per weight set: text rows [0, msplit) then image rows
-    struct Range { int r0, r1; const ms_layer_weights* w; };
-    Range ranges[2] = {{0, msplit, &wt}, {msplit, M, &wi}};
+    // row ranges per weight set: text rows [0, msplit) then image rows; `nw`
+    // is the next block's weight set for the same rows
+    struct Range { int r0, r1; const ms_layer_weights* w; const ms_layer_weights* nw; };
+    Range ranges[2] = {{0, msplit, &wt, next ? &next[dual ? 1 : 0] : nullptr},
+                       {msplit, M, &wi, next}};
     for (const Range& r : ranges) {
         if (r.r1 <= r.r0) continue;
         ms::GemmDesc g{};
@@ -405,12 +437,8 @@ ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w
         g.R = x + (size_t)r.r0 * d * e; g.C = h + (size_t)r.r0 * d * e;
         g.M = r.r1 - r.r0; g.N = d; g.K = d; g.lda = d; g.ldr = d; g.ldc = d;
         g.epilogue = ms::kEpiBiasResid;
-        MS_HIP(run_gemm(s, g, MS_K_GEMM_OUT, st));
-    }
-    {
-        ProfScope p(MS_K_LAYERNORM, st);
-        MS_HIP(ms::launch_layernorm(dt, h, wi.ln2_g, wi.ln2_b, wt.ln2_g, wt.ln2_b, msplit, a, M, d,
-                                    s->desc.ln_eps, st));
+        const LnAfter ln2{r.w->ln2_g, r.w->ln2_b, a + (size_t)r.r0 * d * e};
+        MS_HIP(run_gemm(s, g, MS_K_GEMM_OUT, st, &ln2));
     }
     for (const Range& r : ranges) {
         if (r.r1 <= r.r0) continue;
@@ -428,7 +456,8 @@ ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w
         g.R = h + (size_t)r.r0 * d * e; g.C = x + (size_t)r.r0 * d * e;
         g.M = r.r1 - r.r0; g.N = d; g.K = f; g.lda = f; g.ldr = d; g.ldc = d;
         g.epilogue = ms::kEpiBiasResid;
-        MS_HIP(run_gemm(s, g, MS_K_GEMM_DOWN, st));
+        const LnAfter ln1{r.nw ? r.nw->ln1_g : nullptr, r.nw ? r.nw->ln1_b : nullptr, a + (size_t)r.r0 * d * e};
+        MS_HIP(run_gemm(s, g, MS_K_GEMM_DOWN, st, r.nw ? &ln1 : nullptr));
     }
     return MS_OK;
 }
@@ -500,11 +529,6 @@ ms_status check_pinned(const void* p) {
     if (attr.type != hipMemoryTypeHost)
         return fail(MS_ENOTPINNED, "host K/V pointer is not pinned host memory (memory type %d)", (int)attr.type);
     return MS_OK;
-}
-
-bool env_flag(const char* name) {
-    const char* v = std::getenv(name);
-    return v && v[0] && std::strcmp(v, "0") != 0;
 }
 
 }  // namespace
@@ -971,7 +995,8 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 MS_HIP(ms::launch_gather(d_x, dp.rows, xm, dp.M, s->d * s->elt, cs));
             }
             for (int l = 0; l < k; ++l) {
-                ms_status st = block_forward(s, dp, w + (size_t)l * wstride, xm, kvd, cs);
+                const ms_layer_weights* next = l + 1 < k ? w + (size_t)(l + 1) * wstride : nullptr;
+                ms_status st = block_forward(s, dp, w + (size_t)l * wstride, xm, kvd, cs, next, l > 0);
                 if (st != MS_OK) return st;
             }
             // hidden states of every token back in token order, then the masked rows
@@ -1007,7 +1032,8 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 ms_status st = recompute_kv(s, w + (size_t)l * wstride, src, kvbuf, cs);
                 if (st != MS_OK) return st;
             }
-            ms_status st = block_forward(s, mp, w + (size_t)l * wstride, xm, kvbuf, cs);
+            const ms_layer_weights* next = l + 1 < L ? w + (size_t)(l + 1) * wstride : nullptr;
+            ms_status st = block_forward(s, mp, w + (size_t)l * wstride, xm, kvbuf, cs, next, l > k);
             if (st != MS_OK) return st;
             if (stream_cache && !serialize && j + n_slots < n_cached) {
                 const int sl = j % n_slots;

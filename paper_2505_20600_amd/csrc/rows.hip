@@ -78,6 +78,54 @@ __device__ __forceinline__ float vec_elt(const vec16& v, int e) {
     }
 }
 
+// Normalises one row held by a wave: lane holds the 16-byte vectors c = lane
+// + 64 i of the row (values v as float, affine parameters gv, bv), mean and
+// variance in two passes, y = (v - mean) / sqrt(var + eps) * gamma + beta.
+template <typename T>
+__device__ __forceinline__ void ln_row(float (&v)[kLnMaxVecPerLane][16 / sizeof(T)],
+                                       const vec16 (&gv)[kLnMaxVecPerLane],
+                                       const vec16 (&bv)[kLnMaxVecPerLane], int lane, int nvec, int d,
+                                       float eps, T* __restrict__ yr) {
+    constexpr int V = 16 / sizeof(T);
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+        const int c = lane + i * kWave;
+        if (c < nvec) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) s += v[i][e];
+        }
+    }
+    const float mean = wave_sum(s) / d;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+        const int c = lane + i * kWave;
+        if (c < nvec) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                const float t = v[i][e] - mean;
+                q += t * t;
+            }
+        }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(q) / d + eps);
+#pragma unroll
+    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+        const int c = lane + i * kWave;
+        if (c < nvec) {
+#pragma unroll
+            for (int e = 0; e < V; e += 4) {
+                float o[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    o[k] = (v[i][e + k] - mean) * rstd * vec_elt<T>(gv[i], e + k) + vec_elt<T>(bv[i], e + k);
+                store4<T>(yr + c * V + e, o);
+            }
+        }
+    }
+}
+
 template <typename T>
 __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
     const T* __restrict__ x, const T* __restrict__ g0, const T* __restrict__ b0,
@@ -102,46 +150,123 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
         }
     }
     float v[kLnMaxVecPerLane][V];
-    float s = 0.f;
 #pragma unroll
     for (int i = 0; i < kLnMaxVecPerLane; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
-            for (int e = 0; e < V; ++e) {
-                v[i][e] = vec_elt<T>(xv[i], e);
-                s += v[i][e];
-            }
+            for (int e = 0; e < V; ++e) v[i][e] = vec_elt<T>(xv[i], e);
         }
     }
-    const float mean = wave_sum(s) / d;
-    float q = 0.f;
+    ln_row<T>(v, gv, bv, lane, nvec, d, eps, y + (long)row * d);
+}
+
+// Split-K sum of a residual projection followed by the LayerNorm that reads
+// its output (Sec. 2.1: a block's attention output projection and MLP each
+// add into the residual stream, which the next LayerNorm normalises). Per
+// row: c = sum of the partials in split order + bias + residual, stored in T
+// (the residual stream), then LayerNorm of the stored values into y. The
+// arithmetic and its order are those of the separate split-K sum and
+// LayerNorm kernels, so both outputs equal theirs bit for bit; the residual
+// row is not read back and one launch is saved.
+template <typename T, int KS>
+__global__ __launch_bounds__(kLnWaves * kWave) void reduce_layernorm_kernel(
+    const float* __restrict__ part, const T* __restrict__ bias, const T* __restrict__ R,
+    int ldr, T* __restrict__ C, int ldc, const T* __restrict__ gam, const T* __restrict__ bet,
+    T* __restrict__ y, int ldy, int M, int d, float eps) {
+    constexpr int V = 16 / sizeof(T);
+    const int lane = threadIdx.x % kWave;
+    const int row = blockIdx.x * kLnWaves + threadIdx.x / kWave;
+    if (row >= M) return;
+    const int nvec = d / V;
+    vec16 rv[kLnMaxVecPerLane], gv[kLnMaxVecPerLane], bv[kLnMaxVecPerLane];
 #pragma unroll
     for (int i = 0; i < kLnMaxVecPerLane; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
-#pragma unroll
-            for (int e = 0; e < V; ++e) {
-                const float t = v[i][e] - mean;
-                q += t * t;
-            }
+            rv[i] = ld16(R + (long)row * ldr + c * V);
+            gv[i] = ld16(gam + c * V);
+            bv[i] = ld16(bet + c * V);
         }
     }
-    const float rstd = 1.0f / sqrtf(wave_sum(q) / d + eps);
-    T* yr = y + (long)row * d;
+    // the KS partials of a vector are loaded together (KS is a compile-time
+    // count so that they are all in flight), then summed in split order
+    float v[kLnMaxVecPerLane][V];
+    const float* pr = part + (long)row * d;
+    const long plane = (long)M * d;
 #pragma unroll
     for (int i = 0; i < kLnMaxVecPerLane; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
             for (int e = 0; e < V; e += 4) {
-                float o[4];
+                float4 p[KS];
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    o[k] = (v[i][e + k] - mean) * rstd * vec_elt<T>(gv[i], e + k) + vec_elt<T>(bv[i], e + k);
-                store4<T>(yr + c * V + e, o);
+                for (int s = 0; s < KS; ++s) p[s] = *reinterpret_cast<const float4*>(pr + s * plane + c * V + e);
+                float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+                for (int s = 0; s < KS; ++s) {
+                    a0 += p[s].x; a1 += p[s].y; a2 += p[s].z; a3 += p[s].w;
+                }
+                v[i][e] = a0; v[i][e + 1] = a1; v[i][e + 2] = a2; v[i][e + 3] = a3;
             }
         }
+    }
+#pragma unroll
+    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+        const int c = lane + i * kWave;
+        if (c < nvec) {
+#pragma unroll
+            for (int e = 0; e < V; e += 4) {
+                float bb[4];
+                load4<T>(bias + c * V + e, bb);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    v[i][e + k] += bb[k];
+                    v[i][e + k] += vec_elt<T>(rv[i], e + k);
+                }
+                T* cp = C + (long)row * ldc + c * V + e;
+                if constexpr (sizeof(T) == 2) {
+                    // LayerNorm takes the stored (rounded) residual values
+                    uint2 o;
+                    o.x = pack_bf16x2(v[i][e], v[i][e + 1]);
+                    o.y = pack_bf16x2(v[i][e + 2], v[i][e + 3]);
+                    *reinterpret_cast<uint2*>(cp) = o;
+                    v[i][e] = __uint_as_float(o.x << 16);
+                    v[i][e + 1] = __uint_as_float(o.x & 0xffff0000u);
+                    v[i][e + 2] = __uint_as_float(o.y << 16);
+                    v[i][e + 3] = __uint_as_float(o.y & 0xffff0000u);
+                } else {
+                    store4<T>(cp, &v[i][e]);
+                }
+            }
+        }
+    }
+    ln_row<T>(v, gv, bv, lane, nvec, d, eps, y + (long)row * ldy);
+}
+
+constexpr int kMaxReduceSplit = 8;
+
+template <typename T, int KS>
+hipError_t reduce_ln_launch(const float* part, const void* bias, const void* R, int ldr, void* C, int ldc,
+                            const void* g, const void* b, void* y, int ldy, int M, int d, float eps,
+                            hipStream_t s) {
+    dim3 grid((M + kLnWaves - 1) / kLnWaves), block(kLnWaves * kWave);
+    hipLaunchKernelGGL((reduce_layernorm_kernel<T, KS>), grid, block, 0, s, part,
+                       static_cast<const T*>(bias), static_cast<const T*>(R), ldr, static_cast<T*>(C), ldc,
+                       static_cast<const T*>(g), static_cast<const T*>(b), static_cast<T*>(y), ldy, M, d, eps);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t reduce_ln_dispatch(int ksplit, const float* part, const void* bias, const void* R, int ldr, void* C,
+                              int ldc, const void* g, const void* b, void* y, int ldy, int M, int d, float eps,
+                              hipStream_t s) {
+    switch (ksplit) {
+#define MS_KS(n) case n: return reduce_ln_launch<T, n>(part, bias, R, ldr, C, ldc, g, b, y, ldy, M, d, eps, s);
+        MS_KS(1) MS_KS(2) MS_KS(3) MS_KS(4) MS_KS(5) MS_KS(6) MS_KS(7) MS_KS(8)
+#undef MS_KS
+        default: return hipErrorInvalidValue;
     }
 }
 
@@ -205,6 +330,17 @@ hipError_t launch_layernorm(int dtype, const void* x, const void* g0, const void
                            eps, idx);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_reduce_layernorm(int dtype, const float* part, int ksplit, const void* bias,
+                                   const void* R, int ldr, void* C, int ldc, const void* g,
+                                   const void* b, void* y, int ldy, int M, int d, float eps,
+                                   hipStream_t s) {
+    if (M == 0) return hipSuccess;
+    if (ksplit < 1 || ksplit > kMaxReduceSplit) return hipErrorInvalidValue;
+    return dtype == kBF16
+        ? reduce_ln_dispatch<bf16_t>(ksplit, part, bias, R, ldr, C, ldc, g, b, y, ldy, M, d, eps, s)
+        : reduce_ln_dispatch<float>(ksplit, part, bias, R, ldr, C, ldc, g, b, y, ldy, M, d, eps, s);
 }
 
 }  // namespace ms

@@ -189,6 +189,36 @@ def test_small_bf16_stack_matches_oracle(shape, ratio):
         np.testing.assert_array_equal(kv_gpu[0][b, keep], kv[0][b, keep])
 
 
+FUSE_SHAPES = [
+    # d = 576 at a few hundred rows: both residual projections split K
+    W.ModelShape("fuse_dual_d576", 3, 576, 8, 4, 10, 12, n_text=24, dual_stream=True, dtype="bf16", batch=2),
+    # float32 never splits K: LayerNorm runs per row range after each projection
+    W.ModelShape("fuse_f32_d256", 3, 256, 4, 4, 10, 10, dtype="fp32", batch=2),
+]
+
+
+@pytest.mark.parametrize("shape", FUSE_SHAPES, ids=lambda s: s.name)
+def test_split_k_sum_fused_with_layernorm_is_bit_exact(shape, monkeypatch):
+    """A split-K residual projection with its following LayerNorm in one kernel gives the
+    same bits as the split-K sum and a LayerNorm launch, across blocks (LayerNorm 1 of the
+    next block), with two weight sets, a dense prefix and Y caching."""
+    ws, xt, kv, yc = _inputs(shape, 80, std=0.03)
+    mask = _random_mask(shape, [0.3, 0.1], 17)
+    x = W.edited_hidden(shape, 80, xt, mask)
+    dt = "bf16" if shape.dtype == "bf16" else "fp32"
+    G.assert_close(G.run_stack(shape, mask, x, kv, yc, ws)[0], oracle.masked_stack(x, mask, kv, yc, ws, shape),
+                   dt, f"{shape.name} fused")
+    yin = np.stack([np.asarray(yc)[:, shape.n_text:]] * shape.n_layers)
+    runs = [dict(), dict(dense_prefix=1), dict(pinned=True), dict(inputs=True, pinned=True)]
+    for kw in runs:
+        outs = []
+        for flag in ("0", "1"):
+            monkeypatch.setenv("MS_NO_LN_FUSE", flag)
+            cache = yin if kw.get("inputs") else kv
+            outs.append(G.run_stack(shape, mask, x, cache, yc, ws, **kw)[0])
+        np.testing.assert_array_equal(outs[0], outs[1], err_msg=f"{shape.name} {kw}")
+
+
 def test_all_ones_mask_with_poisoned_cache_equals_dense():
     shape = W.ModelShape("ones", 2, 256, 4, 4, 12, 12, dtype="bf16", batch=2)
     ws, xt, _, _ = _inputs(shape, 40, std=0.03)
