@@ -219,9 +219,12 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
 // that sees them must assume each may write the stage being read and drains
 // every load in flight before the first fragment read of each step.
 
-// Waves per workgroup of the direct-to-LDS kernel: 256x256 tiles run eight
-// waves (2 x 4, 128 x 64 outputs each), the other tiles four (2 x 2).
-constexpr int dl_waves(int bm, int bn) { return bm * bn >= 256 * 256 ? 8 : 4; }
+// Waves per workgroup of the direct-to-LDS kernel: 256x256 and 256x192 tiles
+// run eight waves (2 x 4, 128 x 64 or 128 x 48 outputs each), the other tiles
+// four (2 x 2). 192-wide tiles fill the 256 CUs in whole waves where the
+// projection widths are multiples of 192 and not of 256 (1152, 3072, 4608,
+// 12288 columns).
+constexpr int dl_waves(int bm, int bn) { return bm * bn >= 256 * 192 ? 8 : 4; }
 
 template <int BM, int BN, int S, int EPI>
 __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmDesc g) {
@@ -409,6 +412,7 @@ struct TileCost {
 };
 constexpr TileCost kCost[] = {
     {256, 256, 2, {2.053, 3.925, 5.809, 7.690, 9.645, 12.229, 14.984, 17.740}},
+    {256, 192, 2, {1.662, 3.160, 4.742, 6.133, 7.683, 9.118, 11.446, 13.773}},
     {256, 128, 2, {1.436, 2.538, 3.676, 4.847, 6.029, 7.196, 8.445, 9.694}},
     {256, 128, 3, {1.418, 2.668, 3.898, 5.195, 6.433, 7.714, 9.015, 10.317}},
     {128, 128, 2, {0.942, 1.181, 1.820, 2.194, 2.777, 3.200, 3.716, 4.233}},
@@ -503,6 +507,7 @@ hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
     int st = force_stages > 0 ? force_stages : (g.stages > 0 ? g.stages : 2);
     st = std::max(2, std::min(st, max_stages(g.bm, g.bn)));
     if (g.bm == 256 && g.bn == 256) return launch_dl<256, 256, 2>(g, s);
+    if (g.bm == 256 && g.bn == 192) return launch_dl<256, 192, 2>(g, s);
     if (g.bm == 256 && g.bn == 128) return st == 3 ? launch_dl<256, 128, 3>(g, s) : launch_dl<256, 128, 2>(g, s);
     if (g.bm == 128 && g.bn == 128)
         return st == 4 ? launch_dl<128, 128, 4>(g, s) : st == 3 ? launch_dl<128, 128, 3>(g, s) : launch_dl<128, 128, 2>(g, s);

@@ -9,7 +9,7 @@ from paper_2505_20600_amd import maskstep as MS
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-TILES = [(256, 256), (256, 128), (128, 128), (128, 64), (64, 128), (64, 64)]
+TILES = [(256, 256), (256, 192), (256, 128), (128, 128), (128, 64), (64, 128), (64, 64)]
 
 
 def _ref(A, W, b, R, epi):
