@@ -565,31 +565,65 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
 // Combine of the key-range partials, fixed split order: range s, with running
 // max m_s, sum l_s and normalised output O_s, has weight l_s 2^((m_s - m) c)
 // (m the largest m_s, c the log2-domain scale), and the output is the
-// weighted mean of the O_s.
+// weighted mean of the O_s. One thread per 8 columns of a row (16-byte
+// vectors); with the split count NS known at compile time every partial of
+// the thread is loaded before the first is used (NS = 0: any count, loaded
+// in turn). The arithmetic and its order do not depend on NS.
+template <int NS>
 __global__ __launch_bounds__(256) void attention_combine_kernel(AttnDesc a) {
-    const long n4 = (long)a.M * a.d / 4;
+    const long n8 = (long)a.M * a.d / 8;
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n4) return;
-    const long m = i / (a.d / 4);
-    const int col = (int)(i - m * (a.d / 4)) * 4;
+    if (i >= n8) return;
+    const long m = i / (a.d / 8);
+    const int col = (int)(i - m * (a.d / 8)) * 8;
     const int head = col / a.hd;
-    float gmax = -INFINITY;
-    for (int s = 0; s < a.nsplit; ++s)
-        gmax = fmaxf(gmax, a.part_ml[2 * (((long)s * a.M + m) * a.n_heads + head)]);
-    float L = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < a.nsplit; ++s) {
-        const float* ml = a.part_ml + 2 * (((long)s * a.M + m) * a.n_heads + head);
-        const float w = fast_exp2((ml[0] - gmax) * a.scale_log2) * ml[1];
-        L += w;
-        float po[4];
-        load4<bf16_t>(a.part_o + ((long)s * a.M + m) * a.d + col, po);
+    const int ns = NS > 0 ? NS : a.nsplit;
+    auto ml_of = [&](int s) { return a.part_ml + 2 * (((long)s * a.M + m) * a.n_heads + head); };
+    auto po_of = [&](int s) { return a.part_o + ((long)s * a.M + m) * a.d + col; };
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float L = 0.f;
+    if constexpr (NS > 0) {
+        float2 ml[NS];
+        vec16 po[NS];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] += w * po[r];
+        for (int s = 0; s < NS; ++s) {
+            ml[s] = *reinterpret_cast<const float2*>(ml_of(s));
+            po[s] = ld16(po_of(s));
+        }
+        float gmax = -INFINITY;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) gmax = fmaxf(gmax, ml[s].x);
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const float w = fast_exp2((ml[s].x - gmax) * a.scale_log2) * ml[s].y;
+            L += w;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const uint32_t u = po[s].w[r >> 1];
+                acc[r] += w * __uint_as_float((r & 1) ? (u & 0xffff0000u) : (u << 16));
+            }
+        }
+    } else {
+        float gmax = -INFINITY;
+        for (int s = 0; s < ns; ++s) gmax = fmaxf(gmax, ml_of(s)[0]);
+        for (int s = 0; s < ns; ++s) {
+            const float* ml = ml_of(s);
+            const float w = fast_exp2((ml[0] - gmax) * a.scale_log2) * ml[1];
+            L += w;
+            const vec16 v = ld16(po_of(s));
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const uint32_t u = v.w[r >> 1];
+                acc[r] += w * __uint_as_float((r & 1) ? (u & 0xffff0000u) : (u << 16));
+            }
+        }
     }
     const float inv = 1.0f / L;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] *= inv;
-    store4<bf16_t>(static_cast<bf16_t*>(a.o) + m * a.d + col, acc);
+    for (int r = 0; r < 8; ++r) acc[r] *= inv;
+    bf16_t* o = static_cast<bf16_t*>(a.o) + m * a.d + col;
+    store4<bf16_t>(o, acc);
+    store4<bf16_t>(o + 4, acc + 4);
 }
 
 }  // namespace
@@ -628,8 +662,18 @@ hipError_t launch_attention(int dtype, const AttnDesc& a, hipStream_t s) {
 
 hipError_t launch_attention_combine(int dtype, const AttnDesc& a, hipStream_t s) {
     if (a.M == 0 || a.nsplit <= 1 || !attention_fast_path(dtype, a.hd)) return hipSuccess;
-    const long n4 = (long)a.M * a.d / 4;
-    hipLaunchKernelGGL(attention_combine_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, a);
+    const long n8 = (long)a.M * a.d / 8;
+    const dim3 grid((unsigned)((n8 + 255) / 256)), block(256);
+    switch (a.nsplit) {
+        case 2: hipLaunchKernelGGL(attention_combine_kernel<2>, grid, block, 0, s, a); break;
+        case 3: hipLaunchKernelGGL(attention_combine_kernel<3>, grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL(attention_combine_kernel<4>, grid, block, 0, s, a); break;
+        case 5: hipLaunchKernelGGL(attention_combine_kernel<5>, grid, block, 0, s, a); break;
+        case 6: hipLaunchKernelGGL(attention_combine_kernel<6>, grid, block, 0, s, a); break;
+        case 7: hipLaunchKernelGGL(attention_combine_kernel<7>, grid, block, 0, s, a); break;
+        case 8: hipLaunchKernelGGL(attention_combine_kernel<8>, grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL(attention_combine_kernel<0>, grid, block, 0, s, a); break;
+    }
     return hipGetLastError();
 }
 
