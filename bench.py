@@ -285,6 +285,69 @@ def fit_cost_models(key, shape, n_points, torch, MS, W):
     }
 
 
+# ----------------------------------------------------------------------------- cache-load overlap
+
+
+def _union(iv):
+    out = []
+    for a, b in sorted(iv):
+        if out and a <= out[-1][1]:
+            out[-1][1] = max(out[-1][1], b)
+        else:
+            out.append([a, b])
+    return out
+
+
+def _length(u):
+    return sum(b - a for a, b in u)
+
+
+def _intersection(u, v):
+    i = j = 0
+    tot = 0.0
+    while i < len(u) and j < len(v):
+        lo, hi = max(u[i][0], v[j][0]), min(u[i][1], v[j][1])
+        if hi > lo:
+            tot += hi - lo
+        if u[i][1] < v[j][1]:
+            i += 1
+        else:
+            j += 1
+    return tot
+
+
+def stream_overlap(intervals, steps):
+    """Per step: summed cache-load time, summed kernel time, the first layer's load, and the
+    fraction of the shorter of the two that runs concurrently with the other."""
+    copies = [(a, b) for c, a, b in intervals if c == "copy"]
+    kern = [(a, b) for c, a, b in intervals if c != "copy"]
+    uc, uk = _union(copies), _union(kern)
+    lc, lk = _length(uc), _length(uk)
+    both = _intersection(uc, uk)
+    first = (sum(b - a for a, b in copies) / len(copies)) if copies else 0.0
+    sc, sk = lc / steps, lk / steps
+    return {"sum_copy_ms": round(sc, 4), "sum_kernel_ms": round(sk, 4),
+            "first_layer_copy_ms": round(first, 4), "bound_ms": round(max(sc, sk) + first, 4),
+            "overlap": round(both / min(lc, lk), 4) if min(lc, lk) > 0 else None}
+
+
+def h2d_ceiling(torch, stream, nbytes=256 << 20):
+    h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    h.fill_(1)
+    best = 0.0
+    for _ in range(3):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        with torch.cuda.stream(stream):
+            d.copy_(h, non_blocking=True)
+        b.record(stream)
+        torch.cuda.synchronize()
+        best = max(best, nbytes / (a.elapsed_time(b) / 1e3) / 1e9)
+    return best
+
+
 # ----------------------------------------------------------------------------- CPU oracle
 
 
@@ -548,6 +611,41 @@ def main():
                      "kernel": kname, "per_launch_us": kernels[dom]["us_avg"],
                      "algorithmic_flops_per_launch": round(amount / n_launch) if kind == "mfma" else None})
 
+    # streamed caches: how much of the per-layer load stream runs under the computation
+    # (layer-wise pipelining, Sec. 3.2), against the loads issued in line (the naive loading
+    # the paper measures) and the pinned host-to-device ceiling of this GPU's link
+    stream_info = None
+    if pinned and not args.no_profile_pass:
+        stream_info = stream_overlap(MS.profiler_intervals(), args.steps)
+        row_bytes = (1 if yc_mode else 2) * shape.d_model * (2 if shape.dtype == "bf16" else 4)
+        copy_rows = [c.info().copy_rows for c in ctx]
+        copied = sum((shape.n_layers - prefix[s % args.masks]) * copy_rows[s % args.masks]
+                     for s in range(args.steps)) * row_bytes
+        needed = sum((shape.n_layers - prefix[s % args.masks]) * unmasked[s % args.masks]
+                     for s in range(args.steps)) * row_bytes
+        os.environ["MS_SERIALIZE"] = "1"
+        try:
+            ms_ser = timed(args.steps)[0] / args.steps
+        finally:
+            del os.environ["MS_SERIALIZE"]
+        ceil_gbs = h2d_ceiling(torch, copy_stream)
+        sc = stream_info["sum_copy_ms"]
+        stream_info.update({
+            "step_ms": round(ms_step, 4),
+            "profiled_step_ms": round(ms_prof / args.steps, 4),
+            "serialized_step_ms": round(ms_ser, 4),
+            "speedup_vs_serialized": round(ms_ser / ms_step, 3),
+            "copied_mb_per_step": round(copied / args.steps / 1e6, 2),
+            "needed_mb_per_step": round(needed / args.steps / 1e6, 2),
+            "h2d_gbs": round(copied / args.steps / (sc / 1e3) / 1e9, 2) if sc > 0 else None,
+            "h2d_ceiling_gbs": round(ceil_gbs, 2),
+            "note": "overlap = |copy union & kernel union| / min(|copy union|, |kernel union|) over the "
+                    "profiled pass; bound_ms = max(sum_copy_ms, sum_kernel_ms) + first_layer_copy_ms; "
+                    "serialized = loads issued on the compute stream before each block (MS_SERIALIZE=1); "
+                    "ceiling = best of three 256 MiB pinned host-to-device copies",
+        })
+        log(f"[bench] stream: {stream_info}")
+
     cpu = None
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
@@ -577,6 +675,7 @@ def main():
         "mask_step_init_ms": {"mean": round(float(np.mean(init_ms)), 3), "max": round(float(max(init_ms)), 3),
                               "note": "once per mask set (compaction + one host sync), outside the step"},
         "roofline": roof,
+        "stream": stream_info,
         "kernels": kernels,
         "cpu_baseline": cpu,
     }

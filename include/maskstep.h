@@ -136,6 +136,10 @@ typedef struct {
     int32_t n_qtiles;    /* attention query tiles */
     int32_t text_rows;   /* packed rows that use the text weight set */
     int32_t dense_prefix;/* blocks computed over every token (mask_step_set_dense_prefix) */
+    int32_t copy_spans;  /* host-to-device copies one cached block's load issues */
+    int64_t copy_rows;   /* image rows those copies move (unmasked runs merged across short
+                            masked gaps, so >= the unmasked rows of the requests that
+                            recompute anything); bytes = rows x 2 d x elt (K/V) or d x elt (Y) */
 } ms_step_info;
 
 /* Bytes of device workspace a step over `batch` requests needs (worst case,
@@ -313,11 +317,22 @@ typedef enum {
 ms_status mask_profiler_start(uint32_t class_mask, int32_t capacity);
 ms_status mask_profiler_stop(double* total_ms, int64_t* launches, int64_t* dropped);
 
+/* The launches recorded between the last start and stop, in recording order:
+ * kernel class, and start and end in ms relative to the first recorded start
+ * (one timeline across the compute and copy streams, from the same timing
+ * events). Up to `capacity` entries are written; *count receives the number
+ * recorded. Valid until the next mask_profiler_start. Used to measure how much
+ * of the cache-load stream (Sec. 3.2, layer-wise pipelining) runs under the
+ * computation. */
+ms_status mask_profiler_intervals(int32_t* cls, double* start_ms, double* end_ms, int32_t capacity,
+                                  int32_t* count);
+
 /* Message of the calling thread's last error ("" if none). */
 const char* mask_last_error(void);
 
-/* Version of this interface: 3 (2 added Y caching's kinds and calls, 3 the
- * cost-model and routing calls). */
+/* Version of this interface: 4 (2 added Y caching's kinds and calls, 3 the
+ * cost-model and routing calls, 4 the copy figures of ms_step_info and
+ * mask_profiler_intervals). */
 int32_t mask_abi_version(void);
 
 #ifdef __cplusplus

@@ -20,7 +20,7 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 3;
+constexpr int32_t kAbiVersion = 4;
 constexpr int kMaxBatch = 64;
 // Host-to-device copy spans are merged across masked gaps of at most this
 // many bytes: a gap costs less PCIe time than one more copy submission.
@@ -150,6 +150,9 @@ struct Profiler {
     int64_t dropped = 0;
     std::vector<hipEvent_t> pool;   // 2 per recorded launch
     std::vector<int> cls;
+    // intervals of the last stopped run: class, start, end (ms from the first start)
+    std::vector<int> last_cls;
+    std::vector<double> last_t0, last_t1;
 };
 Profiler g_prof;
 
@@ -635,6 +638,10 @@ ms_status mask_step_get_info(const ms_step* s, ms_step_info* info) {
     info->n_qtiles = s->mp.n_qtiles;
     info->text_rows = s->mp.text_rows;
     info->dense_prefix = s->dense_prefix;
+    info->copy_spans = (int32_t)s->spans.size();
+    int64_t rows = 0;
+    for (const Span& sp : s->spans) rows += sp.n1 - sp.n0;
+    info->copy_rows = rows;
     return ok();
 }
 
@@ -1125,12 +1132,20 @@ ms_status mask_profiler_stop(double* total_ms, int64_t* launches, int64_t* dropp
     g_prof.on.store(false);
     std::vector<double> tot(MS_K_COUNT, 0.0);
     std::vector<int64_t> cnt(MS_K_COUNT, 0);
+    g_prof.last_cls.assign(g_prof.used, 0);
+    g_prof.last_t0.assign(g_prof.used, 0.0);
+    g_prof.last_t1.assign(g_prof.used, 0.0);
     for (int i = 0; i < g_prof.used; ++i) {
         MS_HIP(hipEventSynchronize(g_prof.pool[2 * i + 1]));
-        float ms = 0.f;
+        float ms = 0.f, a = 0.f, b = 0.f;
         MS_HIP(hipEventElapsedTime(&ms, g_prof.pool[2 * i], g_prof.pool[2 * i + 1]));
+        MS_HIP(hipEventElapsedTime(&a, g_prof.pool[0], g_prof.pool[2 * i]));
+        MS_HIP(hipEventElapsedTime(&b, g_prof.pool[0], g_prof.pool[2 * i + 1]));
         tot[g_prof.cls[i]] += ms;
         cnt[g_prof.cls[i]] += 1;
+        g_prof.last_cls[i] = g_prof.cls[i];
+        g_prof.last_t0[i] = a;
+        g_prof.last_t1[i] = b;
     }
     for (int c = 0; c < MS_K_COUNT; ++c) {
         if (total_ms) total_ms[c] = tot[c];
@@ -1138,6 +1153,20 @@ ms_status mask_profiler_stop(double* total_ms, int64_t* launches, int64_t* dropp
     }
     if (dropped) *dropped = g_prof.dropped;
     g_prof.used = 0;
+    return ok();
+}
+
+ms_status mask_profiler_intervals(int32_t* cls, double* start_ms, double* end_ms, int32_t capacity,
+                                  int32_t* count) {
+    if (capacity < 0 || (capacity > 0 && (!cls || !start_ms || !end_ms))) return fail(MS_EINVAL, "NULL output");
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    const int n = (int)g_prof.last_cls.size();
+    for (int i = 0; i < n && i < capacity; ++i) {
+        cls[i] = g_prof.last_cls[i];
+        start_ms[i] = g_prof.last_t0[i];
+        end_ms[i] = g_prof.last_t1[i];
+    }
+    if (count) *count = n;
     return ok();
 }
 

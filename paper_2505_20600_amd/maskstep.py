@@ -52,7 +52,8 @@ class CostModel(C.Structure):
 
 class StepInfo(C.Structure):
     _fields_ = [("batch", C.c_int32), ("rows", C.c_int32), ("n_segments", C.c_int32),
-                ("n_qtiles", C.c_int32), ("text_rows", C.c_int32), ("dense_prefix", C.c_int32)]
+                ("n_qtiles", C.c_int32), ("text_rows", C.c_int32), ("dense_prefix", C.c_int32),
+                ("copy_spans", C.c_int32), ("copy_rows", C.c_int64)]
 
 
 class MaskStepError(RuntimeError):
@@ -93,6 +94,8 @@ def load() -> C.CDLL:
             "mask_profiler_start": (i32, [C.c_uint32, i32]),
             "ms_linear": (i32, [i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, sz, vp]),
             "mask_profiler_stop": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
+            "mask_profiler_intervals": (i32, [C.POINTER(C.c_int32), C.POINTER(C.c_double), C.POINTER(C.c_double),
+                                              i32, C.POINTER(C.c_int32)]),
             "mask_fit_linear": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_double), i32, C.POINTER(C.c_double),
                                       C.POINTER(C.c_double), C.POINTER(C.c_double)]),
             "mask_batch_cost": (i32, [C.POINTER(ModelDesc), C.POINTER(CostModel), C.POINTER(i32), i32,
@@ -113,7 +116,7 @@ EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask
             "mask_scatter_rows", "cache_prefetch_layer", "cache_prefetch_inputs", "mask_recompute_kv",
             "mask_stack_forward", "mask_step_destroy",
             "mask_step_set_dense_prefix", "mask_plan_dense_prefix",
-            "mask_profiler_start", "mask_profiler_stop", "ms_linear",
+            "mask_profiler_start", "mask_profiler_stop", "mask_profiler_intervals", "ms_linear",
             "mask_fit_linear", "mask_batch_cost", "mask_route_request")
 
 MS_EPI_BIAS, MS_EPI_BIAS_RESID, MS_EPI_BIAS_GELU = 0, 1, 2
@@ -150,6 +153,18 @@ def profiler_stop() -> dict:
     out = {c: (ms[i], cnt[i]) for i, c in enumerate(KERNEL_CLASSES) if cnt[i]}
     out["_dropped"] = dropped.value
     return out
+
+
+def profiler_intervals() -> list:
+    """[(class, start_ms, end_ms)] of the launches of the last profiler_start()..profiler_stop()
+    run, on one timeline across streams (ms from the first recorded start)."""
+    lib = load()
+    n = C.c_int32()
+    _check(lib.mask_profiler_intervals(None, None, None, 0, C.byref(n)))
+    k = n.value
+    cls, t0, t1 = (C.c_int32 * max(k, 1))(), (C.c_double * max(k, 1))(), (C.c_double * max(k, 1))()
+    _check(lib.mask_profiler_intervals(cls, t0, t1, k, C.byref(n)))
+    return [(KERNEL_CLASSES[cls[i]], t0[i], t1[i]) for i in range(min(k, n.value))]
 
 
 def _check(status: int):

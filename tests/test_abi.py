@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_abi_version():
-    assert MS.load().mask_abi_version() == 3
+    assert MS.load().mask_abi_version() == 4
 
 
 def _desc(**kw):
