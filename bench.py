@@ -63,6 +63,9 @@ def parse():
                         "per-block costs) or a fixed count")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device copy (HBM counter calibration) and exit")
+    p.add_argument("--ceilings", action="store_true",
+                   help="only measure this GPU's ceilings (a library bf16 GEMM at 8192^3, a device copy, "
+                        "a pinned host-to-device copy), print one JSON line and exit")
     p.add_argument("--fit", type=int, default=0, metavar="K",
                    help="only fit the per-block cost models of Sec. 4.3 on K measured random batches of "
                         "the workload (compute vs FLOPs, cache load vs bytes), run the routing simulation "
@@ -331,6 +334,42 @@ def stream_overlap(intervals, steps):
             "overlap": round(both / min(lc, lk), 4) if min(lc, lk) > 0 else None}
 
 
+def measure_ceilings(torch):
+    """Reference rates of this GPU: hipBLASLt (torch.matmul) bf16 at 8192^3, a 1 GiB device
+    copy (read + write bytes), and 256 MiB pinned host-to-device copies."""
+    dev = "cuda:0"
+
+    def best_ms(fn, reps=5):
+        fn()
+        best = 1e30
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            best = min(best, a.elapsed_time(b))
+        return best
+
+    n = 8192
+    A = torch.randn(n, n, device=dev).bfloat16()
+    Bm = torch.randn(n, n, device=dev).bfloat16()
+    C = torch.empty(n, n, device=dev, dtype=torch.bfloat16)
+    t_mm = best_ms(lambda: torch.matmul(A, Bm, out=C))
+    del A, Bm, C
+    nb = 1 << 30
+    x = torch.empty(nb, dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+    x.fill_(1)
+    t_cp = best_ms(lambda: y.copy_(x))
+    del x, y
+    return {"gemm_bf16_8192_tflops": round(2.0 * n ** 3 / (t_mm / 1e3) / 1e12, 1),
+            "d2d_copy_gbs": round(2.0 * nb / (t_cp / 1e3) / 1e9, 1),
+            "h2d_pinned_gbs": round(h2d_ceiling(torch, torch.cuda.current_stream()), 2),
+            "note": "best of 5 (GEMM, copy) or 3 (H2D) timed runs; copy counts bytes read + written"}
+
+
 def h2d_ceiling(torch, stream, nbytes=256 << 20):
     h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
     d = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
@@ -425,6 +464,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "launches": 3}))
+        return
+
+    if args.ceilings:
+        print(json.dumps(measure_ceilings(torch)), flush=True)
         return
 
     key = args.workload
@@ -556,6 +599,7 @@ def main():
         per_mask.setdefault(s % args.masks, []).append(t)
     per_ratio = sorted([[round(ratios[i], 4), int(Ms[i]), round(float(np.median(v)), 4), prefix[i]]
                         for i, v in per_mask.items()])
+    q10, q50, q90 = (round(float(v), 4) for v in np.percentile(step_ms, [10, 50, 90]))
 
     # profiled pass: per-kernel event timing over a second timed region
     kernels, roof = {}, None
@@ -660,6 +704,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "step_ms_p10_p50_p90": [q10, q50, q90],
+        "effective_tokens_per_s": round(shape.batch * shape.n_tokens / (ms_step / 1e3), 1),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
