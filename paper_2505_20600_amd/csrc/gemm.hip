@@ -440,6 +440,10 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats) 
     if (dtype != kBF16) return p;   // fp32 path: one tile shape
     const int steps = K / 64;
     double best = 1e30;
+    static const double split_scale = [] {   // tuning knob MS_GEMM_SPLIT_COST: scales the split-K pass cost
+        const char* v = std::getenv("MS_GEMM_SPLIT_COST");
+        return v ? std::max(0.0, std::atof(v)) : 1.0;
+    }();
     for (const TileCost& c : kCost) {
         const long grp = (long)((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn);
         for (int ks = 1; ks <= 8 && ks <= steps; ++ks) {
@@ -448,7 +452,7 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats) 
             const long n = (grp * ks + kCUs - 1) / kCUs;
             double us = per * step_us(c, n);
             // partial sums: ks float planes read, one bf16 plane written, ~4 TB/s, + a launch
-            if (ks > 1) us += 2.0 + ((double)ks * 4 + 2) * M * N / 4.0e6;
+            if (ks > 1) us += split_scale * (2.0 + ((double)ks * 4 + 2) * M * N / 4.0e6);
             if (us < best * 0.97) {   // prefer the earlier (larger, unsplit) choice on near-ties
                 best = us;
                 p = GemmPlan{c.bm, c.bn, ks, c.stages};
