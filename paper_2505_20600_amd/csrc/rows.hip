@@ -81,15 +81,14 @@ __device__ __forceinline__ float vec_elt(const vec16& v, int e) {
 // Normalises one row held by a wave: lane holds the 16-byte vectors c = lane
 // + 64 i of the row (values v as float, affine parameters gv, bv), mean and
 // variance in two passes, y = (v - mean) / sqrt(var + eps) * gamma + beta.
-template <typename T>
-__device__ __forceinline__ void ln_row(float (&v)[kLnMaxVecPerLane][16 / sizeof(T)],
-                                       const vec16 (&gv)[kLnMaxVecPerLane],
-                                       const vec16 (&bv)[kLnMaxVecPerLane], int lane, int nvec, int d,
-                                       float eps, T* __restrict__ yr) {
+template <typename T, int NV>
+__device__ __forceinline__ void ln_row(float (&v)[NV][16 / sizeof(T)], const vec16 (&gv)[NV],
+                                       const vec16 (&bv)[NV], int lane, int nvec, int d, float eps,
+                                       T* __restrict__ yr) {
     constexpr int V = 16 / sizeof(T);
     float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+    for (int i = 0; i < NV; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
@@ -99,7 +98,7 @@ __device__ __forceinline__ void ln_row(float (&v)[kLnMaxVecPerLane][16 / sizeof(
     const float mean = wave_sum(s) / d;
     float q = 0.f;
 #pragma unroll
-    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+    for (int i = 0; i < NV; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
@@ -111,7 +110,7 @@ __device__ __forceinline__ void ln_row(float (&v)[kLnMaxVecPerLane][16 / sizeof(
     }
     const float rstd = 1.0f / sqrtf(wave_sum(q) / d + eps);
 #pragma unroll
-    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+    for (int i = 0; i < NV; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
@@ -126,7 +125,9 @@ __device__ __forceinline__ void ln_row(float (&v)[kLnMaxVecPerLane][16 / sizeof(
     }
 }
 
-template <typename T>
+// NV: 16-byte vectors per lane (ceil(d / (64 V))), so the row's registers
+// match the width.
+template <typename T, int NV>
 __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
     const T* __restrict__ x, const T* __restrict__ g0, const T* __restrict__ b0,
     const T* __restrict__ g1, const T* __restrict__ b1, int m_split, T* __restrict__ y, int M,
@@ -139,9 +140,9 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
     const T* bet = row < m_split ? b1 : b0;
     const int nvec = d / V;
     const T* xr = x + (long)(idx ? idx[row] : row) * d;
-    vec16 xv[kLnMaxVecPerLane], gv[kLnMaxVecPerLane], bv[kLnMaxVecPerLane];
+    vec16 xv[NV], gv[NV], bv[NV];
 #pragma unroll
-    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+    for (int i = 0; i < NV; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
             xv[i] = ld16(xr + c * V);
@@ -149,16 +150,16 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
             bv[i] = ld16(bet + c * V);
         }
     }
-    float v[kLnMaxVecPerLane][V];
+    float v[NV][V];
 #pragma unroll
-    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+    for (int i = 0; i < NV; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
             for (int e = 0; e < V; ++e) v[i][e] = vec_elt<T>(xv[i], e);
         }
     }
-    ln_row<T>(v, gv, bv, lane, nvec, d, eps, y + (long)row * d);
+    ln_row<T, NV>(v, gv, bv, lane, nvec, d, eps, y + (long)row * d);
 }
 
 // Split-K sum of a residual projection followed by the LayerNorm that reads
@@ -169,7 +170,7 @@ __global__ __launch_bounds__(kLnWaves * kWave) void layernorm_kernel(
 // arithmetic and its order are those of the separate split-K sum and
 // LayerNorm kernels, so both outputs equal theirs bit for bit; the residual
 // row is not read back and one launch is saved.
-template <typename T, int KS>
+template <typename T, int KS, int NV>
 __global__ __launch_bounds__(kLnWaves * kWave) void reduce_layernorm_kernel(
     const float* __restrict__ part, const T* __restrict__ bias, const T* __restrict__ R,
     int ldr, T* __restrict__ C, int ldc, const T* __restrict__ gam, const T* __restrict__ bet,
@@ -179,9 +180,9 @@ __global__ __launch_bounds__(kLnWaves * kWave) void reduce_layernorm_kernel(
     const int row = blockIdx.x * kLnWaves + threadIdx.x / kWave;
     if (row >= M) return;
     const int nvec = d / V;
-    vec16 rv[kLnMaxVecPerLane], gv[kLnMaxVecPerLane], bv[kLnMaxVecPerLane];
+    vec16 rv[NV], gv[NV], bv[NV];
 #pragma unroll
-    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+    for (int i = 0; i < NV; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
             rv[i] = ld16(R + (long)row * ldr + c * V);
@@ -191,11 +192,11 @@ __global__ __launch_bounds__(kLnWaves * kWave) void reduce_layernorm_kernel(
     }
     // the KS partials of a vector are loaded together (KS is a compile-time
     // count so that they are all in flight), then summed in split order
-    float v[kLnMaxVecPerLane][V];
+    float v[NV][V];
     const float* pr = part + (long)row * d;
     const long plane = (long)M * d;
 #pragma unroll
-    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+    for (int i = 0; i < NV; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(kLnWaves * kWave) void reduce_layernorm_kernel(
         }
     }
 #pragma unroll
-    for (int i = 0; i < kLnMaxVecPerLane; ++i) {
+    for (int i = 0; i < NV; ++i) {
         const int c = lane + i * kWave;
         if (c < nvec) {
 #pragma unroll
@@ -242,20 +243,61 @@ __global__ __launch_bounds__(kLnWaves * kWave) void reduce_layernorm_kernel(
             }
         }
     }
-    ln_row<T>(v, gv, bv, lane, nvec, d, eps, y + (long)row * ldy);
+    ln_row<T, NV>(v, gv, bv, lane, nvec, d, eps, y + (long)row * ldy);
 }
 
 constexpr int kMaxReduceSplit = 8;
+
+// Vectors per lane of a d-wide row (1..kLnMaxVecPerLane; d is validated at
+// model creation).
+template <typename T>
+int ln_nv(int d) {
+    constexpr int V = 16 / sizeof(T);
+    return (d / V + kWave - 1) / kWave;
+}
+
+template <typename T, int KS, int NV>
+hipError_t reduce_ln_launch_nv(const float* part, const void* bias, const void* R, int ldr, void* C, int ldc,
+                               const void* g, const void* b, void* y, int ldy, int M, int d, float eps,
+                               hipStream_t s) {
+    dim3 grid((M + kLnWaves - 1) / kLnWaves), block(kLnWaves * kWave);
+    hipLaunchKernelGGL((reduce_layernorm_kernel<T, KS, NV>), grid, block, 0, s, part,
+                       static_cast<const T*>(bias), static_cast<const T*>(R), ldr, static_cast<T*>(C), ldc,
+                       static_cast<const T*>(g), static_cast<const T*>(b), static_cast<T*>(y), ldy, M, d, eps);
+    return hipGetLastError();
+}
 
 template <typename T, int KS>
 hipError_t reduce_ln_launch(const float* part, const void* bias, const void* R, int ldr, void* C, int ldc,
                             const void* g, const void* b, void* y, int ldy, int M, int d, float eps,
                             hipStream_t s) {
+    switch (ln_nv<T>(d)) {
+#define MS_NV(n) case n: return reduce_ln_launch_nv<T, KS, n>(part, bias, R, ldr, C, ldc, g, b, y, ldy, M, d, eps, s);
+        MS_NV(1) MS_NV(2) MS_NV(3) MS_NV(4) MS_NV(5) MS_NV(6) MS_NV(7) MS_NV(8)
+#undef MS_NV
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <typename T, int NV>
+hipError_t ln_launch_nv(const void* x, const void* g0, const void* b0, const void* g1, const void* b1,
+                        int m_split, void* y, int M, int d, float eps, hipStream_t s, const int32_t* idx) {
     dim3 grid((M + kLnWaves - 1) / kLnWaves), block(kLnWaves * kWave);
-    hipLaunchKernelGGL((reduce_layernorm_kernel<T, KS>), grid, block, 0, s, part,
-                       static_cast<const T*>(bias), static_cast<const T*>(R), ldr, static_cast<T*>(C), ldc,
-                       static_cast<const T*>(g), static_cast<const T*>(b), static_cast<T*>(y), ldy, M, d, eps);
+    hipLaunchKernelGGL((layernorm_kernel<T, NV>), grid, block, 0, s, static_cast<const T*>(x),
+                       static_cast<const T*>(g0), static_cast<const T*>(b0), static_cast<const T*>(g1),
+                       static_cast<const T*>(b1), m_split, static_cast<T*>(y), M, d, eps, idx);
     return hipGetLastError();
+}
+
+template <typename T>
+hipError_t ln_launch(const void* x, const void* g0, const void* b0, const void* g1, const void* b1,
+                     int m_split, void* y, int M, int d, float eps, hipStream_t s, const int32_t* idx) {
+    switch (ln_nv<T>(d)) {
+#define MS_NV(n) case n: return ln_launch_nv<T, n>(x, g0, b0, g1, b1, m_split, y, M, d, eps, s, idx);
+        MS_NV(1) MS_NV(2) MS_NV(3) MS_NV(4) MS_NV(5) MS_NV(6) MS_NV(7) MS_NV(8)
+#undef MS_NV
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <typename T>
@@ -315,21 +357,8 @@ hipError_t launch_layernorm(int dtype, const void* x, const void* g0, const void
                             const void* g1, const void* b1, int m_split, void* y, int M, int d,
                             float eps, hipStream_t s, const int32_t* idx) {
     if (M == 0) return hipSuccess;
-    dim3 grid((M + kLnWaves - 1) / kLnWaves), block(kLnWaves * kWave);
-    if (dtype == kBF16) {
-        hipLaunchKernelGGL(layernorm_kernel<bf16_t>, grid, block, 0, s,
-                           static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(g0),
-                           static_cast<const bf16_t*>(b0), static_cast<const bf16_t*>(g1),
-                           static_cast<const bf16_t*>(b1), m_split, static_cast<bf16_t*>(y), M, d,
-                           eps, idx);
-    } else {
-        hipLaunchKernelGGL(layernorm_kernel<float>, grid, block, 0, s,
-                           static_cast<const float*>(x), static_cast<const float*>(g0),
-                           static_cast<const float*>(b0), static_cast<const float*>(g1),
-                           static_cast<const float*>(b1), m_split, static_cast<float*>(y), M, d,
-                           eps, idx);
-    }
-    return hipGetLastError();
+    return dtype == kBF16 ? ln_launch<bf16_t>(x, g0, b0, g1, b1, m_split, y, M, d, eps, s, idx)
+                          : ln_launch<float>(x, g0, b0, g1, b1, m_split, y, M, d, eps, s, idx);
 }
 
 hipError_t launch_reduce_layernorm(int dtype, const float* part, int ksplit, const void* bias,
