@@ -604,17 +604,36 @@ __global__ __launch_bounds__(256) void attention_combine_kernel(AttnDesc a) {
             }
         }
     } else {
+        // any split count: chunks of 8 splits, each chunk's loads issued together
+        constexpr int CH = 8;
         float gmax = -INFINITY;
-        for (int s = 0; s < ns; ++s) gmax = fmaxf(gmax, ml_of(s)[0]);
-        for (int s = 0; s < ns; ++s) {
-            const float* ml = ml_of(s);
-            const float w = fast_exp2((ml[0] - gmax) * a.scale_log2) * ml[1];
-            L += w;
-            const vec16 v = ld16(po_of(s));
+        for (int s0 = 0; s0 < ns; s0 += CH) {
+            float mv[CH];
 #pragma unroll
-            for (int r = 0; r < 8; ++r) {
-                const uint32_t u = v.w[r >> 1];
-                acc[r] += w * __uint_as_float((r & 1) ? (u & 0xffff0000u) : (u << 16));
+            for (int j = 0; j < CH; ++j) mv[j] = s0 + j < ns ? ml_of(s0 + j)[0] : -INFINITY;
+#pragma unroll
+            for (int j = 0; j < CH; ++j) gmax = fmaxf(gmax, mv[j]);
+        }
+        for (int s0 = 0; s0 < ns; s0 += CH) {
+            float2 ml[CH];
+            vec16 po[CH];
+#pragma unroll
+            for (int j = 0; j < CH; ++j) {
+                if (s0 + j < ns) {
+                    ml[j] = *reinterpret_cast<const float2*>(ml_of(s0 + j));
+                    po[j] = ld16(po_of(s0 + j));
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < CH; ++j) {
+                if (s0 + j >= ns) break;
+                const float w = fast_exp2((ml[j].x - gmax) * a.scale_log2) * ml[j].y;
+                L += w;
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const uint32_t u = po[j].w[r >> 1];
+                    acc[r] += w * __uint_as_float((r & 1) ? (u & 0xffff0000u) : (u << 16));
+                }
             }
         }
     }
