@@ -240,8 +240,12 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
     constexpr int SM = BM / WM / 16;            // 16-row MFMA blocks per wave (rows m)
     constexpr int SN = BN / WN / 16;            // 16-col MFMA blocks per wave (cols n)
     static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "load split");
-    __shared__ __attribute__((aligned(1024))) bf16_t sA[S][BM * ROWE];
-    __shared__ __attribute__((aligned(1024))) bf16_t sW[S][BN * ROWE];
+    // S activation stages, then S weight stages; after the main loop the
+    // same LDS stages the output tile when its float32 form fits
+    __shared__ __attribute__((aligned(1024))) bf16_t smem[S * (BM + BN) * ROWE];
+    bf16_t* const sAb = smem;
+    bf16_t* const sWb = smem + S * BM * ROWE;
+    constexpr bool kStagedOut = S * (BM + BN) * ROWE * 2 >= BM * BN * 4;
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
@@ -270,7 +274,7 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
         const int c = (lane % 8) ^ ((rloc >> 1) & 7);
         if (isA) goff[i] = min(m0 + rloc, M - 1) * g.lda + c * 8;
         else goff[i] = min(n0 + rloc, N - 1) * K + c * 8;
-        ldst[i] = isA ? lds_addr(&sA[0][blk * 512]) : lds_addr(&sW[0][(blk - BM / 8) * 512]);
+        ldst[i] = isA ? lds_addr(sAb + blk * 512) : lds_addr(sWb + (blk - BM / 8) * 512);
     }
     constexpr uint32_t kStageA = BM * ROWE * 2, kStageW = BN * ROWE * 2;   // bytes
     auto issue = [&](int kt, int st) {
@@ -310,30 +314,67 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
             frag_t fa[SM];
 #pragma unroll
             for (int j = 0; j < SM; ++j)
-                fa[j] = *reinterpret_cast<const frag_t*>(&sA[st][(wm * (BM / WM) + j * 16 + lane % 16) * ROWE + ch]);
+                fa[j] = *reinterpret_cast<const frag_t*>(sAb + st * BM * ROWE + (wm * (BM / WM) + j * 16 + lane % 16) * ROWE + ch);
 #pragma unroll
             for (int i = 0; i < SN; ++i) {
-                const frag_t fw = *reinterpret_cast<const frag_t*>(&sW[st][(wn * (BN / WN) + i * 16 + lane % 16) * ROWE + ch]);
+                const frag_t fw = *reinterpret_cast<const frag_t*>(sWb + st * BN * ROWE + (wn * (BN / WN) + i * 16 + lane % 16) * ROWE + ch);
 #pragma unroll
                 for (int j = 0; j < SM; ++j) acc[i][j] = E::mma(fw, fa[j], acc[i][j]);
             }
         }
     }
 
+    // staged unless a bias + residual epilogue writes its tile directly (its
+    // residual reads make the staged form no faster)
+    if (kStagedOut && (EPI != kEpiBiasResid || g.ksplit > 1)) {
+        // Output through LDS: each lane holds 4 columns of 16 rows per MFMA
+        // block, so direct stores write 32-byte pieces of 16 rows; staged,
+        // consecutive lanes write consecutive 4-column groups of one row.
+        // Float32 in LDS, so the epilogue arithmetic is unchanged. The
+        // 16-byte chunks of a staged row are XOR-swizzled by (row & 15), so
+        // both the 16-row writes and the row-wise reads are conflict-free.
+        constexpr int CPR = BN / 4;   // 16-byte chunks per staged row
+        float* const sc = reinterpret_cast<float*>(smem);
+        __syncthreads();   // every wave is past its last operand read
 #pragma unroll
-    for (int i = 0; i < SN; ++i) {
-        const int n = n0 + wn * (BN / WN) + i * 16 + grp * 4;
-        if (n >= N) continue;
+        for (int i = 0; i < SN; ++i) {
+            const int nl = wn * (BN / WN) + i * 16 + grp * 4;
 #pragma unroll
-        for (int j = 0; j < SM; ++j) {
-            const int m = m0 + wm * (BM / WM) + j * 16 + lane % 16;
-            if (m >= M) continue;
-            float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+            for (int j = 0; j < SM; ++j) {
+                const int ml = wm * (BM / WM) + j * 16 + lane % 16;
+                *reinterpret_cast<float4*>(sc + ml * BN + (((nl / 4) ^ (ml & 15)) * 4)) =
+                    make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
+        }
+        __syncthreads();
+        for (int idx = tid; idx < BM * CPR; idx += NW * kWave) {
+            const int ml = idx / CPR, c = idx % CPR;
+            const int m = m0 + ml, n = n0 + c * 4;
+            if (m >= M || n >= N) continue;
+            const float4 t = *reinterpret_cast<const float4*>(sc + ml * BN + ((c ^ (ml & 15)) * 4));
             if (g.ksplit == 1) {
+                float v[4] = {t.x, t.y, t.z, t.w};
                 epilogue_store<bf16_t, EPI>(g, m, n, v);
             } else {
-                *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) =
-                    make_float4(v[0], v[1], v[2], v[3]);
+                *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) = t;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < SN; ++i) {
+            const int n = n0 + wn * (BN / WN) + i * 16 + grp * 4;
+            if (n >= N) continue;
+#pragma unroll
+            for (int j = 0; j < SM; ++j) {
+                const int m = m0 + wm * (BM / WM) + j * 16 + lane % 16;
+                if (m >= M) continue;
+                float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+                if (g.ksplit == 1) {
+                    epilogue_store<bf16_t, EPI>(g, m, n, v);
+                } else {
+                    *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) =
+                        make_float4(v[0], v[1], v[2], v[3]);
+                }
             }
         }
     }
