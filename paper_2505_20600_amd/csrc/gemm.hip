@@ -245,7 +245,11 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
     __shared__ __attribute__((aligned(1024))) bf16_t smem[S * (BM + BN) * ROWE];
     bf16_t* const sAb = smem;
     bf16_t* const sWb = smem + S * BM * ROWE;
-    constexpr bool kStagedOut = S * (BM + BN) * ROWE * 2 >= BM * BN * 4;
+    // output staging passes: the float32 tile in one pass, or in two halves
+    // of its rows (the two wave rows) when only half fits
+    constexpr int kLdsBytes = S * (BM + BN) * ROWE * 2;
+    constexpr int kOutPasses = kLdsBytes >= BM * BN * 4 ? 1 : 2;
+    static_assert(kLdsBytes * 2 >= BM * BN * 4 && WM == 2, "output staging");
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
@@ -324,42 +328,17 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
         }
     }
 
-    // staged unless a bias + residual epilogue writes its tile directly (its
-    // residual reads make the staged form no faster)
-    if (kStagedOut && (EPI != kEpiBiasResid || g.ksplit > 1)) {
-        // Output through LDS: each lane holds 4 columns of 16 rows per MFMA
-        // block, so direct stores write 32-byte pieces of 16 rows; staged,
-        // consecutive lanes write consecutive 4-column groups of one row.
-        // Float32 in LDS, so the epilogue arithmetic is unchanged. The
-        // 16-byte chunks of a staged row are XOR-swizzled by (row & 15), so
-        // both the 16-row writes and the row-wise reads are conflict-free.
-        constexpr int CPR = BN / 4;   // 16-byte chunks per staged row
-        float* const sc = reinterpret_cast<float*>(smem);
-        __syncthreads();   // every wave is past its last operand read
-#pragma unroll
-        for (int i = 0; i < SN; ++i) {
-            const int nl = wn * (BN / WN) + i * 16 + grp * 4;
-#pragma unroll
-            for (int j = 0; j < SM; ++j) {
-                const int ml = wm * (BM / WM) + j * 16 + lane % 16;
-                *reinterpret_cast<float4*>(sc + ml * BN + (((nl / 4) ^ (ml & 15)) * 4)) =
-                    make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-            }
-        }
-        __syncthreads();
-        for (int idx = tid; idx < BM * CPR; idx += NW * kWave) {
-            const int ml = idx / CPR, c = idx % CPR;
-            const int m = m0 + ml, n = n0 + c * 4;
-            if (m >= M || n >= N) continue;
-            const float4 t = *reinterpret_cast<const float4*>(sc + ml * BN + ((c ^ (ml & 15)) * 4));
-            if (g.ksplit == 1) {
-                float v[4] = {t.x, t.y, t.z, t.w};
-                epilogue_store<bf16_t, EPI>(g, m, n, v);
-            } else {
-                *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) = t;
-            }
-        }
-    } else {
+    // Output through LDS: an MFMA block leaves each lane 4 columns of 16 rows,
+    // so direct stores write 32-byte pieces of 16 rows; staged, consecutive
+    // lanes write consecutive 4-column groups of one row. Float32 in LDS, so
+    // the epilogue arithmetic is unchanged. The 16-byte chunks of a staged
+    // row are XOR-swizzled by (row & 15), so both the 16-row writes and the
+    // row-wise reads are conflict-free. Tiles too large for one pass stage
+    // the rows of one wave row (BM / 2) at a time.
+    // Measured per epilogue (c2 / c4 / c5): staging pays for the QKV split
+    // (-7..-13%, its K/V rows are scattered) and the split-K partials; for
+    // the residual and GELU epilogues the direct stores are as fast or faster.
+    if (EPI != kEpiQKV && EPI != kEpiBias && g.ksplit == 1) {
 #pragma unroll
         for (int i = 0; i < SN; ++i) {
             const int n = n0 + wn * (BN / WN) + i * 16 + grp * 4;
@@ -369,12 +348,40 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
                 const int m = m0 + wm * (BM / WM) + j * 16 + lane % 16;
                 if (m >= M) continue;
                 float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-                if (g.ksplit == 1) {
-                    epilogue_store<bf16_t, EPI>(g, m, n, v);
-                } else {
-                    *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) =
-                        make_float4(v[0], v[1], v[2], v[3]);
+                epilogue_store<bf16_t, EPI>(g, m, n, v);
+            }
+        }
+        return;
+    }
+    constexpr int CPR = BN / 4;               // 16-byte chunks per staged row
+    constexpr int PR = BM / kOutPasses;       // rows per pass
+    float* const sc = reinterpret_cast<float*>(smem);
+#pragma unroll
+    for (int pass = 0; pass < kOutPasses; ++pass) {
+        __syncthreads();   // operand reads (or the previous pass's reads) are done
+        if (kOutPasses == 1 || wm == pass) {
+#pragma unroll
+            for (int i = 0; i < SN; ++i) {
+                const int nl = wn * (BN / WN) + i * 16 + grp * 4;
+#pragma unroll
+                for (int j = 0; j < SM; ++j) {
+                    const int ml = wm * (BM / WM) + j * 16 + lane % 16 - pass * PR;
+                    *reinterpret_cast<float4*>(sc + ml * BN + (((nl / 4) ^ (ml & 15)) * 4)) =
+                        make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
                 }
+            }
+        }
+        __syncthreads();
+        for (int idx = tid; idx < PR * CPR; idx += NW * kWave) {
+            const int ml = idx / CPR, c = idx % CPR;
+            const int m = m0 + pass * PR + ml, n = n0 + c * 4;
+            if (m >= M || n >= N) continue;
+            const float4 t = *reinterpret_cast<const float4*>(sc + ml * BN + ((c ^ (ml & 15)) * 4));
+            if (g.ksplit == 1) {
+                float v[4] = {t.x, t.y, t.z, t.w};
+                epilogue_store<bf16_t, EPI>(g, m, n, v);
+            } else {
+                *reinterpret_cast<float4*>(g.part + ((long)kz * M + m) * N + n) = t;
             }
         }
     }
