@@ -257,28 +257,38 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
     const int wm = wave % WM, wn = wave / WM;
     const int M = g.M, N = g.N, K = g.K;
     const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-    const int lb = xcd_logical_block(blockIdx.x, tiles_m * tiles_n * g.ksplit);
-    const TileIdx ti = tile_of(lb, tiles_m, tiles_n, BM, BN, g.group_m);
-    const int kz = ti.kz, m0 = ti.m0, n0 = ti.n0;
-    const int kbeg = kz * g.kchunk;
-    const int kend = min(K, kbeg + g.kchunk);
-    const int nk = (kend - kbeg) / BK;
+    const int total = tiles_m * tiles_n * g.ksplit;
     const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.A);
     const bf16_t* __restrict__ W = static_cast<const bf16_t*>(g.W);
 
-    // per load instruction: this lane's element offset (row * ld + swizzled
-    // chunk) and the wave's 1 KB destination inside a stage (bytes)
+    // Persistent when the grid is smaller than the tile count: workgroup b
+    // takes physical ids b, b + grid, ... (the grid is a multiple of the XCD
+    // count, so every id maps to a tile of the workgroup's own XCD).
+    // Tile state: split index, tile origin, K range, and per load
+    // instruction this lane's element offset (row * ld + swizzled chunk).
+    int kz, m0, n0, kbeg, nk;
     int goff[IPW];
+    auto setup = [&](int hw) {
+        const TileIdx ti = tile_of(xcd_logical_block(hw, total), tiles_m, tiles_n, BM, BN, g.group_m);
+        kz = ti.kz; m0 = ti.m0; n0 = ti.n0;
+        kbeg = kz * g.kchunk;
+        nk = (min(K, kbeg + g.kchunk) - kbeg) / BK;
+#pragma unroll
+        for (int i = 0; i < IPW; ++i) {
+            const int blk = i * NW + wave;                      // 8-row block
+            const bool isA = i < IA;
+            const int rloc = (isA ? blk : blk - BM / 8) * 8 + lane / 8;
+            const int c = (lane % 8) ^ ((rloc >> 1) & 7);
+            if (isA) goff[i] = min(m0 + rloc, M - 1) * g.lda + c * 8;
+            else goff[i] = min(n0 + rloc, N - 1) * K + c * 8;
+        }
+    };
+    // the wave's 1 KB destination of each load instruction inside a stage (bytes)
     uint32_t ldst[IPW];
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
-        const int blk = i * NW + wave;                      // 8-row block
-        const bool isA = i < IA;
-        const int rloc = (isA ? blk : blk - BM / 8) * 8 + lane / 8;
-        const int c = (lane % 8) ^ ((rloc >> 1) & 7);
-        if (isA) goff[i] = min(m0 + rloc, M - 1) * g.lda + c * 8;
-        else goff[i] = min(n0 + rloc, N - 1) * K + c * 8;
-        ldst[i] = isA ? lds_addr(sAb + blk * 512) : lds_addr(sWb + (blk - BM / 8) * 512);
+        const int blk = i * NW + wave;
+        ldst[i] = i < IA ? lds_addr(sAb + blk * 512) : lds_addr(sWb + (blk - BM / 8) * 512);
     }
     constexpr uint32_t kStageA = BM * ROWE * 2, kStageW = BN * ROWE * 2;   // bytes
     auto issue = [&](int kt, int st) {
@@ -289,20 +299,25 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
             else dma_lds16(W + goff[i] + k0, ldst[i] + st * kStageW);
         }
     };
-
-    f32x4_t acc[SN][SM];
+    auto prologue = [&]() {
 #pragma unroll
-    for (int i = 0; i < SN; ++i)
-#pragma unroll
-        for (int j = 0; j < SM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int st = 0; st < S - 1; ++st)
+            if (st < nk) issue(st, st);
+    };
 
     // fragment offsets inside a stage: row r, logical chunk ks*4 + grp, swizzled by (r >> 1) & 7
     const int sw = (lane % 16) >> 1;
     const int grp = lane / 16;
 
+    int hw = blockIdx.x;
+    setup(hw);
+    prologue();
+    for (;;) {
+    f32x4_t acc[SN][SM];
 #pragma unroll
-    for (int st = 0; st < S - 1; ++st)
-        if (st < nk) issue(st, st);
+    for (int i = 0; i < SN; ++i)
+#pragma unroll
+        for (int j = 0; j < SM; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     for (int kt = 0; kt < nk; ++kt) {
         const int st = kt % S;
         // stage kt complete (the loads of the later stages may stay in
@@ -338,20 +353,32 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
     // Measured per epilogue (c2 / c4 / c5): staging pays for the QKV split
     // (-7..-13%, its K/V rows are scattered) and the split-K partials; for
     // the residual and GELU epilogues the direct stores are as fast or faster.
+    const int hw_next = hw + (int)gridDim.x;
+    const bool more = hw_next < total;
     if (EPI != kEpiQKV && EPI != kEpiBias && g.ksplit == 1) {
+        // direct stores from registers: the next tile's first stages load
+        // during them (every wave is past its last read of the stages)
+        const int cm0 = m0, cn0 = n0;
+        if (more) {
+            barrier_only();
+            setup(hw_next);
+            prologue();
+        }
 #pragma unroll
         for (int i = 0; i < SN; ++i) {
-            const int n = n0 + wn * (BN / WN) + i * 16 + grp * 4;
+            const int n = cn0 + wn * (BN / WN) + i * 16 + grp * 4;
             if (n >= N) continue;
 #pragma unroll
             for (int j = 0; j < SM; ++j) {
-                const int m = m0 + wm * (BM / WM) + j * 16 + lane % 16;
+                const int m = cm0 + wm * (BM / WM) + j * 16 + lane % 16;
                 if (m >= M) continue;
                 float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
                 epilogue_store<bf16_t, EPI>(g, m, n, v);
             }
         }
-        return;
+        if (!more) return;
+        hw = hw_next;
+        continue;
     }
     constexpr int CPR = BN / 4;               // 16-byte chunks per staged row
     constexpr int PR = BM / kOutPasses;       // rows per pass
@@ -385,6 +412,12 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
             }
         }
     }
+    if (!more) return;
+    __syncthreads();   // the staging reads are done before the stages refill
+    hw = hw_next;
+    setup(hw);
+    prologue();
+    }
 }
 
 // Split-K: sum the partials in split order, then the epilogue.
@@ -416,17 +449,43 @@ hipError_t launch_tile(const GemmDesc& g, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Grid of a direct-to-LDS launch: one workgroup per tile, or, past what the
+// CUs hold at once, that many persistent workgroups (a multiple of the XCD
+// count) looping over the tiles.
+unsigned dl_grid(int resident, long tiles) {
+    static const bool off = [] {   // tuning knob MS_GEMM_PERSISTENT=0: one workgroup per tile
+        const char* v = std::getenv("MS_GEMM_PERSISTENT");
+        return v && std::strcmp(v, "0") == 0;
+    }();
+    if (off || tiles <= resident) return (unsigned)tiles;
+    return (unsigned)(resident - resident % kXcds);
+}
+
+template <int BM, int BN, int S, int EPI>
+hipError_t launch_dl_epi(const GemmDesc& g, hipStream_t s) {
+    const long tiles = (long)((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM) * g.ksplit;
+    const int threads = kWave * dl_waves(BM, BN);
+    static const int resident = [threads] {   // workgroups of this kernel the CUs hold at once
+        int per_cu = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, gemm_dl_kernel<BM, BN, S, EPI>, threads, 0) !=
+                hipSuccess || per_cu < 1)
+            per_cu = 1;
+        return per_cu * kCUs;
+    }();
+    const unsigned grid = dl_grid(resident, tiles);
+    hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, EPI>), dim3(grid), dim3(threads), 0, s, g);
+    return hipGetLastError();
+}
+
 template <int BM, int BN, int S>
 hipError_t launch_dl(const GemmDesc& g, hipStream_t s) {
-    dim3 grid(((g.N + BN - 1) / BN) * ((g.M + BM - 1) / BM) * g.ksplit), block(kWave * dl_waves(BM, BN));
     switch (g.epilogue) {
-        case kEpiBias: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiBias>), grid, block, 0, s, g); break;
-        case kEpiBiasResid: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiBiasResid>), grid, block, 0, s, g); break;
-        case kEpiBiasGelu: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiBiasGelu>), grid, block, 0, s, g); break;
-        case kEpiQKV: hipLaunchKernelGGL((gemm_dl_kernel<BM, BN, S, kEpiQKV>), grid, block, 0, s, g); break;
+        case kEpiBias: return launch_dl_epi<BM, BN, S, kEpiBias>(g, s);
+        case kEpiBiasResid: return launch_dl_epi<BM, BN, S, kEpiBiasResid>(g, s);
+        case kEpiBiasGelu: return launch_dl_epi<BM, BN, S, kEpiBiasGelu>(g, s);
+        case kEpiQKV: return launch_dl_epi<BM, BN, S, kEpiQKV>(g, s);
         default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 template <typename T>

@@ -101,3 +101,24 @@ def test_linear_rejects_bad_arguments():
         MS.ms_linear(A, W, b, out, epilogue=MS.MS_EPI_BIAS_RESID)   # no residual given
     with pytest.raises(MS.MaskStepError):
         MS.ms_linear(A, W, b, out, ksplit=2)                          # no workspace
+
+
+@pytest.mark.parametrize("tile,M,N", [((64, 64), 4096, 2112), ((128, 64), 3000, 2048), ((256, 256), 4608, 4352)],
+                         ids=["64x64", "128x64", "256x256"])
+@pytest.mark.parametrize("epi", [MS.MS_EPI_BIAS, MS.MS_EPI_BIAS_RESID, MS.MS_EPI_BIAS_GELU],
+                         ids=["bias", "resid", "gelu"])
+def test_linear_more_tiles_than_resident_workgroups(tile, M, N, epi):
+    """More tiles than the CUs hold at once: each workgroup loops over several tiles,
+    loading the next tile's first stages during the current tile's epilogue."""
+    g = torch.Generator(device=DEV).manual_seed(hash((tile, epi, M)) % 1000)
+    K = 192
+    A = torch.randn(M, K, device=DEV, generator=g).bfloat16()
+    W = (torch.randn(N, K, device=DEV, generator=g) * 0.05).bfloat16()
+    b = (torch.randn(N, device=DEV, generator=g) * 0.05).bfloat16()
+    R = torch.randn(M, N, device=DEV, generator=g).bfloat16()
+    out = torch.empty(M, N, device=DEV, dtype=torch.bfloat16)
+    MS.ms_linear(A, W, b, out, resid=R, epilogue=epi, tile=tile, ksplit=1)
+    torch.cuda.synchronize()
+    e = _err(out, _ref(A, W, b, R, epi))
+    print(f"[parity] persistent tile {tile} {M}x{N} epi {epi}: max-norm rel err {e:.2e}")
+    assert e <= 2e-2
