@@ -514,6 +514,16 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
         pv((t % S) * C::STAGEB, sa);
     }
 
+    // Output (or this key range's partial) through LDS: a lane holds 4
+    // consecutive head_dim values of one query row per 16 x 16 block, so
+    // direct stores write 8-byte pieces of 16 rows; staged in the (now free)
+    // stage memory, each wave writes its 32 rows as row-contiguous 16-byte
+    // vectors. Rows of 128 / 256 bytes XOR-swizzle their 16-byte chunks by
+    // the row (head_dim 72 rows are not swizzled).
+    constexpr int CH = HD / 8;                     // 16-byte chunks per row
+    constexpr int SWM = C::SWZ ? (CH >= 16 ? 15 : CH - 1) : 0;
+    __syncthreads();   // every wave is past its last read of the stages
+    uint8_t* const so = smem + wave * 32 * C::ROWB;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         float l;
@@ -525,40 +535,33 @@ __global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) 
         } else {
             l = oacc[qb][C::NHS - 1][0];
         }
-        const int qrow = row0 + wave * 32 + qb * 16 + l16;
-        if (qrow >= row_end) continue;
-        if (a.nsplit == 1) {
-            const float inv_l = 1.0f / l;
-            bf16_t* op = static_cast<bf16_t*>(a.o) + (long)qrow * d + head * HD;
+        // normalised by this key range's own sum (bf16 holds it to the
+        // output's precision at half the bytes of float32)
+        const float inv_l = 1.0f / l;
+        const int rl = qb * 16 + l16;
 #pragma unroll
-            for (int h = 0; h < C::NHS; ++h) {
-                const int cidx = h * 16 + grp * 4;
-                if (cidx < HD) {
-                    float v[4];
+        for (int h = 0; h < C::NHS; ++h) {
+            const int cidx = h * 16 + grp * 4;
+            if (cidx < HD) {
+                float v[4];
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] = oacc[qb][h][r] * inv_l;
-                    store4<bf16_t>(op + cidx, v);
-                }
+                for (int r = 0; r < 4; ++r) v[r] = oacc[qb][h][r] * inv_l;
+                store4<bf16_t>(reinterpret_cast<bf16_t*>(so + rl * C::ROWB + (((cidx / 8) ^ (rl & SWM)) * 16) + (cidx % 8) * 2), v);
             }
-        } else {
-            // this key range's output, normalised by its own sum: bf16 holds
-            // it to the output's precision at half the bytes of float32
-            const float inv_l = 1.0f / l;
-            bf16_t* po = a.part_o + ((long)split * a.M + qrow) * d + head * HD;
-#pragma unroll
-            for (int h = 0; h < C::NHS; ++h) {
-                const int cidx = h * 16 + grp * 4;
-                if (cidx < HD) {
-                    float v[4];
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] = oacc[qb][h][r] * inv_l;
-                    store4<bf16_t>(po + cidx, v);
-                }
-            }
-            if (grp == 0)
-                *reinterpret_cast<float2*>(a.part_ml + 2 * (((long)split * a.M + qrow) * a.n_heads + head)) =
-                    make_float2(m_run[qb], l);
         }
+        const int qrow = row0 + wave * 32 + rl;
+        if (a.nsplit > 1 && grp == 0 && qrow < row_end)
+            *reinterpret_cast<float2*>(a.part_ml + 2 * (((long)split * a.M + qrow) * a.n_heads + head)) =
+                make_float2(m_run[qb], l);
+    }
+    __syncthreads();
+    bf16_t* const dst = a.nsplit == 1 ? static_cast<bf16_t*>(a.o) : a.part_o + (long)split * a.M * d;
+#pragma unroll
+    for (int k = lane; k < 32 * CH; k += kWave) {
+        const int rl = k / CH, c = k % CH;
+        const int qrow = row0 + wave * 32 + rl;
+        if (qrow < row_end)
+            st16(dst + (long)qrow * d + head * HD + c * 8, ld16(so + rl * C::ROWB + ((c ^ (rl & SWM)) * 16)));
     }
 }
 
