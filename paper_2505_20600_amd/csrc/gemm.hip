@@ -6,8 +6,9 @@
 // Both operands are K-contiguous (activations [M][K], Linear weights
 // [N][K]), the native operand layout of the CDNA4 matrix cores. The weight
 // tile is the MFMA "A" operand and the activation tile the "B" operand, so
-// each lane ends up with four consecutive output columns of one row and the
-// epilogue writes 4-element vectors.
+// each lane ends up with four consecutive output columns of one row; the
+// QKV and plain-bias epilogues and the split-K partials first restage the
+// tile through LDS so that consecutive lanes write consecutive columns.
 //
 // Epilogues: bias; bias + residual (out-projection and MLP-down); bias +
 // erf-GELU (MLP-up, erf to 5.5e-7); QKV, which writes Q to its own buffer
@@ -19,7 +20,9 @@
 // 64 x 64 tiles through registers, double-buffered. The host picks tile,
 // stage count and K split from a step-time table measured on MI355X; split
 // workgroups write float32 partials, summed in a fixed order by a second
-// kernel that applies the epilogue.
+// kernel that applies the epilogue (or, before a LayerNorm, by the fused
+// sum + LayerNorm kernel in rows.hip). Launches with more tiles than the
+// CUs hold at once run persistent workgroups.
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
