@@ -1,6 +1,7 @@
 // Token-wise row kernels: gather of the masked rows, the final scatter into the
 // cached hidden state (Sec. 3.1: extract the masked tokens, replenish the
-// unmasked ones from the cache) and LayerNorm over packed rows.
+// unmasked ones from the cache), LayerNorm over packed rows, and the split-K
+// sum of a residual projection fused with the LayerNorm that follows it.
 //
 // Gather and scatter are pure HBM copies: 16-byte vector loads/stores, one
 // row chunk per thread, grid-stride so that any M fills the chip.
