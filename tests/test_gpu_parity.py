@@ -189,6 +189,44 @@ def test_small_bf16_stack_matches_oracle(shape, ratio):
         np.testing.assert_array_equal(kv_gpu[0][b, keep], kv[0][b, keep])
 
 
+# The widest bf16 model the library accepts (d_model 4096, 32 heads of 128), and the
+# largest batch with two weight streams: 64 requests, 2 x 64 packed segments, the
+# most one step holds (masks of 0 to 100% by turns, so whole-request skips too).
+LIMIT_SHAPES = [
+    W.ModelShape("limit_d4096", 1, 4096, 32, 4, 4, 8, dtype="bf16"),
+    W.ModelShape("limit_b64_dual", 1, 256, 2, 4, 4, 4, n_text=4, dual_stream=True, dtype="bf16", batch=64),
+]
+
+
+@pytest.mark.parametrize("shape", LIMIT_SHAPES, ids=lambda s: s.name)
+def test_step_at_the_accepted_limits_matches_oracle(shape):
+    ws, xt, kv, yc = _inputs(shape, 90)
+    ratio = [(b % 5) / 4 for b in range(shape.batch)] if shape.batch > 1 else 0.5
+    mask = _random_mask(shape, ratio, 23)
+    x = W.edited_hidden(shape, 90, xt, mask)
+    y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
+    y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
+    G.assert_close(y, y_ref, "bf16", f"{shape.name} output")
+    G.assert_close(kv_gpu[0], kv_ref[0], "bf16", f"{shape.name} K/V")
+    for b in range(shape.batch):
+        keep = np.concatenate([np.zeros(shape.n_text, bool), mask[b] == 0])
+        np.testing.assert_array_equal(y[b, keep], yc[b, keep])
+
+
+def test_single_masked_token_per_request_matches_oracle():
+    """One recomputed row per request: a query tile of one valid row over every key."""
+    shape = W.ModelShape("one_token_b3", 2, 256, 4, 4, 12, 16, dtype="bf16", batch=3)
+    ws, xt, kv, yc = _inputs(shape, 91, std=0.03)
+    mask = _random_mask(shape, 1.0 / shape.n_image, 29)
+    assert (mask.sum(1) == 1).all()
+    x = W.edited_hidden(shape, 91, xt, mask)
+    y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
+    y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
+    G.assert_close(y, y_ref, "bf16", "one token output")
+    for l in range(shape.n_layers):
+        G.assert_close(kv_gpu[l], kv_ref[l], "bf16", f"one token K/V layer {l}")
+
+
 FUSE_SHAPES = [
     # d = 576 at a few hundred rows: both residual projections split K
     W.ModelShape("fuse_dual_d576", 3, 576, 8, 4, 10, 12, n_text=24, dual_stream=True, dtype="bf16", batch=2),
