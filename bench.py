@@ -319,6 +319,26 @@ def _intersection(u, v):
     return tot
 
 
+def step_fit(per_ratio):
+    """Least-squares line of the median step time against the masked rows (Table 1: the
+    masked computation is linear in M), over the mask sets that share the most common
+    dense prefix; None below three distinct row counts."""
+    if not per_ratio:
+        return None
+    prefixes = [r[3] for r in per_ratio]
+    pre = max(set(prefixes), key=prefixes.count)
+    pts = [(r[1], r[2]) for r in per_ratio if r[3] == pre]
+    x = np.array([p[0] for p in pts], float)
+    y = np.array([p[1] for p in pts], float)
+    if len(set(x.tolist())) < 3:
+        return None
+    slope, icpt = np.polyfit(x, y, 1)
+    ss_tot = float(np.sum((y - y.mean()) ** 2))
+    r2 = 1.0 - float(np.sum((y - (icpt + slope * x)) ** 2)) / ss_tot if ss_tot > 0 else 1.0
+    return {"ms0": round(float(icpt), 4), "ms_per_1k_rows": round(1e3 * float(slope), 4),
+            "r2": round(r2, 4), "points": len(pts), "dense_prefix": pre}
+
+
 def stream_overlap(intervals, steps):
     """Per step: summed cache-load time, summed kernel time, the first layer's load, and the
     fraction of the shorter of the two that runs concurrently with the other."""
@@ -717,6 +737,7 @@ def main():
                    "cache": "per-layer K/V (Fig. 7)" if args.cache == "kv" else
                             "per-layer block inputs, K/V recomputed (Fig. 5 bottom)"},
         "per_mask": {"columns": ["ratio", "masked_rows", "median_ms", "dense_prefix"], "rows": per_ratio},
+        "step_vs_rows_fit": step_fit(per_ratio),
         "prefix_plan": plan_info or None,
         "mask_step_init_ms": {"mean": round(float(np.mean(init_ms)), 3), "max": round(float(max(init_ms)), 3),
                               "note": "once per mask set (compaction + one host sync), outside the step"},

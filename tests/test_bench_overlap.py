@@ -3,6 +3,7 @@ their intersection), checked on hand-made timelines."""
 import importlib.util
 import os
 
+import numpy as np
 import pytest
 
 _spec = importlib.util.spec_from_file_location(
@@ -40,3 +41,16 @@ def test_stream_overlap_figures():
 def test_stream_overlap_without_copies():
     r = bench.stream_overlap([("attention", 0.0, 1.0)], steps=1)
     assert r["overlap"] is None and r["sum_copy_ms"] == 0
+
+
+def test_step_fit_is_the_least_squares_line_over_the_common_prefix():
+    rows = [[0.1, 400, 0.8 + 0.0003 * 400, 0], [0.3, 1200, 0.8 + 0.0003 * 1200, 0],
+            [0.5, 2000, 0.8 + 0.0003 * 2000, 0], [0.9, 3600, 5.0, 2]]
+    f = bench.step_fit(rows)
+    assert f["points"] == 3 and f["dense_prefix"] == 0
+    assert abs(f["ms0"] - 0.8) < 1e-4 and abs(f["ms_per_1k_rows"] - 0.3) < 1e-4 and f["r2"] == 1.0
+    noisy = [[0, m, t, 0] for m, t in ((100, 1.0), (200, 1.3), (300, 1.1), (400, 1.6))]
+    x = np.array([100, 200, 300, 400.0]); y = np.array([1.0, 1.3, 1.1, 1.6])
+    r = np.corrcoef(x, y)[0, 1]
+    assert abs(bench.step_fit(noisy)["r2"] - r * r) < 1e-3
+    assert bench.step_fit(rows[:2]) is None and bench.step_fit([]) is None
