@@ -32,7 +32,10 @@ Precision: everything is evaluated in float64. For the bf16 workloads,
 holds a value in bf16 storage: LN outputs; Q, K, V; the attention output O;
 the out-projection result H (residual included); the GELU output U; the block
 output. Between those points there is no rounding. The fp32 workload uses no
-rounding at all.
+rounding at all. The switch ``round_p`` (bf16 workloads only, off by default)
+also rounds the softmax weights to bf16 before the PV product, the operand
+type of a bf16 matrix unit; the normaliser is then the sum of the same
+rounded weights, so the weights applied still sum to one.
 
 Arrays: hidden ``[B][T][d]``, K/V ``[B][T][2][d]`` (K then V per token), mask
 ``uint8 [B][N]`` over the image grid (nonzero = masked). Token ``t`` of a
@@ -90,11 +93,19 @@ def gelu(x) -> np.ndarray:
     return x * 0.5 * (1.0 + erf(x / np.sqrt(2.0)))
 
 
-def attention_head(q, k, v, scale: float) -> np.ndarray:
-    """softmax(q k^T * scale) v for one head; full softmax over every key (Sec. 3.1)."""
+def attention_head(q, k, v, scale: float, round_p: bool = False) -> np.ndarray:
+    """softmax(q k^T * scale) v for one head; full softmax over every key (Sec. 3.1).
+
+    With ``round_p`` the unnormalised weights ``exp(s - max s)`` (the largest is
+    exactly 1) are rounded to bf16 before they multiply V, and each row is
+    divided by the sum of its rounded weights.
+    """
     s = (np.asarray(q, np.float64) @ np.asarray(k, np.float64).T) * scale
     s = s - s.max(axis=1, keepdims=True)
     p = np.exp(s)
+    if round_p:
+        p = bf16_round(p)
+        return (p @ np.asarray(v, np.float64)) / p.sum(axis=1, keepdims=True)
     p /= p.sum(axis=1, keepdims=True)
     return p @ np.asarray(v, np.float64)
 
@@ -186,13 +197,15 @@ def _token_wise(fn, x_rows, toks, layer_w, n_text):
     return out
 
 
-def block_rows(x_rows, toks, layer_w, kv_b, shape, rnd):
+def block_rows(x_rows, toks, layer_w, kv_b, shape, rnd, round_p: bool = False):
     """One pre-LN block for the rows ``toks`` of one request.
 
     ``x_rows [m][d]`` are the hidden rows of tokens ``toks``; ``kv_b [T][2][d]``
     holds K/V for every token of the request (cache contents). The K/V of
     ``toks`` are recomputed from ``x_rows`` and replace the cached rows
     (Fig. 7); every row in ``toks`` then queries all ``T`` keys (Fig. 5).
+    ``round_p`` rounds the softmax weights to bf16 (bf16 workloads only; see
+    ``attention_head``).
 
     Returns ``(x_out [m][d], kv_work [T][2][d])``.
     """
@@ -214,9 +227,10 @@ def block_rows(x_rows, toks, layer_w, kv_b, shape, rnd):
 
     o = np.empty_like(q)
     scale = 1.0 / np.sqrt(hd)
+    rp = bool(round_p) and shape.dtype == "bf16"
     for j in range(h):
         cs = slice(j * hd, (j + 1) * hd)
-        o[:, cs] = attention_head(q[:, cs], kv_work[:, 0, cs], kv_work[:, 1, cs], scale)
+        o[:, cs] = attention_head(q[:, cs], kv_work[:, 0, cs], kv_work[:, 1, cs], scale, rp)
     o = rnd(o)
 
     def post_attn(pair, w):
@@ -235,7 +249,7 @@ def block_rows(x_rows, toks, layer_w, kv_b, shape, rnd):
 # ---------------------------------------------------------------------------
 
 
-def dense_stack(x, weights, shape):
+def dense_stack(x, weights, shape, round_p: bool = False):
     """Full computation over every token (the Fig. 5 top flow), layer by layer.
 
     Returns ``(y [B][T][d], kv [L][B][T][2][d])``; ``kv`` is what a cache of
@@ -250,14 +264,14 @@ def dense_stack(x, weights, shape):
     for b in range(B):
         xb = x[b]
         for l, w in enumerate(weights):
-            xb, kvw = block_rows(xb, toks, w, np.zeros((T, 2, d)), shape, rnd)
+            xb, kvw = block_rows(xb, toks, w, np.zeros((T, 2, d)), shape, rnd, round_p)
             kv[l, b] = kvw
         y[b] = xb
     return y, kv
 
 
 def masked_stack(x, mask, kv_cache, y_cache, weights, shape, return_kv: bool = False,
-                 dense_prefix: int = 0):
+                 dense_prefix: int = 0, round_p: bool = False):
     """Mask-aware step with K/V caching (Sec. 3.1, Fig. 5 bottom and Fig. 7).
 
     ``kv_cache[l]`` is ``[B][T][2][d]`` (rows of recomputed tokens are ignored),
@@ -271,7 +285,7 @@ def masked_stack(x, mask, kv_cache, y_cache, weights, shape, return_kv: bool = F
     Sec. 4.2 and Alg. 1) and blocks ``k..L-1`` with the cache. With K/V
     caching a block can only skip the cache if all earlier blocks did (only
     then do the unmasked tokens' hidden states exist), so the choice is a
-    prefix.
+    prefix. ``round_p``: see ``attention_head``.
     """
     rnd = rounder(shape.dtype)
     x = np.asarray(x, np.float64)
@@ -294,12 +308,12 @@ def masked_stack(x, mask, kv_cache, y_cache, weights, shape, return_kv: bool = F
             continue
         xb = x[b]
         for l in range(k):
-            xb, kvw = block_rows(xb, all_toks, weights[l], np.zeros((T, 2, d)), shape, rnd)
+            xb, kvw = block_rows(xb, all_toks, weights[l], np.zeros((T, 2, d)), shape, rnd, round_p)
             if return_kv:
                 kv_out[l, b] = kvw
         xm = xb[toks]
         for l in range(k, L):
-            xm, kvw = block_rows(xm, toks, weights[l], kv_cache[l][b], shape, rnd)
+            xm, kvw = block_rows(xm, toks, weights[l], kv_cache[l][b], shape, rnd, round_p)
             if return_kv:
                 kv_out[l, b] = kvw
         y[b, toks] = xm
@@ -308,20 +322,32 @@ def masked_stack(x, mask, kv_cache, y_cache, weights, shape, return_kv: bool = F
     return y
 
 
-def masked_rows_of_stack(x, mask, kv_cache, weights, shape, b: int, rows_sel=None):
-    """Final hidden rows of request ``b`` for the recomputed tokens only.
+def masked_rows_of_stack(x, mask, kv_cache, weights, shape, b: int, dense_prefix: int = 0,
+                         round_p: bool = False):
+    """Final hidden rows of request ``b`` for its recomputed tokens only: ``(toks, rows)``.
 
-    Every recomputed token must pass through every layer (its K/V feed the
-    other tokens' attention), so this runs the whole masked path for one
-    request; ``rows_sel`` then picks packed rows out of the result.
+    The same steps as ``masked_stack`` for that one request (requests never
+    attend across each other): blocks ``0..k-1`` over every token of the
+    request (``k = dense_prefix``), then the cached blocks over its recomputed
+    rows. ``kv_cache[l]`` only needs ``[b]`` indexing, so a caller may pass
+    per-layer arrays of any batch size that hold request ``b``.
     """
     rnd = rounder(shape.dtype)
+    k = int(dense_prefix)
+    L = len(weights)
+    if not 0 <= k <= L:
+        raise ValueError("dense_prefix out of range")
     toks = masked_tokens(mask[b], shape.n_text)
-    xm = np.asarray(x[b][toks], np.float64)
-    for l, w in enumerate(weights):
-        xm, _ = block_rows(xm, toks, w, kv_cache[l][b], shape, rnd)
-    if rows_sel is not None:
-        return toks[rows_sel], xm[rows_sel]
+    if toks.size == 0:
+        return toks, np.zeros((0, shape.d_model))
+    xb = np.asarray(x[b], np.float64)
+    T, d = xb.shape
+    all_toks = np.arange(T)
+    for l in range(k):
+        xb, _ = block_rows(xb, all_toks, weights[l], np.zeros((T, 2, d)), shape, rnd, round_p)
+    xm = xb[toks]
+    for l in range(k, L):
+        xm, _ = block_rows(xm, toks, weights[l], kv_cache[l][b], shape, rnd, round_p)
     return toks, xm
 
 

@@ -57,7 +57,8 @@ def kv_cache_of_inputs(yin_cache, mask, weights, shape) -> np.ndarray:
     return kv
 
 
-def masked_stack_y(x, mask, yin_cache, y_cache, weights, shape, dense_prefix: int = 0):
+def masked_stack_y(x, mask, yin_cache, y_cache, weights, shape, dense_prefix: int = 0,
+                   round_p: bool = False):
     """Mask-aware step with Y caching.
 
     Blocks ``0..k-1`` (``k = dense_prefix``) run over every token without the
@@ -65,6 +66,7 @@ def masked_stack_y(x, mask, yin_cache, y_cache, weights, shape, dense_prefix: in
     cache only while every earlier block did, so the choice is again a
     prefix); blocks ``k..L-1`` recompute the K/V of the unmasked image tokens
     from ``yin_cache[l]`` and everything else for the recomputed rows only.
+    ``round_p``: the bf16 softmax-weight switch of ``oracle.stack.attention_head``.
     """
     rnd = rounder(shape.dtype)
     x = np.asarray(x, np.float64)
@@ -82,19 +84,19 @@ def masked_stack_y(x, mask, yin_cache, y_cache, weights, shape, dense_prefix: in
         un = np.flatnonzero(np.asarray(mask[b]) == 0)
         xb = x[b]
         for l in range(k):
-            xb, _ = block_rows(xb, all_toks, weights[l], np.zeros((T, 2, d)), shape, rnd)
+            xb, _ = block_rows(xb, all_toks, weights[l], np.zeros((T, 2, d)), shape, rnd, round_p)
         xm = xb[toks]
         for l in range(k, L):
             kv_b = np.zeros((T, 2, d), np.float64)
             if un.size:
                 kv_b[shape.n_text + un] = kv_of_inputs(np.asarray(yin_cache[l][b], np.float64)[un],
                                                        weights[l], shape, rnd)
-            xm, _ = block_rows(xm, toks, weights[l], kv_b, shape, rnd)
+            xm, _ = block_rows(xm, toks, weights[l], kv_b, shape, rnd, round_p)
         y[b, toks] = xm
     return y
 
 
-def dense_inputs(x, weights, shape) -> np.ndarray:
+def dense_inputs(x, weights, shape, round_p: bool = False) -> np.ndarray:
     """Input hidden state of every block of the dense flow (Fig. 5 top), image
     tokens only: what a Y cache of this inference holds. ``[L][B][N][d]``."""
     rnd = rounder(shape.dtype)
@@ -108,5 +110,5 @@ def dense_inputs(x, weights, shape) -> np.ndarray:
         xb = x[b]
         for l, w in enumerate(weights):
             out[l, b] = xb[nt:]
-            xb, _ = block_rows(xb, toks, w, np.zeros((T, 2, d)), shape, rnd)
+            xb, _ = block_rows(xb, toks, w, np.zeros((T, 2, d)), shape, rnd, round_p)
     return out

@@ -303,3 +303,87 @@ def test_compact_edge_masks():
         c = oracle.compact(mask)
         assert c["M"] == int(mask.sum())
         np.testing.assert_array_equal(c["rows"], np.flatnonzero(mask.reshape(-1)))
+
+
+# ---------------------------------------------------------------- round_p (bf16 softmax weights)
+
+def test_round_p_hand_example():
+    """Two keys with weights 1 and 1/3: bf16(1/3) = 0.333984375 (8 significant bits, rounded up),
+    so with V = (0, 1) the rounded output is 0.333984375 / 1.333984375 instead of 1/4."""
+    q = np.array([[1.0]])
+    k = np.array([[0.0], [-np.log(3.0)]])
+    v = np.array([[0.0], [1.0]])
+    assert oracle.bf16_round(1.0 / 3.0) == 0.333984375
+    exact = oracle.attention_head(q, k, v, 1.0)
+    rounded = oracle.attention_head(q, k, v, 1.0, round_p=True)
+    assert abs(exact[0, 0] - 0.25) < 1e-15
+    assert rounded[0, 0] == 0.333984375 / 1.333984375
+
+
+def test_round_p_is_exact_for_representable_weights():
+    """Weights 1, 1/2, 1/4, 1/8 are bf16 values: rounding them changes nothing."""
+    g = np.random.default_rng(3)
+    q = np.array([[1.0], [2.0]])
+    k = -np.log(2.0) * np.arange(4.0)[:, None]          # scores 0, -ln2, -2 ln2, -3 ln2 (times q)
+    v = g.standard_normal((4, 5))
+    np.testing.assert_allclose(oracle.attention_head(q, k, v, 1.0, round_p=True),
+                               oracle.attention_head(q, k, v, 1.0), rtol=1e-14, atol=1e-14)
+
+
+def test_round_p_reduces_to_plain_softmax_in_fp32():
+    """The switch only applies to bf16 workloads: an fp32 stack is bit-identical with it."""
+    ws, x = _setup(TINY)
+    mask = np.array([[1, 0, 1, 1, 0, 0, 1, 0, 0, 1, 0, 0]], np.uint8)
+    _, kv = oracle.dense_stack(W.template_hidden(TINY, 12), ws, TINY)
+    yc = W.synthetic_y_cache(TINY, 3)
+    np.testing.assert_array_equal(oracle.masked_stack(x, mask, kv, yc, ws, TINY, round_p=True),
+                                  oracle.masked_stack(x, mask, kv, yc, ws, TINY))
+    np.testing.assert_array_equal(oracle.dense_stack(x, ws, TINY, round_p=True)[0],
+                                  oracle.dense_stack(x, ws, TINY)[0])
+
+
+def test_round_p_in_bf16_moves_the_result_within_bf16_rounding():
+    shape = TINY_BF16.replace(d_model=64, n_heads=2, grid_h=6, grid_w=8)
+    ws = W.stack_weights(shape, 13, random_ln=True, std=0.2)
+    x = W.template_hidden(shape, 13)
+    y0, _ = oracle.dense_stack(x, ws, shape)
+    y1, _ = oracle.dense_stack(x, ws, shape, round_p=True)
+    err = np.max(np.abs(y1 - y0)) / np.max(np.abs(y0))
+    assert 0 < err < 2e-2, err      # changes bits (not vacuous), at the scale of bf16 rounding
+
+
+@pytest.mark.parametrize("shape", [TINY_BF16, TINY_DUAL.replace(dtype="bf16")], ids=["bf16", "dual_bf16"])
+def test_round_p_keeps_the_invariants(shape):
+    """Own cache reproduces dense and the all-ones mask reads no cache, with round_p on both sides."""
+    ws, x = _setup(shape)
+    y, kv = oracle.dense_stack(x, ws, shape, round_p=True)
+    g = np.random.default_rng(9)
+    mask = (g.random((1, shape.n_image)) < 0.4).astype(np.uint8)
+    ym = oracle.masked_stack(x, mask, kv, y, ws, shape, round_p=True)
+    assert np.max(np.abs(ym - y)) <= 2e-2 * np.max(np.abs(y))
+    ones = np.ones((1, shape.n_image), np.uint8)
+    y1 = oracle.masked_stack(x, ones, np.full_like(kv, np.nan), y, ws, shape, round_p=True)
+    assert np.all(np.isfinite(y1))
+    assert np.max(np.abs(y1 - y)) <= 2e-2 * np.max(np.abs(y))
+
+
+# ---------------------------------------------------------------- one request's rows
+
+@pytest.mark.parametrize("shape", [TINY.replace(batch=3), TINY_BF16.replace(batch=2),
+                                   TINY_DUAL.replace(batch=2, dtype="bf16")], ids=["fp32", "bf16", "dual_bf16"])
+@pytest.mark.parametrize("k", [0, 1, 2])
+@pytest.mark.parametrize("round_p", [False, True])
+def test_masked_rows_of_stack_equals_masked_stack(shape, k, round_p):
+    """The one-request form returns exactly the rows masked_stack writes for that request,
+    for every dense prefix, with and without round_p (same steps on the same rows)."""
+    ws, x = _setup(shape)
+    g = np.random.default_rng(21)
+    mask = (g.random((shape.batch, shape.n_image)) < 0.45).astype(np.uint8)
+    mask[-1] = 0                                    # one request with no masked image token
+    kv = np.stack([W.synthetic_kv_cache(shape, 4, l) for l in range(shape.n_layers)])
+    yc = W.synthetic_y_cache(shape, 4)
+    y = oracle.masked_stack(x, mask, kv, yc, ws, shape, dense_prefix=k, round_p=round_p)
+    for b in range(shape.batch):
+        toks, rows = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, b, dense_prefix=k, round_p=round_p)
+        np.testing.assert_array_equal(toks, oracle.masked_tokens(mask[b], shape.n_text))
+        np.testing.assert_array_equal(rows, y[b, toks])
