@@ -180,6 +180,19 @@ def _ptr(t) -> int | None:
     return t.data_ptr()
 
 
+def _event(e) -> int | None:
+    """Raw hipEvent_t of a torch.cuda.Event (or an int handle). torch creates its events
+    on first use; passing one that does not exist yet would silently drop the ordering."""
+    if e is None:
+        return None
+    if isinstance(e, int):
+        return e
+    h = e.cuda_event
+    if not h:
+        raise ValueError("torch.cuda.Event has no HIP event yet: record it once before passing it")
+    return h
+
+
 def _stream(s) -> int | None:
     if s is None:
         return torch.cuda.current_stream().cuda_stream
@@ -325,18 +338,20 @@ class MaskStep:
         _check(self._lib.mask_scatter_rows(self.handle, _ptr(xm), _ptr(ycache), _ptr(y), _stream(stream)))
 
     def prefetch_layer(self, layer: int, h_kv, d_slot, copy_stream, wait_event=None, signal_event=None):
-        ev = lambda e: None if e is None else (e if isinstance(e, int) else e.cuda_event)
+        """cache_prefetch_layer; events are torch.cuda.Event objects (already created, e.g.
+        recorded once) or raw hipEvent_t handles."""
         _check(self._lib.cache_prefetch_layer(self.handle, layer, _ptr(h_kv), _ptr(d_slot),
-                                              _stream(copy_stream), ev(wait_event), ev(signal_event)))
+                                              _stream(copy_stream), _event(wait_event), _event(signal_event)))
 
     def prefetch_inputs(self, layer: int, h_yin, d_slot, copy_stream, wait_event=None, signal_event=None):
-        ev = lambda e: None if e is None else (e if isinstance(e, int) else e.cuda_event)
         _check(self._lib.cache_prefetch_inputs(self.handle, layer, _ptr(h_yin), _ptr(d_slot),
-                                               _stream(copy_stream), ev(wait_event), ev(signal_event)))
+                                               _stream(copy_stream), _event(wait_event), _event(signal_event)))
 
-    def recompute_kv(self, layer: int, weights_c, y_in, kv, stream=None):
-        """K/V of the unmasked image tokens from their cached block input (Y caching)."""
-        _check(self._lib.mask_recompute_kv(self.handle, layer, weights_c, _ptr(y_in), _ptr(kv), _stream(stream)))
+    def recompute_kv(self, layer: int, weights, y_in, kv, stream=None):
+        """K/V of the unmasked image tokens from their cached block input (Y caching);
+        ``weights`` as for block_forward."""
+        arr = weights_array([weights])
+        _check(self._lib.mask_recompute_kv(self.handle, layer, arr, _ptr(y_in), _ptr(kv), _stream(stream)))
 
     def set_dense_prefix(self, k: int, stream=None):
         _check(self._lib.mask_step_set_dense_prefix(self.handle, k, _stream(stream)))

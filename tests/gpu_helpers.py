@@ -1,24 +1,18 @@
 """Shared helpers of the GPU parity tests: device copies of the seeded inputs,
-one step through the C ABI, and the error metric."""
+one step through the C ABI (whole-stack call or per-block calls), and the
+parity gate."""
 from __future__ import annotations
 
 import numpy as np
 import torch
 
+import oracle
 from paper_2505_20600_amd import maskstep as MS
 from paper_2505_20600_amd import workloads as W
+from tests import parity_gate as PG
 
 DEV = "cuda:0"
-# Max relative error of a tensor in the max norm, max|g - r| / max|r|.
-TOL = {"fp32": 1e-4, "bf16": 2e-2}
-# Element-wise guard, |g_i - r_i| / max(|r_i|, rms(r)): fp32 keeps the same
-# 1e-4; for bf16 it is derived from the arithmetic. Rounding the softmax
-# probabilities to bf16 before the PV product (the MFMA operand type) already
-# moves the oracle by 0.0144 after one block and 0.021 after three under this
-# measure, and two bf16 trajectories (GPU fp32 accumulation vs oracle float64)
-# differ by about sqrt(2) times that, growing with depth; 0.1 leaves room for
-# 28 layers while an indexing or algebra mistake gives O(1).
-ELEM_TOL = {"fp32": 1e-4, "bf16": 1e-1}
+TOL = PG.TOL
 
 
 def tdtype(shape):
@@ -43,33 +37,18 @@ def dev_weights(weights, shape):
     return out
 
 
-def max_rel_err(got, ref):
-    """max_i |g_i - r_i| / max_i |r_i|: relative error in the max norm."""
-    got = np.asarray(got, np.float64)
-    ref = np.asarray(ref, np.float64)
-    if ref.size == 0:
-        return 0.0
-    den = np.max(np.abs(ref))
-    return float(np.max(np.abs(got - ref)) / (den if den > 0 else 1.0))
+max_rel_err = PG.max_rel_err
+elem_rel_err = PG.elem_rel_err
 
 
-def elem_rel_err(got, ref):
-    """max_i |g_i - r_i| / max(|r_i|, rms(r)): element-wise relative error with an RMS floor."""
-    got = np.asarray(got, np.float64)
-    ref = np.asarray(ref, np.float64)
-    if ref.size == 0:
-        return 0.0
-    rms = np.sqrt(np.mean(ref ** 2))
-    den = np.maximum(np.abs(ref), rms if rms > 0 else 1.0)
-    return float(np.max(np.abs(got - ref) / den))
-
-
-def assert_close(got, ref, dtype, what=""):
-    e1, e2 = max_rel_err(got, ref), elem_rel_err(got, ref)
-    print(f"[parity] {what} max-norm rel err {e1:.3e} (tol {TOL[dtype]}), element-wise {e2:.3e} "
-          f"(tol {ELEM_TOL[dtype]})", flush=True)
+def assert_close(got, ref, dtype, what="", *, blocks):
+    """Max-norm error within TOL[dtype]; element-wise error within the bound after
+    ``blocks`` blocks between the shared input and the compared tensor (tests/parity_gate)."""
+    ok, e1, e2, lim = PG.check(got, ref, dtype, blocks)
+    print(f"[parity] {what}: max-norm rel err {e1:.3e} (tol {TOL[dtype]}), element-wise {e2:.3e} "
+          f"(tol {lim:.3g}, {blocks} block(s))", flush=True)
     assert e1 <= TOL[dtype], f"{what}: max-norm relative error {e1:.3e} > {TOL[dtype]}"
-    assert e2 <= ELEM_TOL[dtype], f"{what}: element-wise relative error {e2:.3e} > {ELEM_TOL[dtype]}"
+    assert e2 <= lim, f"{what}: element-wise relative error {e2:.3e} > {lim:.3g} ({blocks} block(s))"
 
 
 def new_step(shape, mask_np, stream=None):
@@ -81,7 +60,7 @@ def new_step(shape, mask_np, stream=None):
 
 
 def run_stack(shape, mask, x, kv_cache, y_cache, weights, *, pinned=False, serialize=False,
-              aliased=False, poison_cache=False, n_slots=2, dense_prefix=0, inputs=False):
+              aliased=False, poison_cache=False, n_slots=2, dense_prefix=0, inputs=False, return_kv=True):
     """One step through mask_stack_forward; returns (y, working kv per layer or None, step).
     With ``inputs`` the cache is Y caching's per-layer block inputs ``[L][B][N][d]``."""
     if inputs:
@@ -118,7 +97,7 @@ def run_stack(shape, mask, x, kv_cache, y_cache, weights, *, pinned=False, seria
     step.stack_forward(wc, d_x, d_yc, kv_layers, y, pinned=pinned, slots=slots, stream=cs,
                        copy_stream=copy)
     torch.cuda.synchronize()
-    kv_out = None if pinned else [to_np(t) for t in kv_layers]
+    kv_out = None if (pinned or not return_kv) else [to_np(t) for t in kv_layers]
     return to_np(y), kv_out, step
 
 
@@ -146,3 +125,125 @@ def _run_stack_y(shape, mask, x, yin, y_cache, weights, *, pinned, serialize, n_
                        inputs=True)
     torch.cuda.synchronize()
     return to_np(y), None, step
+
+
+# ------------------------------------------------------------------ a step through the per-block calls
+
+def _pinned(a, shape):
+    t = torch.empty(a.shape, dtype=tdtype(shape), pin_memory=True)
+    t.copy_(torch.as_tensor(np.ascontiguousarray(a, np.float32)).to(tdtype(shape)))
+    return t
+
+
+def run_block_by_block(shape, mask, x, cache, yc, weights, *, form="kv", n_slots=2, keep_kv=True):
+    """One step through the per-block calls: mask_gather_rows; per layer the cache load
+    (form "kv": cache_prefetch_layer of the image rows of ``cache`` [L][B][T][2][d] from
+    pinned host memory; "y": cache_prefetch_inputs of the block inputs [L][B][N][d] and
+    mask_recompute_kv; "resident": ``cache`` copied to HBM, the layer's buffer passed as
+    the working K/V) and mask_block_forward; mask_scatter_rows. Loads run on a copy
+    stream through a ring of ``n_slots`` device slots ordered by events.
+
+    Returns ``(y, snaps, rows)``: the output, per layer (block input rows, block output
+    rows, working K/V after the block or None) as float64, and the packed row table."""
+    L, B, T, N, d = shape.n_layers, shape.batch, shape.n_tokens, shape.n_image, shape.d_model
+    dt = tdtype(shape)
+    dw = dev_weights(weights, shape)
+    step = new_step(shape, mask)
+    M = step.info().rows
+    xm = torch.empty((max(M, 1), d), dtype=dt, device=DEV)
+    d_x, d_yc = to_dev(x, shape), to_dev(yc, shape)
+    cs = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    copied = [torch.cuda.Event() for _ in range(n_slots)]
+    consumed = [torch.cuda.Event() for _ in range(n_slots)]
+    for e in copied + consumed:
+        e.record(copy)                      # creates the HIP events before the library records them
+    if form == "kv":
+        host = [_pinned(np.asarray(cache[l])[:, shape.n_text:], shape) for l in range(L)]
+        slots = [torch.full((B, T, 2, d), float("nan"), dtype=dt, device=DEV) for _ in range(n_slots)]
+    elif form == "y":
+        host = [_pinned(cache[l], shape) for l in range(L)]
+        slots = [torch.full((B, N, d), float("nan"), dtype=dt, device=DEV) for _ in range(n_slots)]
+        kv_work = torch.full((B, T, 2, d), float("nan"), dtype=dt, device=DEV)
+    elif form == "resident":
+        resident = [to_dev(cache[l], shape) for l in range(L)]
+    else:
+        raise ValueError(form)
+    step.gather_rows(d_x, xm)
+    snaps = []
+    for l in range(L):
+        j = l % n_slots
+        wait = consumed[j] if l >= n_slots else None
+        if form == "kv":
+            step.prefetch_layer(l, host[l], slots[j], copy, wait_event=wait, signal_event=copied[j])
+        elif form == "y":
+            step.prefetch_inputs(l, host[l], slots[j], copy, wait_event=wait, signal_event=copied[j])
+        if form != "resident":
+            cs.wait_event(copied[j])
+        x_in = xm[:M].clone()
+        if form == "kv":
+            kvbuf = slots[j]
+        elif form == "y":
+            step.recompute_kv(l, dw[l], slots[j], kv_work)
+            kvbuf = kv_work
+        else:
+            kvbuf = resident[l]
+        step.block_forward(l, dw[l], xm, kvbuf)
+        snaps.append((x_in, xm[:M].clone(), kvbuf.clone() if keep_kv else None))
+        if form != "resident":
+            consumed[j].record(cs)
+    y = torch.empty((B, T, d), dtype=dt, device=DEV)
+    step.scatter_rows(xm, d_yc, y)
+    torch.cuda.synchronize()
+    out = [(to_np(a), to_np(b), None if c is None else to_np(c)) for a, b, c in snaps]
+    rows = oracle.compact(mask, shape.n_text, shape.dual_stream)["rows"]
+    step.close()
+    return to_np(y), out, rows
+
+
+def request_rows(rows, b, T):
+    """Packed positions and token ids of request b's recomputed rows, in token order."""
+    pos = np.flatnonzero(rows // T == b)
+    toks = rows[pos] % T
+    order = np.argsort(toks, kind="stable")
+    return pos[order], toks[order]
+
+
+def check_blocks(shape, snaps, rows, kv_of_layer, weights, what, *, requests=None, loaded_exact=True):
+    """Each block's output (and fresh K/V rows) against the oracle's block applied to the
+    GPU's own block input, at the one-block bound. ``kv_of_layer(l, b)``: request b's
+    [T][2][d] K/V for the unmasked tokens as the block must see them. ``loaded_exact``:
+    those rows were loaded (K/V caching), so the GPU's working K/V must hold them bit for
+    bit; otherwise they were recomputed (Y caching) and are held to the one-block bound."""
+    T = shape.n_tokens
+    reqs = range(shape.batch) if requests is None else requests
+    for l, (x_in, x_out, kv_gpu) in enumerate(snaps):
+        got, ref, kv_got, kv_ref, un_got, un_ref = [], [], [], [], [], []
+        for b in reqs:
+            pos, toks = request_rows(rows, b, T)
+            if pos.size == 0:
+                continue
+            kv_b = kv_of_layer(l, b)
+            out_b, kvw = oracle.block_rows(x_in[pos], toks, weights[l], kv_b, shape, oracle.bf16_round,
+                                           round_p=True)
+            got.append(x_out[pos])
+            ref.append(out_b)
+            if kv_gpu is None:
+                continue
+            kv_got.append(kv_gpu[b, toks])
+            kv_ref.append(kvw[toks])
+            keep = np.setdiff1d(np.arange(shape.n_text, T), toks)
+            if loaded_exact:
+                np.testing.assert_array_equal(kv_gpu[b, keep], kv_b[keep], err_msg=f"{what} layer {l} request {b}")
+            else:
+                un_got.append(kv_gpu[b, keep])
+                un_ref.append(kv_b[keep])
+        if not got:
+            continue
+        assert_close(np.concatenate(got), np.concatenate(ref), shape.dtype, f"{what} block {l} output", blocks=1)
+        if kv_got:
+            assert_close(np.concatenate(kv_got), np.concatenate(kv_ref), shape.dtype, f"{what} block {l} fresh K/V",
+                         blocks=1)
+        if un_got and sum(a.size for a in un_got):
+            assert_close(np.concatenate(un_got), np.concatenate(un_ref), shape.dtype,
+                         f"{what} block {l} recomputed unmasked K/V", blocks=1)

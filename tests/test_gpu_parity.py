@@ -2,7 +2,10 @@
 
 Index work (compaction, gather, scatter, untouched cache rows) is compared bit
 for bit; floating point within max relative error 1e-4 (fp32) and 2e-2 (bf16)
-in the max norm, plus an element-wise guard (see gpu_helpers).
+in the max norm, and element-wise within the bound for the number of blocks
+between the shared input and the compared tensor (tests/parity_gate). bf16
+references round the softmax weights to bf16 (the oracle's ``round_p``), as
+the matrix units do.
 """
 import numpy as np
 import pytest
@@ -122,12 +125,12 @@ def test_block_fresh_kv_rows_match_oracle():
     ws, xt, kv, yc = _inputs(shape, 21, std=0.05)
     mask = _random_mask(shape, 0.3, 5)
     y, kv_gpu, _ = G.run_stack(shape, mask, xt, kv, yc, ws)
-    y_ref, kv_ref = oracle.masked_stack(xt, mask, kv, yc, ws, shape, return_kv=True)
+    y_ref, kv_ref = oracle.masked_stack(xt, mask, kv, yc, ws, shape, return_kv=True, round_p=True)
     toks = oracle.masked_tokens(mask[0], 0)
     keep = np.setdiff1d(np.arange(shape.n_tokens), toks)
     np.testing.assert_array_equal(kv_gpu[0][0, keep], kv[0][0, keep])
-    G.assert_close(kv_gpu[0][0, toks], kv_ref[0, 0, toks], "bf16", "fresh K/V")
-    G.assert_close(y[0, toks], y_ref[0, toks], "bf16", "block output")
+    G.assert_close(kv_gpu[0][0, toks], kv_ref[0, 0, toks], "bf16", "fresh K/V", blocks=1)
+    G.assert_close(y[0, toks], y_ref[0, toks], "bf16", "block output", blocks=1)
     np.testing.assert_array_equal(y[0, keep], yc[0, keep])
 
 
@@ -142,8 +145,8 @@ def test_c1_fp32_block_matches_oracle():
     x = W.edited_hidden(shape, 1, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
     y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
-    G.assert_close(y, y_ref, "fp32", "c1 output")
-    G.assert_close(kv_gpu[0], kv_ref[0], "fp32", "c1 working K/V")
+    G.assert_close(y, y_ref, "fp32", "c1 output", blocks=1)
+    G.assert_close(kv_gpu[0], kv_ref[0], "fp32", "c1 working K/V", blocks=1)
     keep = mask[0] == 0
     # the cached rows pass through the device's float32 copy of the cache unchanged
     np.testing.assert_array_equal(y[0, keep], yc[0, keep].astype(np.float32))
@@ -155,7 +158,7 @@ def test_c1_own_cache_reproduces_dense():
     ws, xt, kv, yc = _inputs(shape, 1, dense_cache=True, random_ln=True)
     mask = W.workload_mask("c1", shape)
     y, _, _ = G.run_stack(shape, mask, xt, kv, yc, ws)
-    G.assert_close(y, yc, "fp32", "c1 own-cache")
+    G.assert_close(y, yc, "fp32", "c1 own-cache", blocks=1)
 
 
 SMALL_BF16 = [
@@ -179,10 +182,10 @@ def test_small_bf16_stack_matches_oracle(shape, ratio):
     mask = _random_mask(shape, [ratio * (1 - 0.3 * b) for b in range(shape.batch)], 7)
     x = W.edited_hidden(shape, 30, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
-    y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
-    G.assert_close(y, y_ref, "bf16", f"{shape.name} output")
+    y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True, round_p=True)
+    G.assert_close(y, y_ref, "bf16", f"{shape.name} output", blocks=shape.n_layers)
     for l in range(shape.n_layers):
-        G.assert_close(kv_gpu[l], kv_ref[l], "bf16", f"{shape.name} K/V layer {l}")
+        G.assert_close(kv_gpu[l], kv_ref[l], "bf16", f"{shape.name} K/V layer {l}", blocks=l + 1)
     for b in range(shape.batch):
         keep = np.concatenate([np.zeros(shape.n_text, bool), mask[b] == 0])
         np.testing.assert_array_equal(y[b, keep], yc[b, keep])
@@ -205,9 +208,9 @@ def test_step_at_the_accepted_limits_matches_oracle(shape):
     mask = _random_mask(shape, ratio, 23)
     x = W.edited_hidden(shape, 90, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
-    y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
-    G.assert_close(y, y_ref, "bf16", f"{shape.name} output")
-    G.assert_close(kv_gpu[0], kv_ref[0], "bf16", f"{shape.name} K/V")
+    y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True, round_p=True)
+    G.assert_close(y, y_ref, "bf16", f"{shape.name} output", blocks=1)
+    G.assert_close(kv_gpu[0], kv_ref[0], "bf16", f"{shape.name} K/V", blocks=1)
     for b in range(shape.batch):
         keep = np.concatenate([np.zeros(shape.n_text, bool), mask[b] == 0])
         np.testing.assert_array_equal(y[b, keep], yc[b, keep])
@@ -221,10 +224,10 @@ def test_single_masked_token_per_request_matches_oracle():
     assert (mask.sum(1) == 1).all()
     x = W.edited_hidden(shape, 91, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
-    y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
-    G.assert_close(y, y_ref, "bf16", "one token output")
+    y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True, round_p=True)
+    G.assert_close(y, y_ref, "bf16", "one token output", blocks=shape.n_layers)
     for l in range(shape.n_layers):
-        G.assert_close(kv_gpu[l], kv_ref[l], "bf16", f"one token K/V layer {l}")
+        G.assert_close(kv_gpu[l], kv_ref[l], "bf16", f"one token K/V layer {l}", blocks=l + 1)
 
 
 FUSE_SHAPES = [
@@ -244,8 +247,9 @@ def test_split_k_sum_fused_with_layernorm_is_bit_exact(shape, monkeypatch):
     mask = _random_mask(shape, [0.3, 0.1], 17)
     x = W.edited_hidden(shape, 80, xt, mask)
     dt = "bf16" if shape.dtype == "bf16" else "fp32"
-    G.assert_close(G.run_stack(shape, mask, x, kv, yc, ws)[0], oracle.masked_stack(x, mask, kv, yc, ws, shape),
-                   dt, f"{shape.name} fused")
+    G.assert_close(G.run_stack(shape, mask, x, kv, yc, ws)[0],
+                   oracle.masked_stack(x, mask, kv, yc, ws, shape, round_p=True), dt, f"{shape.name} fused",
+                   blocks=shape.n_layers)
     yin = np.stack([np.asarray(yc)[:, shape.n_text:]] * shape.n_layers)
     runs = [dict(), dict(dense_prefix=1), dict(pinned=True), dict(inputs=True, pinned=True)]
     for kw in runs:
@@ -260,12 +264,12 @@ def test_split_k_sum_fused_with_layernorm_is_bit_exact(shape, monkeypatch):
 def test_all_ones_mask_with_poisoned_cache_equals_dense():
     shape = W.ModelShape("ones", 2, 256, 4, 4, 12, 12, dtype="bf16", batch=2)
     ws, xt, _, _ = _inputs(shape, 40, std=0.03)
-    y_ref, _ = oracle.dense_stack(xt, ws, shape)
+    y_ref, _ = oracle.dense_stack(xt, ws, shape, round_p=True)
     ones = np.ones((shape.batch, shape.n_image), np.uint8)
     kv = np.zeros((shape.n_layers, shape.batch, shape.n_tokens, 2, shape.d_model))
     y, _, _ = G.run_stack(shape, ones, xt, kv, None, ws, poison_cache=True)
     assert np.all(np.isfinite(y))
-    G.assert_close(y, y_ref, "bf16", "all-ones")
+    G.assert_close(y, y_ref, "bf16", "all-ones", blocks=shape.n_layers)
 
 
 @pytest.mark.parametrize("aliased", [False, True])
@@ -297,7 +301,7 @@ def test_batch_equals_single_requests(monkeypatch):
             if target:
                 np.testing.assert_array_equal(y1[0], yb[b])
             else:
-                G.assert_close(y1[0], yb[b], "bf16", f"request {b} alone vs in the batch")
+                G.assert_close(y1[0], yb[b], "bf16", f"request {b} alone vs in the batch", blocks=shape.n_layers)
 
 
 # ------------------------------------------------------------------ streamed cache
@@ -318,8 +322,8 @@ def test_streamed_cache_matches_resident_and_serialized(shape):
     y_ser, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, serialize=True)
     np.testing.assert_array_equal(y_pipe, y_res)
     np.testing.assert_array_equal(y_ser, y_res)
-    y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape)
-    G.assert_close(y_res, y_ref, "bf16", f"{shape.name} streamed")
+    y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, round_p=True)
+    G.assert_close(y_res, y_ref, "bf16", f"{shape.name} streamed", blocks=shape.n_layers)
 
 
 def test_streamed_repeated_steps_are_identical():
@@ -349,50 +353,6 @@ def test_streamed_repeated_steps_are_identical():
         assert torch.equal(y, outs[0])
 
 
-# ------------------------------------------------------------------ full-size workloads, sampled
-
-@pytest.mark.parametrize("cfg_key,ratio", [("c2", 0.05), ("c3", 0.05)])
-def test_full_size_stack_sampled_request(cfg_key, ratio):
-    """The workload at full size (all layers, T=4096); request 0's recomputed rows vs the oracle.
-
-    The cache is a seeded random stand-in (the masked computation is defined
-    for any cache contents), so the oracle only runs the masked rows.
-    """
-    shape = W.CONFIGS[cfg_key]
-    if cfg_key == "c3":
-        shape = shape.replace(n_layers=6)   # 6 of the 28 layers keep the oracle within seconds
-    ws, xt, kv, yc = _inputs(shape, W.CONFIG_IDS[cfg_key], random_ln=False)
-    mask = W.workload_mask(cfg_key, shape, ratio=ratio)
-    x = W.edited_hidden(shape, W.CONFIG_IDS[cfg_key], xt, mask)
-    y, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=(cfg_key == "c3"))
-    toks, xm_ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, b=0)
-    G.assert_close(y[0, toks], xm_ref, "bf16", f"{cfg_key} full size")
-    keep = np.setdiff1d(np.arange(shape.n_tokens), toks)
-    np.testing.assert_array_equal(y[0, keep], yc[0, keep])
-
-
-@pytest.mark.parametrize("cfg_key,n_layers,pinned", [("c4", 28, False), ("c5", 2, True)])
-def test_full_size_batched_stack_sampled_request(cfg_key, n_layers, pinned):
-    """The batched workloads at full width, token count and batch, with the workload's own
-    mask draw (per-request ratios; c5 with its text rows and the streamed host cache).
-
-    Every request runs through the packed path; the request with the fewest recomputed
-    rows is checked against the oracle (requests attend only within themselves). c4 runs
-    all 28 layers; c5 two of its 19 (full-width layers), so that the oracle and the input
-    generation stay within seconds.
-    """
-    shape = W.CONFIGS[cfg_key].replace(n_layers=n_layers)
-    ws, xt, kv, yc = _inputs(shape, W.CONFIG_IDS[cfg_key], random_ln=False)
-    mask = W.workload_mask(cfg_key, shape)
-    x = W.edited_hidden(shape, W.CONFIG_IDS[cfg_key], xt, mask)
-    y, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=pinned)
-    b = int(np.argmin(mask.sum(1)))
-    toks, xm_ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, b=b)
-    G.assert_close(y[b, toks], xm_ref, "bf16", f"{cfg_key} full size, request {b}")
-    keep = np.setdiff1d(np.arange(shape.n_tokens), toks)
-    np.testing.assert_array_equal(y[b, keep], yc[b, keep])
-
-
 # ------------------------------------------------------------------ attention key-range split
 
 @pytest.mark.parametrize("hd_shape", [
@@ -406,14 +366,14 @@ def test_attention_split_and_unsplit_match_oracle(hd_shape, monkeypatch):
     ws, xt, kv, yc = _inputs(shape, 60, std=0.03)
     mask = _random_mask(shape, 0.4, 13)
     x = W.edited_hidden(shape, 60, xt, mask)
-    y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape)
+    y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, round_p=True)
     outs = []
     for target in ("1", "100000"):
         monkeypatch.setenv("MS_ATTN_SPLIT_TARGET", target)
         y, _, _ = G.run_stack(shape, mask, x, kv, yc, ws)
-        G.assert_close(y, y_ref, "bf16", f"{shape.name} split target {target}")
+        G.assert_close(y, y_ref, "bf16", f"{shape.name} split target {target}", blocks=1)
         outs.append(y)
-    G.assert_close(outs[1], outs[0], "bf16", "split vs unsplit")
+    G.assert_close(outs[1], outs[0], "bf16", "split vs unsplit", blocks=1)
 
 
 # ------------------------------------------------------------------ dense prefix (bubble-free pipeline)
@@ -432,10 +392,10 @@ def test_dense_prefix_matches_oracle_and_streaming_is_exact(shape):
                      enumerate((0.3, 0.12))])
     x = W.edited_hidden(shape, 70, xt, mask)
     for k in (1, 2, shape.n_layers):
-        y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, dense_prefix=k)
+        y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, dense_prefix=k, round_p=True)
         y_res, _, step = G.run_stack(shape, mask, x, kv, yc, ws, dense_prefix=k)
         assert step.info().dense_prefix == k
-        G.assert_close(y_res, y_ref, "bf16", f"{shape.name} dense prefix {k}")
+        G.assert_close(y_res, y_ref, "bf16", f"{shape.name} dense prefix {k}", blocks=shape.n_layers)
         for n_slots in (1, 2, shape.n_layers):
             y_pipe, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, n_slots=n_slots, dense_prefix=k)
             np.testing.assert_array_equal(y_pipe, y_res, err_msg=f"k={k} slots={n_slots}")
@@ -453,10 +413,10 @@ def test_dense_prefix_own_cache_reproduces_dense():
     shape = PREFIX_SHAPE.replace(batch=1)
     ws = W.stack_weights(shape, 71, random_ln=True, std=0.03)
     xt = W.template_hidden(shape, 71)
-    y_dense, kv_dense = oracle.dense_stack(xt, ws, shape)
+    y_dense, kv_dense = oracle.dense_stack(xt, ws, shape, round_p=True)
     mask = np.stack([W.ellipse_mask(16, 16, 0.25, W.rng(7, 3, 9))])
     y, _, _ = G.run_stack(shape, mask, xt, kv_dense, y_dense, ws, pinned=True, n_slots=4, dense_prefix=2)
-    G.assert_close(y, y_dense, "bf16", "own cache with a dense prefix")
+    G.assert_close(y, y_dense, "bf16", "own cache with a dense prefix", blocks=shape.n_layers)
 
 
 # ------------------------------------------------------------------ Y caching (Sec. 3.1, Fig. 5 bottom)
@@ -468,8 +428,8 @@ Y_DUAL = W.ModelShape("ycache_dual", 3, 256, 2, 4, 8, 16, n_text=16, dual_stream
 def _y_inputs(shape, cfg):
     ws = W.stack_weights(shape, cfg, random_ln=True, std=0.03)
     xt = W.template_hidden(shape, cfg)
-    yin = oracle.dense_inputs(xt, ws, shape)          # the template's cached block inputs
-    yc, _ = oracle.dense_stack(xt, ws, shape)
+    yin = oracle.dense_inputs(xt, ws, shape, round_p=True)   # the template's cached block inputs
+    yc, _ = oracle.dense_stack(xt, ws, shape, round_p=True)
     return ws, xt, yin, yc
 
 
@@ -479,9 +439,9 @@ def test_y_cache_matches_oracle_resident_and_streamed(shape):
     mask = np.stack([W.ellipse_mask(shape.grid_h, shape.grid_w, r, W.rng(3, 6, b)) for b, r in
                      enumerate((0.3, 0.1))])
     x = W.edited_hidden(shape, 60, xt, mask)
-    ref = oracle.masked_stack_y(x, mask, yin, yc, ws, shape)
+    ref = oracle.masked_stack_y(x, mask, yin, yc, ws, shape, round_p=True)
     y_res, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True)
-    G.assert_close(y_res, ref, "bf16", f"{shape.name} Y cache resident")
+    G.assert_close(y_res, ref, "bf16", f"{shape.name} Y cache resident", blocks=shape.n_layers)
     for serialize in (False, True):
         y_pin, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True, pinned=True, serialize=serialize)
         np.testing.assert_array_equal(y_pin, y_res)
@@ -505,8 +465,8 @@ def test_y_cache_reads_no_recomputed_row_and_no_prefix_cache():
             poisoned[:, b, mask[b] != 0] = np.nan
         y, _, _ = G.run_stack(shape, mask, x, poisoned, yc, ws, inputs=True, dense_prefix=k, pinned=True)
         np.testing.assert_array_equal(y, ref)
-        G.assert_close(ref, oracle.masked_stack_y(x, mask, yin, yc, ws, shape, dense_prefix=k), "bf16",
-                       f"Y cache, dense prefix {k}")
+        G.assert_close(ref, oracle.masked_stack_y(x, mask, yin, yc, ws, shape, dense_prefix=k, round_p=True),
+                       "bf16", f"Y cache, dense prefix {k}", blocks=shape.n_layers)
 
 
 def test_y_cache_own_cache_is_dense_and_all_masked_reads_nothing():
@@ -515,7 +475,7 @@ def test_y_cache_own_cache_is_dense_and_all_masked_reads_nothing():
     mask = _random_mask(shape, 0.3, 13)
     y_dense = yc                                         # own cache: the current input is the template
     y, _, _ = G.run_stack(shape, mask, xt, yin, yc, ws, inputs=True)
-    G.assert_close(y, y_dense, "bf16", "Y own cache vs dense")
+    G.assert_close(y, y_dense, "bf16", "Y own cache vs dense", blocks=shape.n_layers)
     ones = np.ones_like(mask)
     y1, _, _ = G.run_stack(shape, ones, xt, np.full_like(yin, np.nan), None, ws, inputs=True)
-    G.assert_close(y1, y_dense, "bf16", "all masked, Y cache never read")
+    G.assert_close(y1, y_dense, "bf16", "all masked, Y cache never read", blocks=shape.n_layers)

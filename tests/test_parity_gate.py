@@ -1,0 +1,146 @@
+"""The per-block bf16 gate (tests/parity_gate) admits a correct implementation in
+another precision and rejects plausible mistakes.
+
+* A correct block evaluated the way the matrix units do it (float32
+  accumulation, bf16 rounding at the same storage points, online softmax over
+  64-key tiles with a running maximum that is only raised when it grows by more
+  than 2^8, softmax weights rounded to bf16 against that running maximum, the
+  normaliser summed from the same rounded weights) stays within 2e-2
+  element-wise of the oracle with ``round_p``, for head_dim 64 / 72 / 128.
+* The oracle with a planted mistake (on the CPU: a dropped ragged key tail, the
+  softmax scale of a padded head_dim, keys misaligned with their values by one
+  token, a dropped out-projection bias) fails the same gate against the
+  unaltered oracle.
+
+Inputs as in the GPU per-block tests: weights N(0, 0.08), random LayerNorm
+affine parameters, hidden states N(0, 1), a random cache.
+"""
+import numpy as np
+import pytest
+from scipy.special import erf
+
+import oracle
+from oracle import stack as OS
+from paper_2505_20600_amd import workloads as W
+from tests import parity_gate as PG
+
+STD = 0.08
+SHAPES = [
+    W.ModelShape("hd64_T256", 1, 256, 4, 4, 16, 16, dtype="bf16"),
+    W.ModelShape("hd72_T144", 1, 576, 8, 4, 12, 12, dtype="bf16"),
+    W.ModelShape("hd128_T192", 1, 256, 2, 4, 12, 16, dtype="bf16"),
+]
+RATIOS = (0.05, 0.45, 1.0)
+
+
+def _b16(a):
+    return OS.bf16_round(np.asarray(a, np.float64)).astype(np.float32)
+
+
+def _ln32(x, g, b, eps):
+    mu = x.mean(-1, keepdims=True, dtype=np.float32)
+    var = ((x - mu) ** 2).mean(-1, keepdims=True, dtype=np.float32)
+    return (x - mu) / np.sqrt(var + np.float32(eps)) * g + b
+
+
+def _attention32(q, k, v, scale, tile=64, lazy_log2=8.0):
+    c = np.float32(scale * np.log2(np.e))
+    m = np.full(q.shape[0], -np.inf, np.float32)
+    l = np.zeros(q.shape[0], np.float32)
+    o = np.zeros((q.shape[0], v.shape[1]), np.float32)
+    for t0 in range(0, k.shape[0], tile):
+        s = q @ k[t0:t0 + tile].T
+        m_new = np.maximum(m, s.max(1))
+        if np.any((m_new - m) * c > lazy_log2):
+            corr = np.where(np.isinf(m), 0.0, np.exp2((m - m_new) * c)).astype(np.float32)
+            o *= corr[:, None]
+            l *= corr
+            m = m_new
+        p = _b16(np.exp2(s * c - (m * c)[:, None]))
+        l += p.sum(1)
+        o += p @ v[t0:t0 + tile]
+    return o / l[:, None]
+
+
+def _block32(x, toks, w, kv_b, shape):
+    """One block in float32 with bf16 storage points (an implementation other than the oracle)."""
+    f = {k: np.asarray(v, np.float32) for k, v in w.items()}
+    d, h = shape.d_model, shape.n_heads
+    hd = d // h
+    a = _b16(_ln32(np.asarray(x, np.float32), f["ln1_g"], f["ln1_b"], shape.ln_eps))
+    qkv = _b16(a @ f["w_qkv"].T + f["b_qkv"])
+    kv = np.array(kv_b, np.float32)
+    kv[toks, 0], kv[toks, 1] = qkv[:, d:2 * d], qkv[:, 2 * d:]
+    o = np.empty((len(toks), d), np.float32)
+    for j in range(h):
+        c = slice(j * hd, (j + 1) * hd)
+        o[:, c] = _attention32(qkv[:, c], kv[:, 0, c], kv[:, 1, c], 1.0 / np.sqrt(hd))
+    hh = _b16(np.asarray(x, np.float32) + _b16(o) @ f["w_o"].T + f["b_o"])
+    pre = _b16(_ln32(hh, f["ln2_g"], f["ln2_b"], shape.ln_eps)) @ f["w_1"].T + f["b_1"]
+    u = _b16(pre * np.float32(0.5) * (1 + erf(pre / np.sqrt(2)).astype(np.float32)))
+    return _b16(hh + u @ f["w_2"].T + f["b_2"])
+
+
+def _case(shape, ratio):
+    ws = W.stack_weights(shape, 33, random_ln=True, std=STD)
+    x = W.template_hidden(shape, 33)[0]
+    kv = W.synthetic_kv_cache(shape, 33, 0)[0]
+    n = shape.n_image
+    toks = np.sort(np.random.default_rng(5).choice(n, max(1, int(round(ratio * n))), replace=False))
+    return ws[0], x[toks], toks, kv
+
+
+def _ref(w, x, toks, kv, shape):
+    return oracle.block_rows(x, toks, w, kv, shape, oracle.bf16_round, round_p=True)[0]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
+@pytest.mark.parametrize("ratio", RATIOS)
+def test_float32_block_passes_the_block_gate(shape, ratio):
+    w, x, toks, kv = _case(shape, ratio)
+    ok, e1, e2, lim = PG.check(_block32(x, toks, w, kv, shape), _ref(w, x, toks, kv, shape), "bf16", 1)
+    assert ok, (e1, e2, lim)
+
+
+def _planted(name, shape):
+    """attention_head replacements (and weight edits) that each plant one mistake."""
+    orig = OS.attention_head
+    hd = shape.head_dim
+    T = shape.n_tokens
+    tail = T % 64 or 16
+    if name == "dropped key tail":
+        return lambda q, k, v, s, rp=False: orig(q, k[:T - tail], v[:T - tail], s, rp), None
+    if name == "padded head_dim scale":
+        pad = (hd + 15) // 16 * 16 if hd % 16 else hd + 16
+        return lambda q, k, v, s, rp=False: orig(q, k, v, 1.0 / np.sqrt(pad), rp), None
+    if name == "keys one token off":
+        return lambda q, k, v, s, rp=False: orig(q, np.roll(k, 1, axis=0), v, s, rp), None
+    if name == "out-projection bias dropped":
+        return orig, "b_o"
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
+@pytest.mark.parametrize("mistake", ["dropped key tail", "padded head_dim scale", "keys one token off",
+                                     "out-projection bias dropped"])
+def test_planted_mistake_fails_the_block_gate(shape, mistake, monkeypatch):
+    for ratio in RATIOS:
+        w, x, toks, kv = _case(shape, ratio)
+        good = _ref(w, x, toks, kv, shape)
+        fn, zero = _planted(mistake, shape)
+        monkeypatch.setattr(OS, "attention_head", fn)
+        wb = dict(w)
+        if zero:
+            wb[zero] = np.zeros_like(w[zero])
+        bad = _ref(wb, x, toks, kv, shape)
+        monkeypatch.setattr(OS, "attention_head", oracle.attention_head)
+        ok, e1, e2, lim = PG.check(bad, good, "bf16", 1)
+        assert not ok, f"{mistake} at ratio {ratio} passed: {e1:.3e} / {e2:.3e}"
+
+
+def test_stack_bound_grows_per_block():
+    assert PG.elem_tol("bf16", 1) == 2e-2
+    assert PG.elem_tol("bf16", 3) == pytest.approx(6e-2)
+    assert PG.elem_tol("fp32", 1) == 1e-4
+    with pytest.raises(ValueError):
+        PG.elem_tol("bf16", 0)
