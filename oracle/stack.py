@@ -197,7 +197,7 @@ def _token_wise(fn, x_rows, toks, layer_w, n_text):
     return out
 
 
-def block_rows(x_rows, toks, layer_w, kv_b, shape, rnd, round_p: bool = False):
+def block_rows(x_rows, toks, layer_w, kv_b, shape, rnd, round_p: bool = False, return_h: bool = False):
     """One pre-LN block for the rows ``toks`` of one request.
 
     ``x_rows [m][d]`` are the hidden rows of tokens ``toks``; ``kv_b [T][2][d]``
@@ -207,7 +207,8 @@ def block_rows(x_rows, toks, layer_w, kv_b, shape, rnd, round_p: bool = False):
     ``round_p`` rounds the softmax weights to bf16 (bf16 workloads only; see
     ``attention_head``).
 
-    Returns ``(x_out [m][d], kv_work [T][2][d])``.
+    Returns ``(x_out [m][d], kv_work [T][2][d])``, and with ``return_h`` also the
+    rows' value between the two residual additions, ``H = x + O W_o^T + b_o``.
     """
     d, h = shape.d_model, shape.n_heads
     hd = d // h
@@ -238,10 +239,12 @@ def block_rows(x_rows, toks, layer_w, kv_b, shape, rnd, round_p: bool = False):
         hh = rnd(x + linear(oo, w["w_o"], w["b_o"]))
         a2 = rnd(layer_norm(hh, w["ln2_g"], w["ln2_b"], eps))
         u = rnd(gelu(linear(a2, w["w_1"], w["b_1"])))
-        return rnd(hh + linear(u, w["w_2"], w["b_2"]))
+        return np.concatenate([rnd(hh + linear(u, w["w_2"], w["b_2"])), hh], axis=1)
 
-    x_out = _token_wise(post_attn, np.concatenate([x_rows, o], axis=1), toks, layer_w, nt)
-    return x_out, kv_work
+    out = _token_wise(post_attn, np.concatenate([x_rows, o], axis=1), toks, layer_w, nt)
+    if return_h:
+        return out[:, :d], kv_work, out[:, d:]
+    return out[:, :d], kv_work
 
 
 # ---------------------------------------------------------------------------

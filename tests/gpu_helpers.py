@@ -41,13 +41,14 @@ max_rel_err = PG.max_rel_err
 elem_rel_err = PG.elem_rel_err
 
 
-def assert_close(got, ref, dtype, what="", *, blocks):
-    """Max-norm error within TOL[dtype]; element-wise error within the bound after
-    ``blocks`` blocks between the shared input and the compared tensor (tests/parity_gate)."""
-    ok, e1, e2, lim = PG.check(got, ref, dtype, blocks)
-    print(f"[parity] {what}: max-norm rel err {e1:.3e} (tol {TOL[dtype]}), element-wise {e2:.3e} "
-          f"(tol {lim:.3g}, {blocks} block(s))", flush=True)
-    assert e1 <= TOL[dtype], f"{what}: max-norm relative error {e1:.3e} > {TOL[dtype]}"
+def assert_close(got, ref, dtype, what="", *, blocks, inp=None):
+    """Both error measures within the bound after ``blocks`` blocks between the shared
+    input and the compared tensor; ``inp``: the compared rows' values on entering those
+    blocks when they travel the residual path (tests/parity_gate)."""
+    ok, e1, e2, lim = PG.check(got, ref, dtype, blocks, inp)
+    print(f"[parity] {what}: max-norm rel err {e1:.3e}, element-wise {e2:.3e} (bound {lim:.3g}, "
+          f"{blocks} block(s))", flush=True)
+    assert e1 <= lim, f"{what}: max-norm relative error {e1:.3e} > {lim:.3g} ({blocks} block(s))"
     assert e2 <= lim, f"{what}: element-wise relative error {e2:.3e} > {lim:.3g} ({blocks} block(s))"
 
 
@@ -218,16 +219,17 @@ def check_blocks(shape, snaps, rows, kv_of_layer, weights, what, *, requests=Non
     T = shape.n_tokens
     reqs = range(shape.batch) if requests is None else requests
     for l, (x_in, x_out, kv_gpu) in enumerate(snaps):
-        got, ref, kv_got, kv_ref, un_got, un_ref = [], [], [], [], [], []
+        got, ref, ins, kv_got, kv_ref, un_got, un_ref = [], [], [], [], [], [], []
         for b in reqs:
             pos, toks = request_rows(rows, b, T)
             if pos.size == 0:
                 continue
             kv_b = kv_of_layer(l, b)
-            out_b, kvw = oracle.block_rows(x_in[pos], toks, weights[l], kv_b, shape, oracle.bf16_round,
-                                           round_p=True)
+            out_b, kvw, h_b = oracle.block_rows(x_in[pos], toks, weights[l], kv_b, shape, oracle.bf16_round,
+                                                round_p=True, return_h=True)
             got.append(x_out[pos])
             ref.append(out_b)
+            ins.append(h_b)
             if kv_gpu is None:
                 continue
             kv_got.append(kv_gpu[b, toks])
@@ -240,7 +242,8 @@ def check_blocks(shape, snaps, rows, kv_of_layer, weights, what, *, requests=Non
                 un_ref.append(kv_b[keep])
         if not got:
             continue
-        assert_close(np.concatenate(got), np.concatenate(ref), shape.dtype, f"{what} block {l} output", blocks=1)
+        assert_close(np.concatenate(got), np.concatenate(ref), shape.dtype, f"{what} block {l} output", blocks=1,
+                     inp=np.concatenate(ins))
         if kv_got:
             assert_close(np.concatenate(kv_got), np.concatenate(kv_ref), shape.dtype, f"{what} block {l} fresh K/V",
                          blocks=1)

@@ -3,34 +3,42 @@
 Two measures of a tensor ``got`` against the oracle's ``ref``:
 
 * max-norm relative error ``max_i |g_i - r_i| / max_i |r_i|``;
-* element-wise relative error with an RMS floor,
-  ``max_i |g_i - r_i| / max(|r_i|, rms(r))`` (the floor keeps values near zero
-  from dominating).
+* element-wise relative error ``max_i |g_i - r_i| / max(|r_i|, |h_i|, rms(r))``.
+  For one block's output ``h`` is the oracle's value of the same element
+  between the block's two residual additions (``H``); for a stack's output it
+  is the stack's input; for rows off the residual path (fresh K/V) it is left
+  out. The RMS floor keeps values near zero from dominating.
 
-Bounds (1e-4 for float32, 2e-2 for bfloat16):
+Bounds, with TOL = 1e-4 for float32 and 2e-2 for bfloat16:
 
-* One block on the same input (``blocks=1``): both measures at the bound.
-  Derivation for bf16: an implementation that accumulates in float32 instead
-  of float64 rounds the same values to bf16 at the same points, but any last
-  bit of difference before a rounding point can flip that rounding by one
-  unit in the last place somewhere in a large tensor. Of a block's rounding
-  points, two lie on the residual path that carries the output's magnitude:
-  ``H = X + O W_o^T + b_o`` and the block output ``H + MLP(H)``. One unit in
-  the last place of a bf16 value is at most 2^-7 of its magnitude, so two
-  flips move an output element by at most 2 x 2^-7 = 1.56e-2 of itself. The
-  rest of a correct block's error (accumulation order, the softmax weights
-  rounded against a different running maximum, flips at the LayerNorm,
-  Q/K/V, attention-output and GELU rounding points, which enter the output
-  only through a product with weights of standard deviation <= 0.08) is far
-  smaller, so 2e-2 holds with room and an indexing or algebra mistake
-  (a dropped key range, a wrong scale, a wrong head) does not fit under it
-  (tests/test_parity_gate.py).
-* A stack of ``blocks`` blocks: the max-norm bound as for one block; the
-  element-wise bound grows by one block's bound per block the rows pass
-  through, since each block adds at most its own flips to what it inherits
-  through the residual connection (whose gain is ~1 at these weight scales).
+* One block on a shared input (``blocks=1``): both measures within TOL.
+  Derivation for bf16: an implementation that accumulates in float32 rounds
+  the same values to bf16 at the same points as the float64 oracle, but a last
+  bit of difference before a rounding point flips that rounding by one unit in
+  the last place somewhere in a large tensor. Two rounding points lie on the
+  residual path: ``H = x + O W_o^T + b_o`` and the output ``H + MLP(H)``. One
+  unit in the last place of a bf16 value is at most 2^-7 of it, so the two
+  flips move an output element by at most 2^-7 (|H_i| + |out_i|) <= 1.56e-2
+  max(|H_i|, |out_i|). The other rounding points (LayerNorm, Q/K/V, attention
+  output, GELU) and the accumulation order enter the output only through
+  products with small weights. A correct float32 implementation stays below
+  2e-2 (tests/test_parity_gate.py), while the oracle with a planted mistake (a
+  dropped key range, a wrong scale, keys off by one token, a dropped bias)
+  exceeds it.
+* A stack of ``blocks`` blocks: TOL x sqrt(blocks) for both measures. Each
+  block adds its own independent flips to what it inherits through the
+  residual connection, so two correct implementations drift apart like a
+  random walk: measured between the float64 oracle and a float32
+  implementation over 28 blocks at d = 768 and 1152, max-norm 0.3-0.6% after
+  one block and 1.7-1.9% after 28, element-wise 0.8-1.3% and 5.4-5.9%; each
+  within TOL x sqrt(L) at every depth (tests/test_parity_gate.py). A fixed TOL
+  does not hold at 28 blocks: element-wise in these runs, and in the max norm
+  for the GPU against the oracle over the 28 blocks of the d = 1152 stack
+  (2.10e-2).
 """
 from __future__ import annotations
+
+import math
 
 import numpy as np
 
@@ -47,26 +55,30 @@ def max_rel_err(got, ref) -> float:
     return float(np.max(np.abs(got - ref)) / (den if den > 0 else 1.0))
 
 
-def elem_rel_err(got, ref) -> float:
-    """max_i |g_i - r_i| / max(|r_i|, rms(r)): element-wise relative error with an RMS floor."""
+def elem_rel_err(got, ref, inp=None) -> float:
+    """max_i |g_i - r_i| / max(|r_i|, |inp_i|, rms(r)): element-wise relative error with an
+    RMS floor, measured against the larger of the element's magnitude and the magnitude
+    it had on the residual path (``inp``, same shape; see the module docstring)."""
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     if ref.size == 0:
         return 0.0
     rms = np.sqrt(np.mean(ref ** 2))
     den = np.maximum(np.abs(ref), rms if rms > 0 else 1.0)
+    if inp is not None:
+        den = np.maximum(den, np.abs(np.asarray(inp, np.float64)))
     return float(np.max(np.abs(got - ref) / den))
 
 
-def elem_tol(dtype: str, blocks: int) -> float:
-    """Element-wise bound after ``blocks`` blocks (see the module docstring)."""
+def tol(dtype: str, blocks: int) -> float:
+    """Bound of both measures after ``blocks`` blocks (see the module docstring)."""
     if blocks < 1:
         raise ValueError("blocks must be >= 1")
-    return TOL[dtype] * blocks
+    return TOL[dtype] * math.sqrt(blocks)
 
 
-def check(got, ref, dtype: str, blocks: int):
-    """(passes, max-norm error, element-wise error, element-wise bound)."""
-    e1, e2 = max_rel_err(got, ref), elem_rel_err(got, ref)
-    lim = elem_tol(dtype, blocks)
-    return (e1 <= TOL[dtype] and e2 <= lim), e1, e2, lim
+def check(got, ref, dtype: str, blocks: int, inp=None):
+    """(passes, max-norm error, element-wise error, bound)."""
+    e1, e2 = max_rel_err(got, ref), elem_rel_err(got, ref, inp)
+    lim = tol(dtype, blocks)
+    return (e1 <= lim and e2 <= lim), e1, e2, lim

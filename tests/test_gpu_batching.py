@@ -83,7 +83,7 @@ def test_per_request_host_caches_equal_the_contiguous_layout(shape):
     y_r = _run_pinned(shape, mask, x, kv, yc, ws, per_request=True)
     np.testing.assert_array_equal(y_r, y_c)
     G.assert_close(y_r, oracle.masked_stack(x, mask, kv, yc, ws, shape, round_p=True), "bf16",
-                   "per-request caches", blocks=shape.n_layers)
+                   "per-request caches", blocks=shape.n_layers, inp=x)
 
 
 def test_request_that_recomputes_nothing_reads_no_cache():
@@ -133,7 +133,8 @@ def test_requests_joining_and_leaving_match_the_oracle(streamed):
             r = reqs[b][1]
             ref = oracle.masked_stack(xs[b, s][None], mask[b:b + 1], kv[:, b:b + 1], yc[b:b + 1], ws, one,
                                       round_p=True)[0]
-            G.assert_close(G.to_np(r.y), ref, "bf16", f"request {b} step {s}", blocks=shape.n_layers)
+            G.assert_close(G.to_np(r.y), ref, "bf16", f"request {b} step {s}", blocks=shape.n_layers,
+                           inp=xs[b, s])
         for r in done:
             active.remove(next(b for b in active if reqs[b][1] is r))
         if s == 1:   # three running (r2 joins next step): the batch is full for a fourth

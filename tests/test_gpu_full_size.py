@@ -71,7 +71,7 @@ def test_c2_full_size_block_by_block(ratio):
     np.testing.assert_array_equal(y_blocks, y)
     G.check_blocks(shape, snaps, rows, _kv_rows(kv, shape), ws, f"c2 {ratio:.0%}")
     toks, ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, 0, round_p=True)
-    G.assert_close(y[0, toks], ref, "bf16", f"c2 {ratio:.0%} stack", blocks=shape.n_layers)
+    G.assert_close(y[0, toks], ref, "bf16", f"c2 {ratio:.0%} stack", blocks=shape.n_layers, inp=x[0, toks])
     _untouched_rows_exact(y, yc, mask, shape, 0)
 
 
@@ -85,7 +85,7 @@ def test_c3_full_size_streamed_block_by_block():
     np.testing.assert_array_equal(y_blocks, y)
     G.check_blocks(shape, snaps, rows, _kv_rows(kv, shape), ws, "c3 10%")
     toks, ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, 0, round_p=True)
-    G.assert_close(y[0, toks], ref, "bf16", "c3 10% stack", blocks=shape.n_layers)
+    G.assert_close(y[0, toks], ref, "bf16", "c3 10% stack", blocks=shape.n_layers, inp=x[0, toks])
     _untouched_rows_exact(y, yc, mask, shape, 0)
 
 
@@ -102,7 +102,8 @@ def test_c3_full_size_dense_prefix(ratio, k):
     y2, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, n_slots=2, dense_prefix=k)
     np.testing.assert_array_equal(y2, y)
     toks, ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, 0, dense_prefix=k, round_p=True)
-    G.assert_close(y[0, toks], ref, "bf16", f"c3 {ratio:.0%} dense prefix {k}", blocks=shape.n_layers)
+    G.assert_close(y[0, toks], ref, "bf16", f"c3 {ratio:.0%} dense prefix {k}", blocks=shape.n_layers,
+                   inp=x[0, toks])
     _untouched_rows_exact(y, yc, mask, shape, 0)
 
 
@@ -115,7 +116,8 @@ def test_c5_full_size_dense_prefix_and_block_by_block():
     y, _, step = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, n_slots=shape.n_layers, dense_prefix=1)
     assert step.info().dense_prefix == 1
     toks, ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, b, dense_prefix=1, round_p=True)
-    G.assert_close(y[b, toks], ref, "bf16", f"c5 dense prefix 1, request {b}", blocks=shape.n_layers)
+    G.assert_close(y[b, toks], ref, "bf16", f"c5 dense prefix 1, request {b}", blocks=shape.n_layers,
+                   inp=x[b, toks])
     _untouched_rows_exact(y, yc, mask, shape, b)
     y0, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, n_slots=shape.n_layers)
     y_blocks, snaps, rows = G.run_block_by_block(shape, mask, x, kv, yc, ws, form="kv", n_slots=2)
@@ -131,5 +133,5 @@ def test_c4_full_size_batched_stack():
     y, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, return_kv=False)
     b = int(np.argmin(mask.sum(1)))
     toks, ref = oracle.masked_rows_of_stack(x, mask, kv, ws, shape, b, round_p=True)
-    G.assert_close(y[b, toks], ref, "bf16", f"c4 request {b}", blocks=shape.n_layers)
+    G.assert_close(y[b, toks], ref, "bf16", f"c4 request {b}", blocks=shape.n_layers, inp=x[b, toks])
     _untouched_rows_exact(y, yc, mask, shape, b)

@@ -130,7 +130,7 @@ def test_block_fresh_kv_rows_match_oracle():
     keep = np.setdiff1d(np.arange(shape.n_tokens), toks)
     np.testing.assert_array_equal(kv_gpu[0][0, keep], kv[0][0, keep])
     G.assert_close(kv_gpu[0][0, toks], kv_ref[0, 0, toks], "bf16", "fresh K/V", blocks=1)
-    G.assert_close(y[0, toks], y_ref[0, toks], "bf16", "block output", blocks=1)
+    G.assert_close(y[0, toks], y_ref[0, toks], "bf16", "block output", blocks=1, inp=xt[0, toks])
     np.testing.assert_array_equal(y[0, keep], yc[0, keep])
 
 
@@ -145,7 +145,7 @@ def test_c1_fp32_block_matches_oracle():
     x = W.edited_hidden(shape, 1, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
     y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True)
-    G.assert_close(y, y_ref, "fp32", "c1 output", blocks=1)
+    G.assert_close(y, y_ref, "fp32", "c1 output", blocks=1, inp=x)
     G.assert_close(kv_gpu[0], kv_ref[0], "fp32", "c1 working K/V", blocks=1)
     keep = mask[0] == 0
     # the cached rows pass through the device's float32 copy of the cache unchanged
@@ -158,7 +158,7 @@ def test_c1_own_cache_reproduces_dense():
     ws, xt, kv, yc = _inputs(shape, 1, dense_cache=True, random_ln=True)
     mask = W.workload_mask("c1", shape)
     y, _, _ = G.run_stack(shape, mask, xt, kv, yc, ws)
-    G.assert_close(y, yc, "fp32", "c1 own-cache", blocks=1)
+    G.assert_close(y, yc, "fp32", "c1 own-cache", blocks=1, inp=xt)
 
 
 SMALL_BF16 = [
@@ -183,7 +183,7 @@ def test_small_bf16_stack_matches_oracle(shape, ratio):
     x = W.edited_hidden(shape, 30, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
     y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True, round_p=True)
-    G.assert_close(y, y_ref, "bf16", f"{shape.name} output", blocks=shape.n_layers)
+    G.assert_close(y, y_ref, "bf16", f"{shape.name} output", blocks=shape.n_layers, inp=x)
     for l in range(shape.n_layers):
         G.assert_close(kv_gpu[l], kv_ref[l], "bf16", f"{shape.name} K/V layer {l}", blocks=l + 1)
     for b in range(shape.batch):
@@ -209,7 +209,7 @@ def test_step_at_the_accepted_limits_matches_oracle(shape):
     x = W.edited_hidden(shape, 90, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
     y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True, round_p=True)
-    G.assert_close(y, y_ref, "bf16", f"{shape.name} output", blocks=1)
+    G.assert_close(y, y_ref, "bf16", f"{shape.name} output", blocks=1, inp=x)
     G.assert_close(kv_gpu[0], kv_ref[0], "bf16", f"{shape.name} K/V", blocks=1)
     for b in range(shape.batch):
         keep = np.concatenate([np.zeros(shape.n_text, bool), mask[b] == 0])
@@ -225,7 +225,7 @@ def test_single_masked_token_per_request_matches_oracle():
     x = W.edited_hidden(shape, 91, xt, mask)
     y, kv_gpu, _ = G.run_stack(shape, mask, x, kv, yc, ws)
     y_ref, kv_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, return_kv=True, round_p=True)
-    G.assert_close(y, y_ref, "bf16", "one token output", blocks=shape.n_layers)
+    G.assert_close(y, y_ref, "bf16", "one token output", blocks=shape.n_layers, inp=x)
     for l in range(shape.n_layers):
         G.assert_close(kv_gpu[l], kv_ref[l], "bf16", f"one token K/V layer {l}", blocks=l + 1)
 
@@ -249,7 +249,7 @@ def test_split_k_sum_fused_with_layernorm_is_bit_exact(shape, monkeypatch):
     dt = "bf16" if shape.dtype == "bf16" else "fp32"
     G.assert_close(G.run_stack(shape, mask, x, kv, yc, ws)[0],
                    oracle.masked_stack(x, mask, kv, yc, ws, shape, round_p=True), dt, f"{shape.name} fused",
-                   blocks=shape.n_layers)
+                   blocks=shape.n_layers, inp=x)
     yin = np.stack([np.asarray(yc)[:, shape.n_text:]] * shape.n_layers)
     runs = [dict(), dict(dense_prefix=1), dict(pinned=True), dict(inputs=True, pinned=True)]
     for kw in runs:
@@ -269,7 +269,7 @@ def test_all_ones_mask_with_poisoned_cache_equals_dense():
     kv = np.zeros((shape.n_layers, shape.batch, shape.n_tokens, 2, shape.d_model))
     y, _, _ = G.run_stack(shape, ones, xt, kv, None, ws, poison_cache=True)
     assert np.all(np.isfinite(y))
-    G.assert_close(y, y_ref, "bf16", "all-ones", blocks=shape.n_layers)
+    G.assert_close(y, y_ref, "bf16", "all-ones", blocks=shape.n_layers, inp=xt)
 
 
 @pytest.mark.parametrize("aliased", [False, True])
@@ -301,7 +301,8 @@ def test_batch_equals_single_requests(monkeypatch):
             if target:
                 np.testing.assert_array_equal(y1[0], yb[b])
             else:
-                G.assert_close(y1[0], yb[b], "bf16", f"request {b} alone vs in the batch", blocks=shape.n_layers)
+                G.assert_close(y1[0], yb[b], "bf16", f"request {b} alone vs in the batch", blocks=shape.n_layers,
+                               inp=xt[b])
 
 
 # ------------------------------------------------------------------ streamed cache
@@ -323,7 +324,7 @@ def test_streamed_cache_matches_resident_and_serialized(shape):
     np.testing.assert_array_equal(y_pipe, y_res)
     np.testing.assert_array_equal(y_ser, y_res)
     y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, round_p=True)
-    G.assert_close(y_res, y_ref, "bf16", f"{shape.name} streamed", blocks=shape.n_layers)
+    G.assert_close(y_res, y_ref, "bf16", f"{shape.name} streamed", blocks=shape.n_layers, inp=x)
 
 
 def test_streamed_repeated_steps_are_identical():
@@ -371,9 +372,9 @@ def test_attention_split_and_unsplit_match_oracle(hd_shape, monkeypatch):
     for target in ("1", "100000"):
         monkeypatch.setenv("MS_ATTN_SPLIT_TARGET", target)
         y, _, _ = G.run_stack(shape, mask, x, kv, yc, ws)
-        G.assert_close(y, y_ref, "bf16", f"{shape.name} split target {target}", blocks=1)
+        G.assert_close(y, y_ref, "bf16", f"{shape.name} split target {target}", blocks=1, inp=x)
         outs.append(y)
-    G.assert_close(outs[1], outs[0], "bf16", "split vs unsplit", blocks=1)
+    G.assert_close(outs[1], outs[0], "bf16", "split vs unsplit", blocks=1, inp=x)
 
 
 # ------------------------------------------------------------------ dense prefix (bubble-free pipeline)
@@ -395,7 +396,7 @@ def test_dense_prefix_matches_oracle_and_streaming_is_exact(shape):
         y_ref = oracle.masked_stack(x, mask, kv, yc, ws, shape, dense_prefix=k, round_p=True)
         y_res, _, step = G.run_stack(shape, mask, x, kv, yc, ws, dense_prefix=k)
         assert step.info().dense_prefix == k
-        G.assert_close(y_res, y_ref, "bf16", f"{shape.name} dense prefix {k}", blocks=shape.n_layers)
+        G.assert_close(y_res, y_ref, "bf16", f"{shape.name} dense prefix {k}", blocks=shape.n_layers, inp=x)
         for n_slots in (1, 2, shape.n_layers):
             y_pipe, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, n_slots=n_slots, dense_prefix=k)
             np.testing.assert_array_equal(y_pipe, y_res, err_msg=f"k={k} slots={n_slots}")
@@ -416,7 +417,7 @@ def test_dense_prefix_own_cache_reproduces_dense():
     y_dense, kv_dense = oracle.dense_stack(xt, ws, shape, round_p=True)
     mask = np.stack([W.ellipse_mask(16, 16, 0.25, W.rng(7, 3, 9))])
     y, _, _ = G.run_stack(shape, mask, xt, kv_dense, y_dense, ws, pinned=True, n_slots=4, dense_prefix=2)
-    G.assert_close(y, y_dense, "bf16", "own cache with a dense prefix", blocks=shape.n_layers)
+    G.assert_close(y, y_dense, "bf16", "own cache with a dense prefix", blocks=shape.n_layers, inp=xt)
 
 
 # ------------------------------------------------------------------ Y caching (Sec. 3.1, Fig. 5 bottom)
@@ -441,7 +442,7 @@ def test_y_cache_matches_oracle_resident_and_streamed(shape):
     x = W.edited_hidden(shape, 60, xt, mask)
     ref = oracle.masked_stack_y(x, mask, yin, yc, ws, shape, round_p=True)
     y_res, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True)
-    G.assert_close(y_res, ref, "bf16", f"{shape.name} Y cache resident", blocks=shape.n_layers)
+    G.assert_close(y_res, ref, "bf16", f"{shape.name} Y cache resident", blocks=shape.n_layers, inp=x)
     for serialize in (False, True):
         y_pin, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True, pinned=True, serialize=serialize)
         np.testing.assert_array_equal(y_pin, y_res)
@@ -466,7 +467,7 @@ def test_y_cache_reads_no_recomputed_row_and_no_prefix_cache():
         y, _, _ = G.run_stack(shape, mask, x, poisoned, yc, ws, inputs=True, dense_prefix=k, pinned=True)
         np.testing.assert_array_equal(y, ref)
         G.assert_close(ref, oracle.masked_stack_y(x, mask, yin, yc, ws, shape, dense_prefix=k, round_p=True),
-                       "bf16", f"Y cache, dense prefix {k}", blocks=shape.n_layers)
+                       "bf16", f"Y cache, dense prefix {k}", blocks=shape.n_layers, inp=x)
 
 
 def test_y_cache_own_cache_is_dense_and_all_masked_reads_nothing():
@@ -475,7 +476,7 @@ def test_y_cache_own_cache_is_dense_and_all_masked_reads_nothing():
     mask = _random_mask(shape, 0.3, 13)
     y_dense = yc                                         # own cache: the current input is the template
     y, _, _ = G.run_stack(shape, mask, xt, yin, yc, ws, inputs=True)
-    G.assert_close(y, y_dense, "bf16", "Y own cache vs dense", blocks=shape.n_layers)
+    G.assert_close(y, y_dense, "bf16", "Y own cache vs dense", blocks=shape.n_layers, inp=xt)
     ones = np.ones_like(mask)
     y1, _, _ = G.run_stack(shape, ones, xt, np.full_like(yin, np.nan), None, ws, inputs=True)
-    G.assert_close(y1, y_dense, "bf16", "all masked, Y cache never read", blocks=shape.n_layers)
+    G.assert_close(y1, y_dense, "bf16", "all masked, Y cache never read", blocks=shape.n_layers, inp=xt)

@@ -91,14 +91,17 @@ def _case(shape, ratio):
 
 
 def _ref(w, x, toks, kv, shape):
-    return oracle.block_rows(x, toks, w, kv, shape, oracle.bf16_round, round_p=True)[0]
+    """The oracle's block output and its value between the two residual additions."""
+    out, _, h = oracle.block_rows(x, toks, w, kv, shape, oracle.bf16_round, round_p=True, return_h=True)
+    return out, h
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
 @pytest.mark.parametrize("ratio", RATIOS)
 def test_float32_block_passes_the_block_gate(shape, ratio):
     w, x, toks, kv = _case(shape, ratio)
-    ok, e1, e2, lim = PG.check(_block32(x, toks, w, kv, shape), _ref(w, x, toks, kv, shape), "bf16", 1)
+    ref, h = _ref(w, x, toks, kv, shape)
+    ok, e1, e2, lim = PG.check(_block32(x, toks, w, kv, shape), ref, "bf16", 1, inp=h)
     assert ok, (e1, e2, lim)
 
 
@@ -126,21 +129,44 @@ def _planted(name, shape):
 def test_planted_mistake_fails_the_block_gate(shape, mistake, monkeypatch):
     for ratio in RATIOS:
         w, x, toks, kv = _case(shape, ratio)
-        good = _ref(w, x, toks, kv, shape)
+        good, h = _ref(w, x, toks, kv, shape)
         fn, zero = _planted(mistake, shape)
         monkeypatch.setattr(OS, "attention_head", fn)
         wb = dict(w)
         if zero:
             wb[zero] = np.zeros_like(w[zero])
-        bad = _ref(wb, x, toks, kv, shape)
+        bad = _ref(wb, x, toks, kv, shape)[0]
         monkeypatch.setattr(OS, "attention_head", oracle.attention_head)
-        ok, e1, e2, lim = PG.check(bad, good, "bf16", 1)
+        ok, e1, e2, lim = PG.check(bad, good, "bf16", 1, inp=h)
         assert not ok, f"{mistake} at ratio {ratio} passed: {e1:.3e} / {e2:.3e}"
 
 
-def test_stack_bound_grows_per_block():
-    assert PG.elem_tol("bf16", 1) == 2e-2
-    assert PG.elem_tol("bf16", 3) == pytest.approx(6e-2)
-    assert PG.elem_tol("fp32", 1) == 1e-4
+def test_stack_bound_grows_with_the_square_root_of_depth():
+    assert PG.tol("bf16", 1) == 2e-2
+    assert PG.tol("bf16", 4) == pytest.approx(4e-2)
+    assert PG.tol("fp32", 1) == 1e-4
     with pytest.raises(ValueError):
-        PG.elem_tol("bf16", 0)
+        PG.tol("bf16", 0)
+
+
+@pytest.mark.parametrize("d,heads,grid,seed", [(768, 12, 32, 4), (1152, 16, 24, 3)])
+def test_two_correct_implementations_drift_within_the_stack_bound(d, heads, grid, seed):
+    """The float64 oracle and the float32 block above through 28 blocks of a workload-like
+    stack (weights N(0, 0.02), LayerNorm 1/0, 10% of the tokens recomputed, a random
+    cache): at every depth both measures stay within 2e-2 sqrt(L), and after 28 blocks
+    the element-wise divergence is beyond a fixed 2e-2 (a depth allowance is needed)."""
+    L = 28
+    shape = W.ModelShape("deep", L, d, heads, 4, grid, grid, dtype="bf16")
+    ws = W.stack_weights(shape, seed)
+    x0 = W.template_hidden(shape, seed)[0]
+    n = shape.n_image
+    toks = np.sort(np.random.default_rng(seed).choice(n, n // 10, replace=False))
+    xr = x0[toks].astype(np.float64)
+    xe = xr.astype(np.float32)
+    for l in range(L):
+        kv = W.synthetic_kv_cache(shape, seed, l)[0]
+        xr = oracle.block_rows(xr, toks, ws[l], kv, shape, oracle.bf16_round, round_p=True)[0]
+        xe = _block32(xe, toks, ws[l], kv, shape)
+        ok, e1, e2, lim = PG.check(xe, xr, "bf16", l + 1, inp=x0[toks])
+        assert ok, (l + 1, e1, e2, lim)
+    assert PG.elem_rel_err(xe, xr, x0[toks]) > PG.TOL["bf16"]
