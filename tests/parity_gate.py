@@ -20,11 +20,12 @@ Bounds, with TOL = 1e-4 for float32 and 2e-2 for bfloat16:
   unit in the last place of a bf16 value is at most 2^-7 of it, so the two
   flips move an output element by at most 2^-7 (|H_i| + |out_i|) <= 1.56e-2
   max(|H_i|, |out_i|). The other rounding points (LayerNorm, Q/K/V, attention
-  output, GELU) and the accumulation order enter the output only through
-  products with small weights. A correct float32 implementation stays below
-  2e-2 (tests/test_parity_gate.py), while the oracle with a planted mistake (a
-  dropped key range, a wrong scale, keys off by one token, a dropped bias)
-  exceeds it.
+  output, GELU) and the accumulation order reach the output through products
+  with the weights; their share is measured, not bounded: at the tests' weight
+  scale (N(0, 0.05) for the per-block tests, 0.02 for the workloads) a correct
+  float32 implementation stays at about 1.45e-2, while the oracle with a
+  planted mistake (a dropped key range, a wrong softmax scale, keys off by one
+  token, a dropped bias) reaches 3e-2 or more (tests/test_parity_gate.py).
 * A stack of ``blocks`` blocks: TOL x sqrt(blocks) for both measures. Each
   block adds its own independent flips to what it inherits through the
   residual connection, so two correct implementations drift apart like a

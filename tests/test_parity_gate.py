@@ -7,13 +7,17 @@ another precision and rejects plausible mistakes.
   than 2^8, softmax weights rounded to bf16 against that running maximum, the
   normaliser summed from the same rounded weights) stays within 2e-2
   element-wise of the oracle with ``round_p``, for head_dim 64 / 72 / 128.
-* The oracle with a planted mistake (on the CPU: a dropped ragged key tail, the
-  softmax scale of a padded head_dim, keys misaligned with their values by one
-  token, a dropped out-projection bias) fails the same gate against the
-  unaltered oracle.
+* The oracle with a planted mistake (on the CPU: a dropped ragged key tail, a
+  wrong softmax scale (that of the zero-padded head_dim 80 for head_dim 72; an
+  exp2 without the log2(e) prescale otherwise), keys misaligned with their
+  values by one token, a dropped out-projection bias) fails the same gate
+  against the unaltered oracle.
 
-Inputs as in the GPU per-block tests: weights N(0, 0.08), random LayerNorm
-affine parameters, hidden states N(0, 1), a random cache.
+Inputs as in the GPU per-block tests: weights N(0, 0.05), random LayerNorm
+affine parameters, hidden states N(0, 1), a random cache. At this scale a
+correct float32 block stays at about 1.45e-2 while every planted mistake
+reaches 3e-2 or more; at 0.06-0.08 the mistakes show more but correct blocks
+reach 1.6-2.0e-2 (the Q/K roundings move a sharper softmax).
 """
 import numpy as np
 import pytest
@@ -24,7 +28,7 @@ from oracle import stack as OS
 from paper_2505_20600_amd import workloads as W
 from tests import parity_gate as PG
 
-STD = 0.08
+STD = 0.05
 SHAPES = [
     W.ModelShape("hd64_T256", 1, 256, 4, 4, 16, 16, dtype="bf16"),
     W.ModelShape("hd72_T144", 1, 576, 8, 4, 12, 12, dtype="bf16"),
@@ -113,9 +117,11 @@ def _planted(name, shape):
     tail = T % 64 or 16
     if name == "dropped key tail":
         return lambda q, k, v, s, rp=False: orig(q, k[:T - tail], v[:T - tail], s, rp), None
-    if name == "padded head_dim scale":
-        pad = (hd + 15) // 16 * 16 if hd % 16 else hd + 16
-        return lambda q, k, v, s, rp=False: orig(q, k, v, 1.0 / np.sqrt(pad), rp), None
+    if name == "wrong softmax scale":
+        if hd % 16:      # the scale of the head_dim padded to the matrix-unit step
+            return lambda q, k, v, s, rp=False: orig(q, k, v, 1.0 / np.sqrt((hd + 15) // 16 * 16), rp), None
+        # exp2 of scores that miss the log2(e) prescale: exp(s ln 2)
+        return lambda q, k, v, s, rp=False: orig(q, k, v, s * np.log(2.0), rp), None
     if name == "keys one token off":
         return lambda q, k, v, s, rp=False: orig(q, np.roll(k, 1, axis=0), v, s, rp), None
     if name == "out-projection bias dropped":
@@ -124,7 +130,7 @@ def _planted(name, shape):
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
-@pytest.mark.parametrize("mistake", ["dropped key tail", "padded head_dim scale", "keys one token off",
+@pytest.mark.parametrize("mistake", ["dropped key tail", "wrong softmax scale", "keys one token off",
                                      "out-projection bias dropped"])
 def test_planted_mistake_fails_the_block_gate(shape, mistake, monkeypatch):
     for ratio in RATIOS:
