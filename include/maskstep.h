@@ -37,7 +37,9 @@
  *    the text rows of all requests come first, then the image rows of all
  *    requests. Each packed row m has a flat token index rows[m] = b*T + t.
  *  - Limits: d % 64 == 0; head_dim = d / n_heads, a multiple of 8, <= 128;
- *    every pointer 16-byte aligned; batch <= max_batch <= 64.
+ *    every pointer 16-byte aligned; batch <= max_batch <= 64; tokens <= 2^20;
+ *    bf16: d <= 4096 and one request's K/V block (T x 2 x d x 2 bytes) below
+ *    4 GiB; fp32: d <= 2048, head_dim <= 64.
  */
 #ifndef MASKSTEP_H
 #define MASKSTEP_H

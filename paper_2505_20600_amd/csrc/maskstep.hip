@@ -87,6 +87,10 @@ ms_status validate_desc(const ms_model_desc* d) {
     if (d->grid_h < 1 || d->grid_w < 1) return fail(MS_ESHAPE, "grid must be at least 1x1");
     if (d->n_text < 0) return fail(MS_ESHAPE, "n_text must be >= 0");
     if ((int64_t)d->grid_h * d->grid_w + d->n_text > (1 << 20)) return fail(MS_ESHAPE, "too many tokens");
+    // the bf16 attention addresses one request's K/V block [T][2][d] with 32-bit
+    // buffer offsets, so the block must stay below 4 GiB
+    if (d->dtype == MS_BF16 && 4ll * ((int64_t)d->grid_h * d->grid_w + d->n_text) * d->d_model >= (1ll << 32))
+        return fail(MS_ESHAPE, "one request's K/V block (tokens x 2 x d_model x 2 bytes) must stay below 4 GiB");
     if (d->dual_stream != 0 && d->dual_stream != 1) return fail(MS_EINVAL, "dual_stream must be 0 or 1");
     if (d->max_batch < 1 || d->max_batch > kMaxBatch) return fail(MS_ESHAPE, "max_batch must be in 1..%d", kMaxBatch);
     if (!(d->ln_eps >= 0.f) || !std::isfinite(d->ln_eps)) return fail(MS_EINVAL, "ln_eps must be finite and >= 0");

@@ -38,6 +38,16 @@ def test_abi_version():
     assert MS.load().mask_abi_version() == 4
 
 
+def test_kv_block_of_4_gib_is_rejected():
+    """The bf16 attention's 32-bit buffer offsets: T x 2 x d x 2 bytes must stay below 2^32."""
+    ok = W.ModelShape("k", 1, 4096, 32, 4, 512, 511, dtype="bf16")      # 4 * 261632 * 4096 < 2^32
+    bad = W.ModelShape("k", 1, 4096, 32, 4, 512, 512, dtype="bf16")     # = 2^32
+    assert MS.mask_workspace_bytes(MS.model_desc(ok), 1) > 0
+    with pytest.raises(MS.MaskStepError) as e:
+        MS.mask_workspace_bytes(MS.model_desc(bad), 1)
+    assert "4 GiB" in str(e.value)
+
+
 def _desc(**kw):
     d = MS.model_desc(W.CONFIGS["c2"])
     for k, v in kw.items():
