@@ -158,6 +158,27 @@ size_t mask_workspace_bytes(const ms_model_desc* desc, int32_t batch);
 ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch,
                          const uint8_t* d_mask, void* d_ws, size_t ws_bytes, void* stream);
 
+/* Bytes of the device array behind mask_step_init_static (one per device). */
+#define MS_STATIC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/* For callers that cannot allocate device memory (code under stream capture,
+ * serving loops or harnesses that forbid allocation): mask_step_init with the
+ * workspace taken from a device array of the library instead of the caller,
+ * MS_STATIC_SCRATCH_BYTES (128 MiB) on each device the library runs on, held
+ * from the first call on that device until the process ends. The step must
+ * fit: mask_workspace_bytes(desc, batch) <= MS_STATIC_SCRATCH_BYTES (a 12-block
+ * d=768 stack over 4096 tokens needs 99 MiB), else MS_EWORKSPACE and nothing
+ * is done. One such context per device at a time: while one is alive, another
+ * call on the same device returns MS_ESTATE; mask_step_destroy gives the array
+ * back. The array keeps what the last context left in it; nothing in it needs
+ * to start at zero (the compaction writes every table the step reads). Work of
+ * two contexts that overlaps on one device races on the array: destroy a
+ * context only after the work enqueued with it has completed. The call
+ * allocates no device memory and creates no HIP object; like mask_step_init it
+ * synchronizes `stream` once. Every other call takes the context as usual. */
+ms_status mask_step_init_static(ms_step** out, const ms_model_desc* desc, int32_t batch,
+                                const uint8_t* d_mask, void* stream);
+
 ms_status mask_step_get_info(const ms_step* step, ms_step_info* info);
 
 /* Device pointers into the workspace: rows [M] (flat b*T + t of each packed
@@ -332,9 +353,9 @@ ms_status mask_profiler_intervals(int32_t* cls, double* start_ms, double* end_ms
 /* Message of the calling thread's last error ("" if none). */
 const char* mask_last_error(void);
 
-/* Version of this interface: 4 (2 added Y caching's kinds and calls, 3 the
+/* Version of this interface: 5 (2 added Y caching's kinds and calls, 3 the
  * cost-model and routing calls, 4 the copy figures of ms_step_info and
- * mask_profiler_intervals). */
+ * mask_profiler_intervals, 5 mask_step_init_static). */
 int32_t mask_abi_version(void);
 
 #ifdef __cplusplus

@@ -17,8 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmaskstep.so")
 
-SOURCES = ["compact.hip", "rows.hip", "gemm.hip", "attention.hip", "maskstep.hip"]
-HEADERS = ["common.h", "kernels.h"]
+SOURCES = ["compact.hip", "rows.hip", "gemm.hip", "attention.hip", "maskstep.hip", "noalloc.hip"]
+HEADERS = ["common.h", "kernels.h", "step_internal.h"]
 
 ARCH = "gfx950"
 FLAGS = [

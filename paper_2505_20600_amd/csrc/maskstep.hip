@@ -17,10 +17,11 @@
 #include "../../include/maskstep.h"
 #include "../../include/maskstep_ops.h"
 #include "kernels.h"
+#include "step_internal.h"
 
 namespace {
 
-constexpr int32_t kAbiVersion = 4;
+constexpr int32_t kAbiVersion = 5;
 constexpr int kMaxBatch = 64;
 // Host-to-device copy spans are merged across masked gaps of at most this
 // many bytes: a gap costs less PCIe time than one more copy submission.
@@ -197,8 +198,9 @@ struct ms_step {
     // unmasked image rows: index into a [B][N] input cache and flat token row (Y caching)
     int U = 0;
     std::vector<int32_t> h_usrc, h_utok;
-    std::vector<hipEvent_t> ev_copied, ev_consumed;
+    std::vector<hipEvent_t> ev_copied, ev_consumed;   // created on first streamed use
     hipEvent_t ev_start = nullptr;
+    int static_dev = -1;        // device whose static scratch is the workspace (mask_step_init_static)
 
     int M() const { return mp.M; }
     void* buf(size_t off) const { return ws + off; }
@@ -217,6 +219,13 @@ void destroy_events(ms_step* s) {
 }
 
 ms_status ensure_events(ms_step* s, int n) {
+    if (!s->ev_start) {
+        hipError_t e = hipEventCreateWithFlags(&s->ev_start, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            s->ev_start = nullptr;
+            return fail(MS_EHIP, "event creation: %s", hipGetErrorString(e));
+        }
+    }
     while ((int)s->ev_copied.size() < n) {
         hipEvent_t a = nullptr, b = nullptr;
         hipError_t e = hipEventCreateWithFlags(&a, hipEventDisableTiming);
@@ -558,6 +567,33 @@ size_t mask_workspace_bytes(const ms_model_desc* desc, int32_t batch) {
 
 ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch,
                          const uint8_t* d_mask, void* d_ws, size_t ws_bytes, void* stream) {
+    return ms::step_init(out, desc, batch, d_mask, d_ws, ws_bytes, stream, -1);
+}
+
+}  // extern "C"
+
+namespace ms {
+
+ms_status set_error(ms_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+ms_status workspace_need(const ms_model_desc* desc, int32_t batch, size_t* need) {
+    ms_status st = validate_desc(desc);
+    if (st != MS_OK) return st;
+    if (batch < 1 || batch > desc->max_batch) return fail(MS_ESHAPE, "batch %d outside 1..max_batch", batch);
+    *need = make_layout(*desc, batch).total;
+    return MS_OK;
+}
+
+ms_status step_init(ms_step** out, const ms_model_desc* desc, int32_t batch, const uint8_t* d_mask,
+                    void* d_ws, size_t ws_bytes, void* stream, int static_dev) {
     if (!out) return fail(MS_EINVAL, "out is NULL");
     *out = nullptr;
     ms_status st = validate_desc(desc);
@@ -581,6 +617,7 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
     s->elt = elt_bytes(desc->dtype);
     s->ws = static_cast<char*>(d_ws);
     s->lay = lay;
+    s->static_dev = static_dev;
     const bool split = desc->dual_stream && desc->n_text > 0;
     Packing& p = s->mp;
     p.rows = s->at<int32_t>(lay.rows);
@@ -592,6 +629,7 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
     p.text_rows = split ? batch * desc->n_text : 0;
 
     hipStream_t hs = static_cast<hipStream_t>(stream);
+    // on failure the caller keeps ownership of a static scratch (static_dev)
     auto bail = [&](ms_status code) { destroy_events(s); delete s; return code; };
     hipError_t e;
     {
@@ -626,13 +664,13 @@ ms_status mask_step_init(ms_step** out, const ms_model_desc* desc, int32_t batch
             e = hipMemcpyAsync(s->buf(lay.u_tok), s->h_utok.data(), s->U * sizeof(int32_t), hipMemcpyHostToDevice, hs);
         if (e != hipSuccess) return bail(fail(MS_EHIP, "unmasked-row upload: %s", hipGetErrorString(e)));
     }
-    st = ensure_events(s, 2);
-    if (st != MS_OK) return bail(st);
-    e = hipEventCreateWithFlags(&s->ev_start, hipEventDisableTiming);
-    if (e != hipSuccess) return bail(fail(MS_EHIP, "event creation: %s", hipGetErrorString(e)));
     *out = s;
     return ok();
 }
+
+}  // namespace ms
+
+extern "C" {
 
 ms_status mask_step_get_info(const ms_step* s, ms_step_info* info) {
     if (!s || !info) return fail(MS_EINVAL, "NULL argument");
@@ -1066,6 +1104,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
 void mask_step_destroy(ms_step* s) {
     if (!s) return;
     destroy_events(s);
+    if (s->static_dev >= 0) ms::release_static_scratch(s->static_dev);
     delete s;
 }
 

@@ -77,6 +77,7 @@ def load() -> C.CDLL:
             "mask_last_error": (C.c_char_p, []),
             "mask_workspace_bytes": (sz, [C.POINTER(ModelDesc), i32]),
             "mask_step_init": (i32, [C.POINTER(vp), C.POINTER(ModelDesc), i32, vp, vp, sz, vp]),
+            "mask_step_init_static": (i32, [C.POINTER(vp), C.POINTER(ModelDesc), i32, vp, vp]),
             "mask_step_get_info": (i32, [vp, C.POINTER(StepInfo)]),
             "mask_step_index": (i32, [vp, C.POINTER(vp), C.POINTER(vp), C.POINTER(vp)]),
             "mask_gather_rows": (i32, [vp, vp, vp, vp]),
@@ -111,7 +112,10 @@ def load() -> C.CDLL:
     return _lib
 
 
+STATIC_SCRATCH_BYTES = 128 << 20   # MS_STATIC_SCRATCH_BYTES
+
 EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask_step_init",
+            "mask_step_init_static",
             "mask_step_get_info", "mask_step_index", "mask_gather_rows", "mask_block_forward",
             "mask_scatter_rows", "cache_prefetch_layer", "cache_prefetch_inputs", "mask_recompute_kv",
             "mask_stack_forward", "mask_step_destroy",
@@ -278,16 +282,20 @@ def weights_array(layers) -> C.Array:
 class MaskStep:
     """One step context (mask set): wraps mask_step_init ... mask_step_destroy."""
 
-    def __init__(self, desc: ModelDesc, batch: int, d_mask: torch.Tensor, workspace: torch.Tensor,
+    def __init__(self, desc: ModelDesc, batch: int, d_mask: torch.Tensor, workspace: torch.Tensor | None,
                  stream=None):
+        """``workspace`` None: mask_step_init_static (the library's static scratch)."""
         self._lib = load()
         self.desc = desc
         self.batch = batch
         self.workspace = workspace
         self.mask = d_mask
         h = C.c_void_p()
-        _check(self._lib.mask_step_init(C.byref(h), C.byref(desc), batch, _ptr(d_mask), _ptr(workspace),
-                                        workspace.numel() * workspace.element_size(), _stream(stream)))
+        if workspace is None:
+            _check(self._lib.mask_step_init_static(C.byref(h), C.byref(desc), batch, _ptr(d_mask), _stream(stream)))
+        else:
+            _check(self._lib.mask_step_init(C.byref(h), C.byref(desc), batch, _ptr(d_mask), _ptr(workspace),
+                                            workspace.numel() * workspace.element_size(), _stream(stream)))
         self.handle = h
 
     def close(self):
@@ -314,6 +322,8 @@ class MaskStep:
 
     def index_views(self):
         """(rows [M], inv [B*T], seg_start [n_seg+1]) as int32 views into the workspace."""
+        if self.workspace is None:
+            raise ValueError("a step on the static scratch has no workspace tensor to view")
         r, i, s = C.c_void_p(), C.c_void_p(), C.c_void_p()
         _check(self._lib.mask_step_index(self.handle, C.byref(r), C.byref(i), C.byref(s)))
         info = self.info()

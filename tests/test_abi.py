@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_abi_version():
-    assert MS.load().mask_abi_version() == 4
+    assert MS.load().mask_abi_version() == 5
 
 
 def test_kv_block_of_4_gib_is_rejected():
@@ -46,6 +46,18 @@ def test_kv_block_of_4_gib_is_rejected():
     with pytest.raises(MS.MaskStepError) as e:
         MS.mask_workspace_bytes(MS.model_desc(bad), 1)
     assert "4 GiB" in str(e.value)
+
+
+def test_static_scratch_rejects_before_any_device_work():
+    lib = MS.load()
+    big = W.CONFIGS["c3"]
+    desc = MS.model_desc(big)
+    assert MS.mask_workspace_bytes(desc, 1) > MS.STATIC_SCRATCH_BYTES
+    h = C.c_void_p()
+    assert lib.mask_step_init_static(C.byref(h), C.byref(desc), 1, 16, None) == MS.MS_EWORKSPACE
+    assert b"static scratch" in lib.mask_last_error()
+    assert lib.mask_step_init_static(None, C.byref(desc), 1, 16, None) == MS.MS_EINVAL
+    assert lib.mask_step_init_static(C.byref(h), C.byref(desc), 0, 16, None) == MS.MS_ESHAPE
 
 
 def _desc(**kw):
