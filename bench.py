@@ -10,9 +10,11 @@ the workload's distribution; each mask set's step context (the mask
 compaction, fixed over a request's denoising steps) is built once before the
 timed steps and its cost reported separately.
 
-Prints ONE JSON line on stdout. Default workload: the 12-block d=768 bf16
-stack over 4096 tokens with an HBM-resident cache and ellipse-union masks of
-ratio U[5%, 60%].
+Prints ONE JSON line on stdout. Default workload: the largest, a 19-block
+dual-stream d=3072 bf16 stack over 4 requests of 4096 image + 512 text
+tokens, each block's image K/V streamed from pinned host memory on a copy
+stream, Gaussian-blob masks of ratio U[10%, 40%], and the Alg. 1 dense
+prefix planned per mask set from per-block costs measured on this GPU.
 """
 from __future__ import annotations
 
@@ -51,13 +53,29 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=40)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="c2", choices=sorted(DESCR))
+    p.add_argument("--workload", default="c5", choices=sorted(DESCR))
     p.add_argument("--masks", type=int, default=8, help="distinct seeded mask sets cycled over the steps")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cache", default="kv", choices=("kv", "y"),
                    help="kv: per-layer K/V cache (Fig. 7); y: per-layer cached block inputs (Fig. 5 bottom)")
     p.add_argument("--no-profile-pass", action="store_true")
+    p.add_argument("--trace-marks", action="store_true",
+                   help="launch a marker kernel (torch's spin kernel) right before and after the profiled pass, "
+                        "so that a rocprofv3 trace of this run can be cut to exactly the launches the roofline "
+                        "averages (see --summarize-trace)")
+    p.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                   help="only summarise a rocprofv3 kernel trace of a --trace-marks run: per kernel symbol over "
+                        "the profiled pass, and the roofline kernel's family; with --pmc-fetch/--pmc-write/"
+                        "--copy-fetch/--copy-write also its copy-calibrated HBM traffic per launch")
+    p.add_argument("--family", help="with --summarize-trace: the bench kernel class to aggregate (e.g. gemm_up)")
+    p.add_argument("--pmc-fetch")
+    p.add_argument("--pmc-write")
+    p.add_argument("--copy-fetch")
+    p.add_argument("--copy-write")
+    p.add_argument("--counters", action="append", default=[],
+                   help="with --summarize-trace and --family: a rocprofv3 counter-collection CSV of a "
+                        "--trace-marks run; per-dispatch averages of its counters over the family's launches")
     p.add_argument("--prefix", default="auto",
                    help="dense-prefix blocks for streamed caches: 'auto' (Alg. 1 planner on measured "
                         "per-block costs) or a fixed count")
@@ -145,11 +163,23 @@ def make_inputs(key, shape, n_masks, torch, W, cache="kv"):
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 
+# Kernel symbols (as rocprofv3 names them) of each bench kernel class: the GEMM
+# classes are told apart by their epilogue template argument (1 residual:
+# out and down projections alike, 2 GELU, 3 QKV split).
+FAMILY = {
+    "attention": (r"attention_dma_kernel<(\d+), 2>", "paper_2505_20600_amd/csrc/attention.hip"),
+    "gemm_up": (r"gemm_dl_kernel<\d+, \d+, \d, 2>", "paper_2505_20600_amd/csrc/gemm.hip"),
+    "gemm_qkv": (r"gemm_dl_kernel<\d+, \d+, \d, 3>", "paper_2505_20600_amd/csrc/gemm.hip"),
+    "gemm_out": (r"gemm_dl_kernel<\d+, \d+, \d, 1>", "paper_2505_20600_amd/csrc/gemm.hip"),
+    "gemm_down": (r"gemm_dl_kernel<\d+, \d+, \d, 1>", "paper_2505_20600_amd/csrc/gemm.hip"),
+}
+MARKER = "spin_kernel"
 
-def measured_traffic(kernel: str):
-    """Calibrated HBM bytes per launch of `kernel` from a profiles/hbm_traffic_*.txt summary
-    (rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by a plain-copy calibration), or None
-    when there is none or the kernel's source changed since it was taken."""
+
+def measured_traffic(kernel: str, workload: str | None = None):
+    """Calibrated HBM bytes per launch of `kernel` on `workload` from a profiles/hbm_traffic_*.txt
+    summary (rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by a plain-copy calibration), or
+    None when there is none or the kernel's source changed since it was taken."""
     import glob
     import hashlib
     for fn in sorted(glob.glob(os.path.join(ROOT, "profiles", "hbm_traffic_*.txt"))):
@@ -158,7 +188,7 @@ def measured_traffic(kernel: str):
             if "=" in line and not line.startswith("#"):
                 k, v = line.strip().split("=", 1)
                 kv[k] = v
-        if kv.get("kernel") != kernel:
+        if kv.get("kernel") != kernel or kv.get("workload") != workload:
             continue
         src = os.path.join(ROOT, kv.get("source", ""))
         if not os.path.exists(src):
@@ -168,6 +198,100 @@ def measured_traffic(kernel: str):
             return None
         return {"bytes_per_launch": float(kv["hbm_bytes_per_launch"]), "file": os.path.relpath(fn, ROOT)}
     return None
+
+
+# ----------------------------------------------------------------------------- rocprofv3 trace summaries
+
+
+def _read_csv(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _window(rows):
+    """The rows of dispatches that ran between the first two marker dispatches (--trace-marks);
+    counter traces hold one row per counter and dispatch."""
+    marks = sorted({(int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in rows if MARKER in r["Kernel_Name"]})
+    if len(marks) < 2:
+        raise SystemExit("the trace has fewer than two marker dispatches: trace a bench.py --trace-marks run")
+    t0, t1 = marks[0][1], marks[1][0]
+    return sorted((r for r in rows if int(r["Start_Timestamp"]) >= t0 and int(r["End_Timestamp"]) <= t1
+                   and MARKER not in r["Kernel_Name"]), key=lambda r: int(r["Start_Timestamp"]))
+
+
+def _short(name):
+    name = name.replace("void ", "").replace("ms::(anonymous namespace)::", "")
+    return name.split("(")[0] if not name.startswith("__") else name
+
+
+def summarize_trace(args):
+    """Per-symbol statistics of a rocprofv3 kernel trace over the profiled pass of a
+    --trace-marks run, the roofline kernel family's launch average, and (given the counter
+    traces) its HBM bytes per launch scaled by a plain device copy's counter readings."""
+    import re
+    rows = _window(_read_csv(args.summarize_trace))
+    per = {}
+    for r in rows:
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        a = per.setdefault(_short(r["Kernel_Name"]), [0, 0.0, 1e30, 0.0])
+        a[0] += 1
+        a[1] += us
+        a[2] = min(a[2], us)
+        a[3] = max(a[3], us)
+    tot = sum(a[1] for a in per.values())
+    print(f"# {len(rows)} dispatches between the marker kernels (the profiled pass), {tot / 1e3:.3f} ms of kernel time")
+    print(f"{'kernel':<64} {'calls':>6} {'total_ms':>10} {'avg_us':>9} {'min_us':>9} {'max_us':>9} {'pct':>6}")
+    for name, (n, t, lo, hi) in sorted(per.items(), key=lambda kv: -kv[1][1]):
+        print(f"{name[:64]:<64} {n:6d} {t / 1e3:10.3f} {t / n:9.2f} {lo:9.2f} {hi:9.2f} {100 * t / tot:6.2f}")
+    if not args.family:
+        return
+    rx = re.compile(FAMILY[args.family][0])
+    fam = [r for r in rows if rx.search(r["Kernel_Name"])]
+    fus = sum((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in fam)
+    print(f"family {args.family} ({FAMILY[args.family][0]}): {len(fam)} launches, {fus / 1e3:.3f} ms, "
+          f"{fus / max(1, len(fam)):.2f} us per launch")
+    for path in args.counters:
+        vals = {}
+        for r in _window(_read_csv(path)):
+            if rx.search(r["Kernel_Name"]):
+                vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+        for c, v in sorted(vals.items()):
+            print(f"counter {c}: {sum(v) / len(v):.6g} per dispatch over {len(v)} dispatches")
+    if not (args.pmc_fetch and args.pmc_write and args.copy_fetch and args.copy_write):
+        return
+
+    def per_dispatch(path, window=True):
+        rr = _read_csv(path)
+        if window:
+            rr = _window(rr)
+        vals = [float(r["Counter_Value"]) for r in rr if rx.search(r["Kernel_Name"])]
+        return sum(vals) / max(1, len(vals)), len(vals)
+
+    def copy_kib(path):
+        vals = [float(r["Counter_Value"]) for r in _read_csv(path) if "copy" in r["Kernel_Name"].lower()]
+        return sum(vals) / max(1, len(vals))
+
+    fetch, nf = per_dispatch(args.pmc_fetch)
+    write, nw = per_dispatch(args.pmc_write)
+    copy_bytes = float(1 << 30)
+    ff = copy_bytes / (copy_kib(args.copy_fetch) * 1024)
+    wf = copy_bytes / (copy_kib(args.copy_write) * 1024)
+    import hashlib
+    src = FAMILY[args.family][1]
+    sha = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()[:16]
+    print(f"# calibration: a plain 1 GiB device copy reads FETCH_SIZE {copy_bytes / ff / 1024:.1f} KiB and "
+          f"WRITE_SIZE {copy_bytes / wf / 1024:.1f} KiB per dispatch")
+    print(f"kernel={args.family}")
+    print(f"symbols={FAMILY[args.family][0]}")
+    print(f"source={src}")
+    print(f"source_sha256_16={sha}")
+    print(f"dispatches={nf},{nw}")
+    print(f"fetch_kib_per_dispatch={fetch:.1f}")
+    print(f"write_kib_per_dispatch={write:.1f}")
+    print(f"fetch_factor={ff:.4f}")
+    print(f"write_factor={wf:.4f}")
+    print(f"hbm_bytes_per_launch={round((fetch * ff + write * wf) * 1024)}")
 
 
 # ----------------------------------------------------------------------------- cost-model fit (Sec. 4.3)
@@ -411,7 +535,10 @@ def h2d_ceiling(torch, stream, nbytes=256 << 20):
 
 
 def cpu_baseline(key, shape, budget_s):
-    """The oracle as it stands, timed on this host over a bounded sample of the workload."""
+    """The oracle as it stands, timed on this host over a bounded sample of the workload: the
+    masked path (request 0's recomputed rows through as many layers as half the budget allows)
+    and, beside it, the dense path (one block over every token of request 0), each scaled to
+    the full stack and batch."""
     import oracle
     from paper_2505_20600_amd import workloads as W
     try:
@@ -428,21 +555,27 @@ def cpu_baseline(key, shape, budget_s):
     toks = oracle.masked_tokens(mask[0], one.n_text)
     M = len(toks)
     rnd = oracle.rounder(one.dtype)
+
+    def layer(l):
+        w = W.layer_weights(one, cfg, l)
+        return (w, W.layer_weights(one, cfg, l, text=True)) if one.dual_stream else w
+
     xm = np.asarray(x[0][toks], np.float64)
     t_layers, n = 0.0, 0
     for l in range(one.n_layers):
-        w = W.layer_weights(one, cfg, l)
-        if one.dual_stream:
-            w = (w, W.layer_weights(one, cfg, l, text=True))
-        kv = W.synthetic_kv_cache(one, cfg, l)[0]
+        w, kv = layer(l), W.synthetic_kv_cache(one, cfg, l)[0]
         t0 = time.perf_counter()
-        xm, _ = oracle.block_rows(xm, toks, w, kv, one, rnd)
+        xm, _ = oracle.block_rows(xm, toks, w, kv, one, rnd, round_p=True)
         t_layers += time.perf_counter() - t0
         n += 1
-        if t_layers >= budget_s:
+        if t_layers >= budget_s / 2:
             break
     per_layer = t_layers / n
-    step_s = per_layer * shape.n_layers * shape.batch * 1.0
+    T = one.n_tokens
+    t0 = time.perf_counter()
+    oracle.block_rows(np.asarray(x[0], np.float64), np.arange(T), layer(0), np.zeros((T, 2, one.d_model)), one,
+                      rnd, round_p=True)
+    dense_layer = time.perf_counter() - t0
     # masked tokens of the whole step: the batch's expected M equals B x this request's M
     value = M / (per_layer * shape.n_layers)
     try:
@@ -451,9 +584,14 @@ def cpu_baseline(key, shape, budget_s):
         model = "unknown"
     return {
         "value": value, "unit": "masked tokens/s", "cores": int(cores), "kind": "oracle",
-        "sample": f"request 0 of mask set 0 (M={M} masked rows), {n} of {shape.n_layers} layers "
-                  f"timed ({t_layers:.1f} s), scaled to the full stack; float64 NumPy; host: {model}",
+        "sample": f"masked path: request 0 of mask set 0 (M={M} recomputed rows), {n} of {shape.n_layers} layers "
+                  f"timed ({t_layers:.1f} s), scaled to the full stack; dense path: one block over all {T} tokens "
+                  f"of request 0 ({dense_layer:.1f} s), scaled to the full stack; float64 NumPy, bf16 rounding "
+                  f"points and round_p as in the parity tests; host: {model}",
         "ms_per_layer": per_layer * 1e3,
+        "dense_ms_per_layer": dense_layer * 1e3,
+        "dense_tokens_per_s": T / (dense_layer * shape.n_layers),
+        "masked_vs_dense_step": (per_layer / dense_layer),
     }
 
 
@@ -462,6 +600,9 @@ def cpu_baseline(key, shape, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the method serves each request set on a single GPU); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
@@ -624,9 +765,15 @@ def main():
     # profiled pass: per-kernel event timing over a second timed region
     kernels, roof = {}, None
     if not args.no_profile_pass:
+        if args.trace_marks:
+            torch.cuda._sleep(1000)
+            torch.cuda.synchronize()
         MS.profiler_start(MS.KERNEL_CLASSES, capacity=1 << 16)
         ms_prof, _, tot_m_prof, _, tot_rl_prof, u_sum = timed(args.steps)
         prof = MS.profiler_stop()
+        if args.trace_marks:
+            torch.cuda._sleep(1000)
+            torch.cuda.synchronize()
         log(f"[bench] profiled pass: {ms_prof / args.steps:.4f} ms/step; {prof}")
         d, T, L, f = shape.d_model, shape.n_tokens, shape.n_layers, shape.mlp_mult * shape.d_model
         e = 2 if shape.dtype == "bf16" else 4
@@ -652,13 +799,20 @@ def main():
         dom = max((c for c in kernels if c in work), key=lambda c: kernels[c]["ms_total"])
         kind, amount = work[dom]
         t_s = kernels[dom]["ms_total"] / 1e3
-        hd = shape.d_model // shape.n_heads
-        kname = {"attention": f"attention_dma_kernel<{hd}, 2>"}.get(dom, dom)
-        # algorithmic HBM bytes per launch of the dominant kernel
+        # algorithmic HBM bytes per launch of the dominant kernel: attention reads every token's
+        # K/V of the batch and the masked rows' Q, writes their O; a projection reads its rows
+        # of A, its weights and (residual epilogues) the residual rows, writes its rows of C
         n_launch = kernels[dom]["launches"]
         m_avg = m_sum / n_launch
-        alg_bytes = {"attention": (4 * shape.batch * T * d + 4 * m_avg * d) * e / 2}.get(dom)
-        tr = measured_traffic(kname)
+        gemm_dims = {"gemm_qkv": (d, 3 * d, 1), "gemm_out": (d, d, 2), "gemm_up": (d, f, 1), "gemm_down": (f, d, 2)}
+        if dom == "attention":
+            alg_bytes = (2 * shape.batch * T * d + 2 * m_avg * d) * e
+        elif dom in gemm_dims:
+            K_, N_, outs = gemm_dims[dom]
+            alg_bytes = (m_avg * K_ + N_ * K_ + outs * m_avg * N_) * e
+        else:
+            alg_bytes = None
+        tr = measured_traffic(dom, key)
         if kind == "mfma":
             peak = PEAK["bf16_mfma_tflops"] if shape.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
             ach = amount / t_s / 1e12
@@ -672,7 +826,8 @@ def main():
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "traffic_source": tr["file"] if tr else None,
                      "algorithmic_bytes_per_launch": round(alg_bytes) if alg_bytes else None,
-                     "kernel": kname, "per_launch_us": kernels[dom]["us_avg"],
+                     "kernel": dom, "kernel_symbols": FAMILY.get(dom, (None,))[0],
+                     "per_launch_us": kernels[dom]["us_avg"],
                      "algorithmic_flops_per_launch": round(amount / n_launch) if kind == "mfma" else None})
 
     # streamed caches: how much of the per-layer load stream runs under the computation

@@ -23,9 +23,18 @@ namespace {
 
 constexpr int32_t kAbiVersion = 5;
 constexpr int kMaxBatch = 64;
-// Host-to-device copy spans are merged across masked gaps of at most this
-// many bytes: a gap costs less PCIe time than one more copy submission.
-constexpr size_t kGapMergeBytes = 256 * 1024;
+// A block's cache load is one host-to-device copy per run of unmasked rows,
+// with runs merged across masked gaps that cost less link time than a copy of
+// their own. Measured on MI355X from pinned host memory: a copy costs the copy
+// engine ~9 us beyond its bytes (500 copies of 384 KiB run at 24 GB/s, 4 of
+// 48 MiB at 57 GB/s), worth ~512 KiB at the link's rate. Spreading the copies
+// over several streams hides that cost only while no kernels run: next to the
+// compute stream's GEMMs, hundreds of small copies per block crawl at 30-34
+// GB/s on 1, 2 or 4 streams, while merged copies keep the link's full rate.
+// Gaps of up to 512 KiB merge (on the 19-block d=3072 workload: 1.3x the
+// needed bytes at 56 GB/s, 52.5 ms per step, against 54.6 ms for 256 KiB and
+// 60 ms for 128 KiB).
+constexpr size_t kGapMergeBytes = 512 * 1024;
 
 thread_local std::string g_err;
 
@@ -1024,16 +1033,29 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         const int n_cached = L - k;
         const bool stream_cache = pinned && !s->all_masked && n_cached > 0;
         const bool serialize = stream_cache && (env_flag("MS_SERIALIZE") || ps == cs);
-        if (stream_cache && !serialize) {
-            // the copy stream must not overwrite a slot an earlier call still reads; the first
-            // n_slots cached layers then load from the start, under the dense prefix if any
-            MS_HIP(hipEventRecord(s->ev_start, cs));
-            MS_HIP(hipStreamWaitEvent(ps, s->ev_start, 0));
-            for (int j = 0; j < std::min(n_slots, n_cached); ++j) {
-                ms_status st = prefetch_signal(s, host_layer(k + j), kv->slots[j], ps, nullptr, s->ev_copied[j],
+        const bool pipelined = stream_cache && !serialize;
+        // Loads of the cached layers on the copy stream. Load j goes to slot j % n_slots and may
+        // be issued once the cached block that used that slot before (j - n_slots) is launched;
+        // the issue is spread over the block launches so the first kernels go out early (the
+        // host stays far ahead of both streams either way).
+        int issued = 0, launched = 0;
+        auto allowed = [&]() { return std::min(n_cached, launched + n_slots); };
+        auto issue_upto = [&](int limit) -> ms_status {
+            for (; issued < limit; ++issued) {
+                const int sl = issued % n_slots;
+                ms_status st = prefetch_signal(s, host_layer(k + issued), kv->slots[sl], ps,
+                                               issued >= n_slots ? s->ev_consumed[sl] : nullptr, s->ev_copied[sl],
                                                ycache);
                 if (st != MS_OK) return st;
             }
+            return MS_OK;
+        };
+        if (pipelined) {
+            // the copy stream must not overwrite a slot an earlier call still reads
+            MS_HIP(hipEventRecord(s->ev_start, cs));
+            MS_HIP(hipStreamWaitEvent(ps, s->ev_start, 0));
+            ms_status st = issue_upto(std::min(allowed(), 2));
+            if (st != MS_OK) return st;
         }
         if (k > 0) {
             // dense prefix: every token, fresh K/V into the workspace buffer, no cache read
@@ -1047,6 +1069,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 const ms_layer_weights* next = l + 1 < k ? w + (size_t)(l + 1) * wstride : nullptr;
                 ms_status st = block_forward(s, dp, w + (size_t)l * wstride, xm, kvd, cs, next, l > 0);
                 if (st != MS_OK) return st;
+                if (pipelined && (st = issue_upto(std::min(allowed(), issued + 2))) != MS_OK) return st;
             }
             // hidden states of every token back in token order, then the masked rows
             void* flat = s->buf(s->lay.o);
@@ -1070,6 +1093,8 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                     ms_status st = prefetch(s, host_layer(l), src, cs, nullptr, ycache);
                     if (st != MS_OK) return st;
                 } else if (stream_cache) {
+                    ms_status st = issue_upto(allowed());   // includes load j
+                    if (st != MS_OK) return st;
                     MS_HIP(hipStreamWaitEvent(cs, s->ev_copied[j % n_slots], 0));
                 }
             }
@@ -1084,12 +1109,10 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             const ms_layer_weights* next = l + 1 < L ? w + (size_t)(l + 1) * wstride : nullptr;
             ms_status st = block_forward(s, mp, w + (size_t)l * wstride, xm, kvbuf, cs, next, l > k);
             if (st != MS_OK) return st;
-            if (stream_cache && !serialize && j + n_slots < n_cached) {
-                const int sl = j % n_slots;
-                MS_HIP(hipEventRecord(s->ev_consumed[sl], cs));
-                st = prefetch_signal(s, host_layer(l + n_slots), kv->slots[sl], ps, s->ev_consumed[sl],
-                                     s->ev_copied[sl], ycache);
-                if (st != MS_OK) return st;
+            if (pipelined) {
+                if (j + n_slots < n_cached) MS_HIP(hipEventRecord(s->ev_consumed[j % n_slots], cs));
+                launched = j + 1;
+                if ((st = issue_upto(allowed())) != MS_OK) return st;
             }
         }
     }
