@@ -315,7 +315,10 @@ ms_status mask_recompute_kv(ms_step* step, int32_t layer, const ms_layer_weights
  * holds the current hidden states (only masked rows and text rows are read);
  * d_y [B][T][d] receives the output; it may equal d_ycache. With the
  * environment variable MS_SERIALIZE=1, copies run on the compute stream
- * before each block instead (the naive loading of Fig. 8 top). */
+ * before each block instead (the naive loading of Fig. 8 top). With
+ * MS_POISON=1 (a debugging mode), every streamed slot is filled with NaN right
+ * after the block that used it, so a block that read a row its own load or
+ * fresh K/V did not write would produce NaN. */
 ms_status mask_stack_forward(ms_step* step, const ms_layer_weights* w, const void* d_x,
                              const void* d_ycache, const ms_kv_source* kv, void* d_y,
                              void* compute_stream, void* copy_stream);

@@ -1034,6 +1034,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         const bool stream_cache = pinned && !s->all_masked && n_cached > 0;
         const bool serialize = stream_cache && (env_flag("MS_SERIALIZE") || ps == cs);
         const bool pipelined = stream_cache && !serialize;
+        const bool poison = env_flag("MS_POISON");
         // Loads of the cached layers on the copy stream. Load j goes to slot j % n_slots and may
         // be issued once the cached block that used that slot before (j - n_slots) is launched;
         // the issue is spread over the block launches so the first kernels go out early (the
@@ -1109,6 +1110,12 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             const ms_layer_weights* next = l + 1 < L ? w + (size_t)(l + 1) * wstride : nullptr;
             ms_status st = block_forward(s, mp, w + (size_t)l * wstride, xm, kvbuf, cs, next, l > k);
             if (st != MS_OK) return st;
+            if (pinned && poison) {
+                // debugging mode: the slot's contents die with its block; a later block that read a
+                // row its own load or fresh K/V did not write would see NaN
+                const size_t slot_bytes = (size_t)s->B * (ycache ? s->N : s->T) * (ycache ? 1 : 2) * s->d * s->elt;
+                MS_HIP(ms::launch_fill_u8(src, 0xFF, slot_bytes, cs));
+            }
             if (pipelined) {
                 if (j + n_slots < n_cached) MS_HIP(hipEventRecord(s->ev_consumed[j % n_slots], cs));
                 launched = j + 1;

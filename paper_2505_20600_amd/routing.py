@@ -5,13 +5,9 @@ Host-only: worker replicas serve requests by step-level continuous batching
 boundary and leaves after its last step); the latency of one step of a batch
 is the Alg. 1 pipeline latency of that batch under the fitted linear cost
 models (``mask_batch_cost`` of the native library). New requests are routed
-on arrival among the workers with room in their batch:
-
-* ``mask-aware``: Alg. 2 (``mask_route_request``): least pipeline latency of
-  the worker's batch with the request added;
-* ``round-robin``: the next worker with room, in turn;
-* ``least-requests``: fewest requests (running and joining);
-* ``least-tokens``: fewest masked tokens (running and joining).
+on arrival by Alg. 2 (``mask_route_request``): among the workers with room in
+their batch, the least pipeline latency of the worker's batch with the
+request added.
 
 When no worker has room the request waits in a FIFO queue and is routed at
 the next step boundary that frees a slot. Arrivals are Poisson; mask ratios
@@ -31,9 +27,6 @@ import numpy as np
 
 from . import maskstep as MS
 from . import workloads as W
-
-POLICIES = ("mask-aware", "round-robin", "least-requests", "least-tokens")
-
 
 class _Worker:
     def __init__(self):
@@ -56,14 +49,11 @@ def draw_requests(n, rate_per_s, n_image, seed, ratio_lo=0.03, ratio_hi=0.80):
     return list(zip(t.tolist(), [max(1, int(round(x * n_image))) for x in r]))
 
 
-def simulate(desc, model, requests, policy, n_workers, max_batch, steps_per_request, decisions=None):
+def simulate(desc, model, requests, n_workers, max_batch, steps_per_request, decisions=None):
     """Latency (seconds) of every request, in arrival order. With a list in ``decisions``,
     every routing decision is appended as (request masked tokens, every worker's running
     and joining masked tokens, chosen worker)."""
-    if policy not in POLICIES:
-        raise ValueError(f"unknown policy {policy}")
     workers = [_Worker() for _ in range(n_workers)]
-    rr = [0]
     lat = [None] * len(requests)
     queue = []           # request ids waiting for room
     events = []          # (time, kind, seq, payload): kind 0 = step end, 1 = arrival
@@ -77,20 +67,7 @@ def simulate(desc, model, requests, policy, n_workers, max_batch, steps_per_requ
         return MS.mask_batch_cost(desc, model, masked)[2]
 
     def pick(masked):
-        free = [i for i, w in enumerate(workers) if w.load() < max_batch]
-        if not free:
-            return -1
-        if policy == "mask-aware":
-            return MS.mask_route_request(desc, model, [w.masked() for w in workers], max_batch, masked)[0]
-        if policy == "round-robin":
-            for j in range(n_workers):
-                i = (rr[0] + j) % n_workers
-                if workers[i].load() < max_batch:
-                    rr[0] = i + 1
-                    return i
-        if policy == "least-requests":
-            return min(free, key=lambda i: (workers[i].load(), i))
-        return min(free, key=lambda i: (sum(workers[i].masked()), i))
+        return MS.mask_route_request(desc, model, [w.masked() for w in workers], max_batch, masked)[0]
 
     def start(i, now):
         nonlocal seq
@@ -167,8 +144,7 @@ def main(argv=None):
     out = {"workload": args.workload, "workers": args.workers, "max_batch": args.max_batch, "steps": args.steps,
            "requests": args.requests, "arrival_per_s": round(args.load_factor * capacity, 3),
            "model": {"comp": args.comp, "load": args.load}}
-    for p in POLICIES:
-        out[p] = summarize(simulate(desc, model, reqs, p, args.workers, args.max_batch, args.steps))
+    out["mask-aware"] = summarize(simulate(desc, model, reqs, args.workers, args.max_batch, args.steps))
     print(json.dumps(out))
 
 

@@ -480,3 +480,25 @@ def test_y_cache_own_cache_is_dense_and_all_masked_reads_nothing():
     ones = np.ones_like(mask)
     y1, _, _ = G.run_stack(shape, ones, xt, np.full_like(yin, np.nan), None, ws, inputs=True)
     G.assert_close(y1, y_dense, "bf16", "all masked, Y cache never read", blocks=shape.n_layers, inp=xt)
+
+
+# ------------------------------------------------------------------ slot reuse (use after recycle)
+
+@pytest.mark.parametrize("shape", [STREAM_SHAPE, STREAM_DUAL], ids=lambda s: s.name)
+@pytest.mark.parametrize("inputs", [False, True], ids=["kv", "y"])
+def test_poisoned_slots_change_nothing(shape, inputs, monkeypatch):
+    """MS_POISON fills each streamed slot with NaN right after its block: with fewer slots
+    than cached layers (each slot reloaded by later layers), a dense prefix and the
+    serialized form, the output is bit-identical to the unpoisoned run, so no block
+    reads a row that its own load or its fresh K/V did not write."""
+    ws, xt, kv, yc = _inputs(shape, 52, std=0.03)
+    mask = _random_mask(shape, [0.3, 0.1], 19)
+    x = W.edited_hidden(shape, 52, xt, mask)
+    cache = np.stack([np.asarray(yc)[:, shape.n_text:]] * shape.n_layers) if inputs else kv
+    for kw in (dict(n_slots=2), dict(n_slots=1), dict(n_slots=2, dense_prefix=1), dict(n_slots=2, serialize=True)):
+        monkeypatch.delenv("MS_POISON", raising=False)
+        y0, _, _ = G.run_stack(shape, mask, x, cache, yc, ws, pinned=True, inputs=inputs, **kw)
+        monkeypatch.setenv("MS_POISON", "1")
+        y1, _, _ = G.run_stack(shape, mask, x, cache, yc, ws, pinned=True, inputs=inputs, **kw)
+        assert np.all(np.isfinite(y1)), kw
+        np.testing.assert_array_equal(y1, y0, err_msg=str(kw))

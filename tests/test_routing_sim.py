@@ -13,39 +13,37 @@ BPT = 2.0 * SHAPE.d_model * 2
 VALS = (0.4, 2.0, 0.3, 5.0)
 
 
-def _run(policy, n_workers=3, max_batch=3, steps=4, n=60, rate=40.0, decisions=None):
+def _run(n_workers=3, max_batch=3, steps=4, n=60, rate=40.0, decisions=None):
     desc = MS.model_desc(SHAPE, max_batch=max_batch)
     model = MS.CostModel(*VALS, BPT)
     reqs = R.draw_requests(n, rate, SHAPE.n_image, seed=3)
-    return reqs, R.simulate(desc, model, reqs, policy, n_workers, max_batch, steps, decisions)
+    return reqs, R.simulate(desc, model, reqs, n_workers, max_batch, steps, decisions)
 
 
-@pytest.mark.parametrize("policy", R.POLICIES)
-def test_every_request_is_served_no_faster_than_alone(policy):
+def test_every_request_is_served_no_faster_than_alone():
     desc = MS.model_desc(SHAPE, max_batch=3)
     model = MS.CostModel(*VALS, BPT)
-    reqs, lat = _run(policy)
+    reqs, lat = _run()
     assert all(v is not None for v in lat)
     for (t, m), v in zip(reqs, lat):
         alone = MS.mask_batch_cost(desc, model, [m])[2] / 1e3
         assert v >= 4 * alone * (1 - 1e-12)
 
 
-def test_one_worker_leaves_no_choice():
-    out = [_run(p, n_workers=1)[1] for p in R.POLICIES]
-    for o in out[1:]:
-        assert o == out[0]
+def test_one_worker_serves_in_arrival_order_batches():
+    """With one worker every request that finds room joins it; more workers never make the
+    mean latency worse on the same arrivals."""
+    one = _run(n_workers=1)[1]
+    three = _run(n_workers=3)[1]
+    assert all(v is not None for v in one)
+    assert np.mean(three) <= np.mean(one) + 1e-12
 
 
 def test_mask_aware_decisions_are_the_oracle_router():
     dec = []
-    _run("mask-aware", n_workers=4, max_batch=2, n=80, rate=2000.0, decisions=dec)
+    _run(n_workers=4, max_batch=2, n=80, rate=2000.0, decisions=dec)
     model = oracle.CostModel(*VALS, BPT)
     assert any(w >= 0 for _, _, w in dec) and any(w < 0 for _, _, w in dec)   # full cluster reached
     for masked, workers, chosen in dec:
         assert chosen == oracle.route(masked, workers, 2, SHAPE, model)[0]
 
-
-def test_unknown_policy_is_rejected():
-    with pytest.raises(ValueError):
-        _run("random")
