@@ -723,14 +723,19 @@ def main():
     torch.cuda.synchronize()
 
     def row_layers(i):
-        # rows each block of the step actually computes: every token in the dense-prefix
-        # blocks, the masked rows (plus text rows) in the others
+        # rows each block of the step computes in full: every token in the first k - 1 blocks
+        # of a dense prefix, the masked rows (plus text rows) in the others (the prefix's last
+        # block projects K/V over every token and computes the rest over the masked rows)
         k = prefix[i]
-        return k * shape.batch * shape.n_tokens + (shape.n_layers - k) * Ms[i]
+        full = max(k - 1, 0)
+        return full * shape.batch * shape.n_tokens + (shape.n_layers - full) * Ms[i]
 
     def unmasked_layers(i):
-        # Y caching: unmasked rows whose K/V each cached block recomputes
-        return (shape.n_layers - prefix[i]) * unmasked[i] if yc_mode else 0
+        # rows whose K/V alone are projected: every token in a dense prefix's last block; with
+        # Y caching, the unmasked rows of every cached block
+        k = prefix[i]
+        kv_rows = shape.batch * shape.n_tokens if k > 0 else 0
+        return kv_rows + ((shape.n_layers - k) * unmasked[i] if yc_mode else 0)
 
     def timed(k, per_step=False):
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(k + 1)]

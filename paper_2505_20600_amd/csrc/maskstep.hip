@@ -487,6 +487,39 @@ ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w
     return MS_OK;
 }
 
+// K/V of every row of a packing from its hidden rows x: LayerNorm 1 (unless `a_ready`:
+// the scratch row buffer already holds it), then the K/V columns of the QKV
+// projection, written to the rows' tokens in kv [B][T][2][d]; text rows with the
+// text weight set.
+ms_status kv_of_rows(ms_step* s, const Packing& pk, const ms_layer_weights* w, const void* x, void* kv,
+                     hipStream_t st, bool a_ready) {
+    if (pk.M == 0) return MS_OK;
+    const bool dual = s->desc.dual_stream && s->desc.n_text > 0;
+    const ms_layer_weights& wi = w[0];
+    const ms_layer_weights& wt = dual ? w[1] : w[0];
+    const int d = s->d, e = s->elt, msplit = pk.text_rows;
+    char* a = static_cast<char*>(s->buf(s->lay.a));
+    if (!a_ready) {
+        ProfScope p(MS_K_LAYERNORM, st);
+        MS_HIP(ms::launch_layernorm(s->desc.dtype, x, wi.ln1_g, wi.ln1_b, wt.ln1_g, wt.ln1_b, msplit, a, pk.M, d,
+                                    s->desc.ln_eps, st));
+    }
+    struct Range { int r0, r1; const ms_layer_weights* w; };
+    const Range ranges[2] = {{0, msplit, &wt}, {msplit, pk.M, &wi}};
+    for (const Range& r : ranges) {
+        if (r.r1 <= r.r0) continue;
+        ms::GemmDesc g{};
+        g.A = a + (size_t)r.r0 * d * e;
+        g.W = static_cast<const char*>(r.w->w_qkv) + (size_t)d * d * e;
+        g.bias = static_cast<const char*>(r.w->b_qkv) + (size_t)d * e;
+        g.kv = kv; g.rows = pk.rows + r.r0;
+        g.M = r.r1 - r.r0; g.N = 2 * d; g.K = d; g.lda = d; g.ldc = 2 * d; g.d = 0; g.kvld = 2 * d;
+        g.epilogue = ms::kEpiQKV;
+        MS_HIP(run_gemm(s, g, MS_K_GEMM_QKV, st));
+    }
+    return MS_OK;
+}
+
 // Y caching (Sec. 3.1, Fig. 5 bottom): K/V of the unmasked image tokens from
 // their cached block input y_in [B][N][d]: LayerNorm of the gathered rows,
 // then the K/V columns of the QKV projection, written to their token rows of
@@ -1058,20 +1091,27 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             ms_status st = issue_upto(std::min(allowed(), 2));
             if (st != MS_OK) return st;
         }
+        bool first_ln_ready = false;   // LayerNorm 1 of block k already in the scratch rows
         if (k > 0) {
-            // dense prefix: every token, fresh K/V into the workspace buffer, no cache read
+            // dense prefix, no cache read: blocks [0, k-1) over every token. Block k-1 needs every
+            // token only for its K/V (block k reads the cache, and the step's output takes the
+            // unmasked rows from the cached state), so it projects K/V over every token and runs
+            // the rest of the block over the masked rows.
             const Packing& dp = s->dp;
             void* kvd = s->buf(s->lay.kv_dense);
             {
                 ProfScope p(MS_K_GATHER, cs);
                 MS_HIP(ms::launch_gather(d_x, dp.rows, xm, dp.M, s->d * s->elt, cs));
             }
-            for (int l = 0; l < k; ++l) {
-                const ms_layer_weights* next = l + 1 < k ? w + (size_t)(l + 1) * wstride : nullptr;
-                ms_status st = block_forward(s, dp, w + (size_t)l * wstride, xm, kvd, cs, next, l > 0);
+            for (int l = 0; l < k - 1; ++l) {
+                ms_status st = block_forward(s, dp, w + (size_t)l * wstride, xm, kvd, cs, w + (size_t)(l + 1) * wstride,
+                                             l > 0);
                 if (st != MS_OK) return st;
                 if (pipelined && (st = issue_upto(std::min(allowed(), issued + 2))) != MS_OK) return st;
             }
+            const ms_layer_weights* wl = w + (size_t)(k - 1) * wstride;
+            ms_status st = kv_of_rows(s, dp, wl, xm, kvd, cs, k > 1);
+            if (st != MS_OK) return st;
             // hidden states of every token back in token order, then the masked rows
             void* flat = s->buf(s->lay.o);
             {
@@ -1079,8 +1119,15 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 MS_HIP(ms::launch_scatter(xm, dp.rows, dp.inv, flat, flat, dp.M, s->B * s->T,
                                           s->d * s->elt, cs));
             }
-            ProfScope p(MS_K_GATHER, cs);
-            MS_HIP(ms::launch_gather(flat, mp.rows, xm, mp.M, s->d * s->elt, cs));
+            {
+                ProfScope p(MS_K_GATHER, cs);
+                MS_HIP(ms::launch_gather(flat, mp.rows, xm, mp.M, s->d * s->elt, cs));
+            }
+            const ms_layer_weights* next = k < L ? w + (size_t)k * wstride : nullptr;
+            st = block_forward(s, mp, wl, xm, kvd, cs, next, false);
+            if (st != MS_OK) return st;
+            if (pipelined && (st = issue_upto(std::min(allowed(), issued + 2))) != MS_OK) return st;
+            first_ln_ready = next != nullptr;
         } else {
             ProfScope p(MS_K_GATHER, cs);
             MS_HIP(ms::launch_gather(d_x, mp.rows, xm, mp.M, s->d * s->elt, cs));
@@ -1108,7 +1155,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 if (st != MS_OK) return st;
             }
             const ms_layer_weights* next = l + 1 < L ? w + (size_t)(l + 1) * wstride : nullptr;
-            ms_status st = block_forward(s, mp, w + (size_t)l * wstride, xm, kvbuf, cs, next, l > k);
+            ms_status st = block_forward(s, mp, w + (size_t)l * wstride, xm, kvbuf, cs, next, l > k || first_ln_ready);
             if (st != MS_OK) return st;
             if (pinned && poison) {
                 // debugging mode: the slot's contents die with its block; a later block that read a
