@@ -334,7 +334,13 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
         if (kt + S - 1 <= nk) wait_vmcnt<(S - 2) * IPW>();
         else wait_vmcnt<0>();
         barrier_only();
-        if (kt + S - 1 < nk) issue(kt + S - 1, (kt + S - 1) % S);
+        // The 8-wave tiles spread this step's copies over the MFMA groups of
+        // the first half step, so the matrix cores start right after the
+        // barrier (measured +3..12% on their shapes); the 4-wave tiles issue
+        // them at once, which keeps their shorter prefetch distance whole.
+        const bool more_k = kt + S - 1 < nk;
+        const int k_next = kbeg + (kt + S - 1) * BK, st_next = (kt + S - 1) % S;
+        if (NW != 8 && more_k) issue(kt + S - 1, st_next);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             const int ch = ((ks * 4 + grp) ^ sw) * 8;
@@ -347,6 +353,15 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
                 const frag_t fw = *reinterpret_cast<const frag_t*>(sWb + st * BN * ROWE + (wn * (BN / WN) + i * 16 + lane % 16) * ROWE + ch);
 #pragma unroll
                 for (int j = 0; j < SM; ++j) acc[i][j] = E::mma(fw, fa[j], acc[i][j]);
+                if (NW == 8 && ks == 0 && more_k) {
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int q = i * IPW / SN; q < (i + 1) * IPW / SN; ++q) {
+                        if (q < IA) dma_lds16(A + goff[q] + k_next, ldst[q] + st_next * kStageA);
+                        else dma_lds16(W + goff[q] + k_next, ldst[q] + st_next * kStageW);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
         }
     }
@@ -512,41 +527,67 @@ hipError_t launch_reduce(const GemmDesc& g, hipStream_t s) {
 
 }  // namespace
 
-// Tile and stage choice from a measured cost table. Each entry gives the
-// time (us) of one 64-deep K step of a whole grid in which every CU holds n
-// = 1..8 workgroups of that tile and stage count (MI355X, bf16, direct-to-LDS
-// main loop, grouped tile order, K = 2048; n = 7 interpolated). A launch costs about steps x
-// time(n_busiest) with n_busiest = ceil(groups / 256); past n = 8 the last
-// measured slope extends the table. More stages pay off when few workgroups
-// share a CU (deeper prefetch), fewer when many do (LDS occupancy). Split-K
-// multiplies the groups, divides the steps and adds the partial-sum pass.
+// Tile and stage choice from a measured cost model. A launch whose busiest
+// CU holds n workgroups of a tile and stage count costs about
+// steps x a(n) + b(n) us: a(n) per 64-deep K step of the whole grid, b(n) the
+// per-tile work outside the K loop (prologue, epilogue, stores). Both come
+// from timing grids of n x 256 tiles (16 tile columns, GELU epilogue) at
+// K = 1024 and K = 4096 on MI355X with the direct-to-LDS main loop; between
+// the measured n the model interpolates linearly, past n = 48 it scales with n.
+// Checked against 17 projection shapes of the workloads (M 1243..16384,
+// N 1152..12288, K 768..12288): the predicted rate is within 10% of the
+// measured one for the chosen tile on all but the deepest K (12288, +26%,
+// same choice). Split-K multiplies the groups, divides the steps and adds the
+// partial-sum pass.
 namespace {
+constexpr int kCostN = 13;
+constexpr int kCostAt[kCostN] = {1, 2, 3, 4, 5, 6, 7, 8, 12, 16, 24, 32, 48};
 struct TileCost {
     int bm, bn, stages;
-    double us[8];
+    double step[kCostN];   // a(n), us per K step
+    double tile[kCostN];   // b(n), us per launch
 };
 constexpr TileCost kCost[] = {
-    {256, 256, 2, {2.053, 3.925, 5.809, 7.690, 9.645, 12.229, 14.984, 17.740}},
-    {256, 192, 2, {1.662, 3.160, 4.742, 6.133, 7.683, 9.118, 11.446, 13.773}},
-    {256, 128, 2, {1.436, 2.538, 3.676, 4.847, 6.029, 7.196, 8.445, 9.694}},
-    {256, 128, 3, {1.418, 2.668, 3.898, 5.195, 6.433, 7.714, 9.015, 10.317}},
-    {128, 128, 2, {0.942, 1.181, 1.820, 2.194, 2.777, 3.200, 3.716, 4.233}},
-    {128, 128, 3, {0.910, 1.645, 2.386, 3.100, 3.816, 4.524, 5.279, 6.034}},
-    {128, 128, 4, {0.849, 1.601, 2.339, 3.053, 3.749, 4.497, 5.223, 5.948}},
-    {128, 64, 2, {0.611, 0.812, 1.093, 1.613, 1.698, 1.946, 2.243, 2.540}},
-    {128, 64, 3, {0.686, 0.833, 1.313, 1.482, 1.920, 2.162, 2.463, 2.764}},
-    {128, 64, 4, {0.650, 1.166, 1.668, 2.171, 2.670, 3.166, 3.631, 4.096}},
-    {64, 128, 2, {0.754, 0.840, 1.065, 1.581, 1.667, 1.966, 2.266, 2.566}},
-    {64, 128, 3, {0.670, 0.827, 1.288, 1.510, 1.936, 2.176, 2.503, 2.831}},
-    {64, 128, 4, {0.589, 1.122, 1.623, 2.133, 2.603, 3.076, 3.572, 4.068}},
-    {64, 64, 2, {0.422, 0.628, 0.708, 0.943, 1.325, 1.357, 1.520, 1.683}},
-    {64, 64, 3, {0.464, 0.562, 0.771, 1.087, 1.219, 1.483, 1.700, 1.917}},
-    {64, 64, 4, {0.440, 0.579, 0.872, 1.034, 1.358, 1.522, 1.758, 1.994}},
+    {256, 256, 2, {1.353, 2.677, 3.726, 5.789, 7.043, 9.378, 11.009, 12.507, 18.991, 24.576, 34.741, 49.206, 73.895},
+     {23.6, 44.1, 81.1, 79.3, 103.5, 98.8, 114.7, 172.7, 215.0, 360.7, 556.3, 541.7, 843.8}},
+    {256, 192, 2, {1.056, 2.152, 3.243, 4.544, 6.230, 7.835, 9.340, 10.339, 14.877, 19.229, 30.646, 39.311, 59.356},
+     {18.8, 29.5, 40.4, 47.4, 49.2, 51.8, 61.3, 82.1, 173.6, 237.3, 322.0, 447.8, 652.3}},
+    {256, 128, 2, {0.865, 1.797, 2.624, 3.601, 4.574, 5.530, 6.697, 7.757, 11.686, 15.233, 23.217, 31.222, 46.550},
+     {21.3, 35.0, 50.1, 62.9, 73.9, 85.7, 91.4, 100.0, 147.7, 223.4, 316.3, 421.8, 611.1}},
+    {256, 128, 3, {0.885, 1.787, 2.633, 3.593, 4.522, 5.451, 6.686, 7.655, 11.689, 15.144, 23.001, 31.000, 46.451},
+     {22.4, 38.8, 55.5, 69.0, 82.1, 94.1, 99.8, 110.9, 154.1, 216.6, 311.6, 410.4, 595.6}},
+    {128, 128, 2, {0.667, 0.872, 1.426, 1.794, 2.263, 2.677, 3.221, 3.821, 5.954, 8.068, 11.962, 16.089, 24.757},
+     {8.7, 14.0, 17.0, 19.1, 21.6, 26.4, 26.4, 29.4, 43.7, 60.3, 114.0, 158.4, 211.3}},
+    {128, 128, 3, {0.574, 1.152, 1.716, 2.263, 2.870, 3.428, 4.064, 4.601, 6.858, 9.405, 14.008, 18.876, 27.324},
+     {11.5, 17.8, 24.8, 31.7, 37.5, 45.0, 50.5, 57.3, 85.5, 109.5, 164.1, 223.9, 347.6}},
+    {128, 128, 4, {0.515, 1.059, 1.569, 2.113, 2.627, 3.235, 3.764, 4.230, 6.562, 8.995, 13.730, 18.619, 26.798},
+     {13.7, 22.4, 31.8, 40.0, 49.7, 55.6, 64.0, 75.6, 103.3, 129.4, 175.2, 232.1, 362.3}},
+    {128, 64, 2, {0.575, 0.579, 0.770, 1.252, 1.319, 1.669, 2.037, 2.174, 3.349, 5.283, 8.289, 11.171, 15.806},
+     {3.6, 7.2, 11.6, 11.1, 13.5, 14.1, 14.6, 16.7, 23.4, 11.7, 11.0, 15.4, 89.5}},
+    {128, 64, 3, {0.411, 0.547, 0.933, 1.104, 1.489, 1.749, 2.069, 2.405, 3.661, 5.545, 8.539, 12.549, 16.871},
+     {6.5, 8.6, 11.0, 12.6, 13.8, 14.7, 15.9, 17.4, 22.4, 20.0, 29.1, 22.3, 89.9}},
+    {128, 64, 4, {0.372, 0.759, 1.119, 1.505, 1.865, 2.241, 2.604, 3.044, 4.527, 6.203, 9.681, 13.186, 18.494},
+     {7.0, 10.7, 14.7, 17.5, 21.6, 25.4, 29.4, 32.4, 46.6, 62.4, 80.6, 102.3, 191.8}},
+    {64, 128, 2, {0.592, 0.609, 0.835, 1.270, 1.357, 1.622, 1.963, 2.110, 3.356, 4.356, 7.593, 10.284, 15.445},
+     {3.9, 7.8, 9.4, 10.6, 11.9, 14.1, 14.9, 16.7, 20.5, 24.6, 24.2, 26.8, 73.6}},
+    {64, 128, 3, {0.444, 0.559, 0.978, 1.121, 1.507, 1.656, 2.055, 2.233, 3.550, 4.680, 8.045, 11.099, 16.777},
+     {7.0, 8.7, 10.8, 12.7, 14.8, 17.9, 18.8, 22.8, 28.0, 41.7, 41.9, 48.0, 75.7}},
+    {64, 128, 4, {0.404, 0.815, 1.211, 1.603, 2.021, 2.429, 2.792, 3.216, 4.830, 6.428, 9.697, 13.225, 19.503},
+     {7.0, 10.8, 15.1, 18.5, 22.2, 26.5, 31.0, 33.9, 49.1, 65.3, 94.5, 120.0, 192.6}},
+    {64, 64, 2, {0.512, 0.497, 0.520, 0.629, 1.065, 1.074, 1.145, 1.308, 2.322, 3.429, 5.004, 7.991, 15.165},
+     {1.1, 3.0, 5.3, 7.6, 7.6, 8.8, 10.8, 10.6, 13.3, 13.8, 19.3, 11.3, 0.0}},
+    {64, 64, 3, {0.303, 0.387, 0.567, 0.740, 0.883, 1.100, 1.172, 1.348, 2.152, 2.900, 4.561, 7.126, 11.196},
+     {5.2, 5.3, 5.3, 7.4, 8.2, 8.6, 9.8, 10.6, 12.5, 14.5, 17.1, 7.0, 5.1}},
+    {64, 64, 4, {0.287, 0.373, 0.598, 0.692, 0.939, 1.043, 1.327, 1.423, 2.106, 2.839, 4.474, 7.037, 10.639},
+     {5.3, 4.7, 7.5, 8.0, 9.1, 10.8, 10.2, 12.6, 17.5, 20.5, 26.6, 25.2, 27.5}},
 };
 
-double step_us(const TileCost& c, long n) {
-    if (n <= 8) return c.us[n - 1];
-    return c.us[7] + (double)(n - 8) * (c.us[7] - c.us[5]) / 2.0;
+double interp(const double* v, long n) {
+    if (n <= kCostAt[0]) return v[0];
+    for (int i = 1; i < kCostN; ++i)
+        if (n <= kCostAt[i])
+            return v[i - 1] + (v[i] - v[i - 1]) * (double)(n - kCostAt[i - 1]) / (kCostAt[i] - kCostAt[i - 1]);
+    return v[kCostN - 1] * (double)n / kCostAt[kCostN - 1];
 }
 }  // namespace
 
@@ -565,7 +606,7 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats) 
             if (ks > 1 && (size_t)ks * M * N > part_capacity_floats) break;
             const int per = (steps + ks - 1) / ks;
             const long n = (grp * ks + kCUs - 1) / kCUs;
-            double us = per * step_us(c, n);
+            double us = per * interp(c.step, n) + interp(c.tile, n);
             // partial sums: ks float planes read, one bf16 plane written, ~4 TB/s, + a launch
             if (ks > 1) us += split_scale * (2.0 + ((double)ks * 4 + 2) * M * N / 4.0e6);
             if (us < best * 0.97) {   // prefer the earlier (larger, unsplit) choice on near-ties
