@@ -171,7 +171,7 @@ FAMILY = {
     "gemm_up": (r"gemm_dl_kernel<\d+, \d+, \d, 2>", "paper_2505_20600_amd/csrc/gemm.hip"),
     "gemm_qkv": (r"gemm_dl_kernel<\d+, \d+, \d, 3>", "paper_2505_20600_amd/csrc/gemm.hip"),
     "gemm_out": (r"gemm_dl_kernel<\d+, \d+, \d, 1>", "paper_2505_20600_amd/csrc/gemm.hip"),
-    "gemm_down": (r"gemm_dl_kernel<\d+, \d+, \d, 1>", "paper_2505_20600_amd/csrc/gemm.hip"),
+    "gemm_down": (r"gemm_dl_kernel<\d+, \d+, \d, 4>", "paper_2505_20600_amd/csrc/gemm.hip"),
 }
 MARKER = "spin_kernel"
 

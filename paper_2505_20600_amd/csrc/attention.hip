@@ -279,8 +279,13 @@ __device__ __forceinline__ bf16x4_t ld_tr16(lds_cptr p) {
     return __builtin_bit_cast(bf16x4_t, v);
 }
 
+// Workgroups per CU the register budget is set for: four for head_dim 64
+// (128 VGPRs, no spills), two for 72 and 128 (whose 140 / 208 VGPRs then
+// allow three and two).
+constexpr int dma_occupancy(int hd) { return hd == 64 ? 4 : 2; }
+
 template <int HD, int S>
-__global__ __launch_bounds__(kThreads, 2) void attention_dma_kernel(AttnDesc a) {
+__global__ __launch_bounds__(kThreads, dma_occupancy(HD)) void attention_dma_kernel(AttnDesc a) {
     using C = DmaCfg<HD>;
     __shared__ __attribute__((aligned(1024))) uint8_t smem[S * C::STAGEB + 16];
     const uint32_t lds0 = lds_addr(smem);

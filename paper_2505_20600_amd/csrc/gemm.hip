@@ -60,7 +60,7 @@ __device__ __forceinline__ void epilogue_store(const GemmDesc& g, int m, int n, 
     load4<T>(bias + n, bv);
 #pragma unroll
     for (int r = 0; r < 4; ++r) v[r] += bv[r];
-    if constexpr (EPI == kEpiBiasResid) {
+    if constexpr (epi_resid(EPI)) {
         float rv[4];
         load4<T>(static_cast<const T*>(g.R) + (long)m * g.ldr + n, rv);
 #pragma unroll
@@ -467,6 +467,7 @@ hipError_t launch_tile(const GemmDesc& g, hipStream_t s) {
         case kEpiBiasResid: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, kEpiBiasResid>), grid, block, 0, s, g); break;
         case kEpiBiasGelu: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, kEpiBiasGelu>), grid, block, 0, s, g); break;
         case kEpiQKV: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, kEpiQKV>), grid, block, 0, s, g); break;
+        case kEpiBiasResidMlp: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, kEpiBiasResidMlp>), grid, block, 0, s, g); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -507,6 +508,7 @@ hipError_t launch_dl(const GemmDesc& g, hipStream_t s) {
         case kEpiBiasResid: return launch_dl_epi<BM, BN, S, kEpiBiasResid>(g, s);
         case kEpiBiasGelu: return launch_dl_epi<BM, BN, S, kEpiBiasGelu>(g, s);
         case kEpiQKV: return launch_dl_epi<BM, BN, S, kEpiQKV>(g, s);
+        case kEpiBiasResidMlp: return launch_dl_epi<BM, BN, S, kEpiBiasResidMlp>(g, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -520,6 +522,7 @@ hipError_t launch_reduce(const GemmDesc& g, hipStream_t s) {
         case kEpiBiasResid: hipLaunchKernelGGL((gemm_reduce_kernel<T, kEpiBiasResid>), grid, block, 0, s, g); break;
         case kEpiBiasGelu: hipLaunchKernelGGL((gemm_reduce_kernel<T, kEpiBiasGelu>), grid, block, 0, s, g); break;
         case kEpiQKV: hipLaunchKernelGGL((gemm_reduce_kernel<T, kEpiQKV>), grid, block, 0, s, g); break;
+        case kEpiBiasResidMlp: hipLaunchKernelGGL((gemm_reduce_kernel<T, kEpiBiasResidMlp>), grid, block, 0, s, g); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -43,7 +43,12 @@ hipError_t launch_reduce_layernorm(int dtype, const float* part, int ksplit, con
                                    const void* b, void* y, int ldy, int M, int d, float eps,
                                    hipStream_t s);
 
-enum Epilogue { kEpiBias = 0, kEpiBiasResid = 1, kEpiBiasGelu = 2, kEpiQKV = 3 };
+enum Epilogue { kEpiBias = 0, kEpiBiasResid = 1, kEpiBiasGelu = 2, kEpiQKV = 3, kEpiBiasResidMlp = 4 };
+
+// kEpiBiasResidMlp is kEpiBiasResid for the MLP's second projection: the same
+// arithmetic in its own kernel instantiation, so that traces and counters
+// tell the two residual projections of a block apart.
+constexpr bool epi_resid(int e) { return e == kEpiBiasResid || e == kEpiBiasResidMlp; }
 
 struct GemmDesc {
     const void* A;      // [M][K] activations, row stride lda (elements)

@@ -379,7 +379,7 @@ hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, int cls, hipStream_t st, const 
     if (e != hipSuccess) return e;
     if (g.ksplit > 1) {
         ProfScope prof(MS_K_GEMM_REDUCE, st);
-        if (ln && g.epilogue == ms::kEpiBiasResid && !env_flag("MS_NO_LN_FUSE"))
+        if (ln && ms::epi_resid(g.epilogue) && !env_flag("MS_NO_LN_FUSE"))
             return ms::launch_reduce_layernorm(s->desc.dtype, g.part, g.ksplit, g.bias, g.R, g.ldr, g.C,
                                                g.ldc, ln->g, ln->b, ln->y, g.N, g.M, g.N, s->desc.ln_eps, st);
         e = ms::launch_gemm_reduce(s->desc.dtype, g, st);
@@ -480,7 +480,7 @@ ms_status block_forward(ms_step* s, const Packing& pk, const ms_layer_weights* w
         g.A = u + (size_t)r.r0 * f * e; g.W = r.w->w_2; g.bias = r.w->b_2;
         g.R = h + (size_t)r.r0 * d * e; g.C = x + (size_t)r.r0 * d * e;
         g.M = r.r1 - r.r0; g.N = d; g.K = f; g.lda = f; g.ldr = d; g.ldc = d;
-        g.epilogue = ms::kEpiBiasResid;
+        g.epilogue = ms::kEpiBiasResidMlp;
         const LnAfter ln1{r.nw ? r.nw->ln1_g : nullptr, r.nw ? r.nw->ln1_b : nullptr, a + (size_t)r.r0 * d * e};
         MS_HIP(run_gemm(s, g, MS_K_GEMM_DOWN, st, r.nw ? &ln1 : nullptr));
     }
