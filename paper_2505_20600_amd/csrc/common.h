@@ -110,21 +110,6 @@ __device__ __forceinline__ int xcd_logical_block(int hw, int total) {
     return x * per + min(x, rem) + i;
 }
 
-// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
-// lane i's 16 bytes land at lds + 16 * i; `lds` must be the same for the whole wave.
-__device__ __forceinline__ void load_lds16(const void* g, void* lds) {
-    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds), 16, 0, 0);
-}
-
-// The same copy issued as an opaque instruction: the compiler does not see the
-// LDS write, so it adds no wait of its own before later LDS reads (of other
-// stages); the caller orders them with wait_vmcnt + barrier_only. `lds` is a
-// wave-uniform LDS byte address. The loads complete in issue order with every
-// other vector-memory load, so the compiler's own vmcnt waits stay correct.
-__device__ __forceinline__ void dma_lds16(const void* g, uint32_t lds) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(g) : "memory", "m0");
-}
 // Buffer resource (four SGPRs) over `bytes` bytes from `base`, raw addressing:
 // loads at or past `bytes` (per-lane offset plus scalar offset) return zeros.
 __device__ __forceinline__ u32x4_t raw_rsrc(const void* base, uint32_t bytes) {
@@ -138,8 +123,12 @@ __device__ __forceinline__ u32x4_t raw_rsrc(const void* base, uint32_t bytes) {
 }
 
 // One 16-byte-per-lane buffer load into LDS at `lds` + 16 * lane (gfx950
-// buffer_load_dwordx4 ... lds), issued as an opaque instruction like
-// dma_lds16; `soff` and `lds` are wave-uniform.
+// buffer_load_dwordx4 ... lds), issued as an opaque instruction: the
+// compiler does not see the LDS write, so it adds no wait of its own before
+// later LDS reads (of other stages); the caller orders them with wait_vmcnt +
+// barrier_only. The loads complete in issue order with every other
+// vector-memory load, so the compiler's own vmcnt waits stay correct. `soff`
+// and `lds` are wave-uniform.
 __device__ __forceinline__ void dma_buf16(u32x4_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                  :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc),

@@ -217,13 +217,15 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
     }
 }
 
-// bf16 main loop with direct global->LDS loads (gfx950 global_load_lds_dwordx4)
-// into S LDS stages, so S-1 K steps are in flight without staging registers.
+// bf16 main loop with direct global->LDS loads (gfx950 buffer_load_dwordx4
+// ... lds, one buffer resource per tile and operand, so rows past M or N read
+// as zeros) into S LDS stages, so S-1 K steps are in flight without staging
+// registers.
 // LDS rows are 128 bytes (one K step of 64 bf16) with their eight 16-byte
 // chunks XOR-swizzled by (row >> 1) & 7: each load instruction fills 1 KB
 // (8 rows) contiguously, and the 16-row MFMA fragment reads of one K chunk
 // still touch 16 distinct bank groups. The copies are issued as opaque
-// instructions (dma_lds16) and ordered by explicit counter waits: a compiler
+// instructions (dma_buf16) and ordered by explicit counter waits: a compiler
 // that sees them must assume each may write the stage being read and drains
 // every load in flight before the first fragment read of each step.
 
@@ -272,25 +274,29 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
     // Persistent when the grid is smaller than the tile count: workgroup b
     // takes physical ids b, b + grid, ... (the grid is a multiple of the XCD
     // count, so every id maps to a tile of the workgroup's own XCD).
-    // Tile state: split index, tile origin, K range, and per load
-    // instruction this lane's element offset (row * ld + swizzled chunk).
+    // Tile state: split index, tile origin, K range, and the tile's operand
+    // rows as buffer resources (rows past M or N read as zeros).
     int kz, m0, n0, kbeg, nk;
-    int goff[IPW];
+    u32x4_t rA, rW;
     auto setup = [&](int hw) {
         const TileIdx ti = tile_of(xcd_logical_block(hw, total), tiles_m, tiles_n, BM, BN, g.group_m);
         kz = ti.kz; m0 = ti.m0; n0 = ti.n0;
         kbeg = kz * g.kchunk;
         nk = (min(K, kbeg + g.kchunk) - kbeg) / BK;
-#pragma unroll
-        for (int i = 0; i < IPW; ++i) {
-            const int blk = i * NW + wave;                      // 8-row block
-            const bool isA = i < IA;
-            const int rloc = (isA ? blk : blk - BM / 8) * 8 + lane / 8;
-            const int c = (lane % 8) ^ ((rloc >> 1) & 7);
-            if (isA) goff[i] = min(m0 + rloc, M - 1) * g.lda + c * 8;
-            else goff[i] = min(n0 + rloc, N - 1) * K + c * 8;
-        }
+        rA = raw_rsrc(A + (size_t)m0 * g.lda, (uint32_t)((size_t)min(BM, M - m0) * g.lda * 2));
+        rW = raw_rsrc(W + (size_t)n0 * K, (uint32_t)((size_t)min(BN, N - n0) * K * 2));
     };
+    // per load instruction this lane's byte offset inside the tile's rows
+    // (row * ld + swizzled chunk)
+    uint32_t voff[IPW];
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+        const int blk = i * NW + wave;                      // 8-row block
+        const bool isA = i < IA;
+        const int rloc = (isA ? blk : blk - BM / 8) * 8 + lane / 8;
+        const int c = (lane % 8) ^ ((rloc >> 1) & 7);
+        voff[i] = (uint32_t)((isA ? rloc * g.lda : rloc * K) + c * 8) * 2u;
+    }
     // the wave's 1 KB destination of each load instruction inside a stage (bytes)
     uint32_t ldst[IPW];
 #pragma unroll
@@ -300,11 +306,11 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
     }
     constexpr uint32_t kStageA = BM * ROWE * 2, kStageW = BN * ROWE * 2;   // bytes
     auto issue = [&](int kt, int st) {
-        const int k0 = kbeg + kt * BK;
+        const uint32_t k0 = (uint32_t)(kbeg + kt * BK) * 2u;
 #pragma unroll
         for (int i = 0; i < IPW; ++i) {
-            if (i < IA) dma_lds16(A + goff[i] + k0, ldst[i] + st * kStageA);
-            else dma_lds16(W + goff[i] + k0, ldst[i] + st * kStageW);
+            if (i < IA) dma_buf16(rA, voff[i], k0, ldst[i] + st * kStageA);
+            else dma_buf16(rW, voff[i], k0, ldst[i] + st * kStageW);
         }
     };
     auto prologue = [&]() {
@@ -357,8 +363,8 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
                     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int q = i * IPW / SN; q < (i + 1) * IPW / SN; ++q) {
-                        if (q < IA) dma_lds16(A + goff[q] + k_next, ldst[q] + st_next * kStageA);
-                        else dma_lds16(W + goff[q] + k_next, ldst[q] + st_next * kStageW);
+                        if (q < IA) dma_buf16(rA, voff[q], (uint32_t)k_next * 2u, ldst[q] + st_next * kStageA);
+                        else dma_buf16(rW, voff[q], (uint32_t)k_next * 2u, ldst[q] + st_next * kStageW);
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
