@@ -229,12 +229,13 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmDesc g) {
 // that sees them must assume each may write the stage being read and drains
 // every load in flight before the first fragment read of each step.
 
-// Waves per workgroup of the direct-to-LDS kernel: 256x256 and 256x192 tiles
-// run eight waves (2 x 4, 128 x 64 or 128 x 48 outputs each), the other tiles
-// four (2 x 2). 192-wide tiles fill the 256 CUs in whole waves where the
-// projection widths are multiples of 192 and not of 256 (1152, 3072, 4608,
-// 12288 columns).
-constexpr int dl_waves(int bm, int bn) { return bm * bn >= 256 * 192 ? 8 : 4; }
+// Waves per workgroup of the direct-to-LDS kernel: 256x256, 256x192 and
+// 192x192 tiles run eight waves (2 x 4, 128 x 64, 128 x 48 or 96 x 48
+// outputs each), the other tiles four (2 x 2). 192-wide tiles fill the 256
+// CUs in whole waves where the projection widths are multiples of 192 and not
+// of 256 (1152, 3072, 4608, 12288 columns); 192x192 holds three stages in LDS
+// and quantises rows more finely than 256-row tiles.
+constexpr int dl_waves(int bm, int bn) { return bm * bn >= 192 * 192 ? 8 : 4; }
 
 template <int BM, int BN, int S, int EPI>
 __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmDesc g) {
@@ -561,6 +562,10 @@ constexpr TileCost kCost[] = {
      {23.6, 44.1, 81.1, 79.3, 103.5, 98.8, 114.7, 172.7, 215.0, 360.7, 556.3, 541.7, 843.8}},
     {256, 192, 2, {1.056, 2.152, 3.243, 4.544, 6.230, 7.835, 9.340, 10.339, 14.877, 19.229, 30.646, 39.311, 59.356},
      {18.8, 29.5, 40.4, 47.4, 49.2, 51.8, 61.3, 82.1, 173.6, 237.3, 322.0, 447.8, 652.3}},
+    {192, 192, 2, {0.897, 1.802, 2.688, 3.442, 4.039, 5.675, 6.665, 8.428, 12.631, 17.056, 25.517, 34.277, 50.877},
+     {14.7, 23.3, 33.4, 54.9, 80.7, 60.6, 75.1, 59.2, 109.6, 142.3, 209.1, 273.6, 439.7}},
+    {192, 192, 3, {0.918, 1.858, 2.544, 3.481, 3.979, 5.346, 6.764, 7.776, 11.618, 15.656, 23.449, 31.492, 47.153},
+     {15.4, 24.3, 43.5, 53.6, 83.8, 82.1, 72.7, 77.7, 122.1, 163.2, 235.1, 299.6, 456.9}},
     {256, 128, 2, {0.865, 1.797, 2.624, 3.601, 4.574, 5.530, 6.697, 7.757, 11.686, 15.233, 23.217, 31.222, 46.550},
      {21.3, 35.0, 50.1, 62.9, 73.9, 85.7, 91.4, 100.0, 147.7, 223.4, 316.3, 421.8, 611.1}},
     {256, 128, 3, {0.885, 1.787, 2.633, 3.593, 4.522, 5.451, 6.686, 7.655, 11.689, 15.144, 23.001, 31.000, 46.451},
@@ -677,6 +682,7 @@ hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
     st = std::max(2, std::min(st, max_stages(g.bm, g.bn)));
     if (g.bm == 256 && g.bn == 256) return launch_dl<256, 256, 2>(g, s);
     if (g.bm == 256 && g.bn == 192) return launch_dl<256, 192, 2>(g, s);
+    if (g.bm == 192 && g.bn == 192) return st >= 3 ? launch_dl<192, 192, 3>(g, s) : launch_dl<192, 192, 2>(g, s);
     if (g.bm == 256 && g.bn == 128) return st == 3 ? launch_dl<256, 128, 3>(g, s) : launch_dl<256, 128, 2>(g, s);
     if (g.bm == 128 && g.bn == 128)
         return st == 4 ? launch_dl<128, 128, 4>(g, s) : st == 3 ? launch_dl<128, 128, 3>(g, s) : launch_dl<128, 128, 2>(g, s);

@@ -1202,7 +1202,7 @@ ms_status ms_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* 
     if (ksplit < 0) return fail(MS_EINVAL, "ksplit must be >= 0");
     ms::GemmPlan p = ms::plan_gemm(dtype, M, N, K, d_ws ? ws_bytes / 4 : 0);
     if (tile_m || tile_n) {
-        const int ok_tiles[7][2] = {{256, 256}, {256, 192}, {256, 128}, {128, 128}, {128, 64}, {64, 128}, {64, 64}};
+        const int ok_tiles[8][2] = {{256, 256}, {256, 192}, {192, 192}, {256, 128}, {128, 128}, {128, 64}, {64, 128}, {64, 64}};
         bool ok = false;
         for (const auto& t : ok_tiles) ok |= (t[0] == tile_m && t[1] == tile_n);
         if (!ok || (dtype == MS_FP32 && !(tile_m == 64 && tile_n == 64)))
