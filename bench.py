@@ -172,6 +172,8 @@ FAMILY = {
     "gemm_qkv": (r"gemm_dl_kernel<\d+, \d+, \d, 3>", "paper_2505_20600_amd/csrc/gemm.hip"),
     "gemm_out": (r"gemm_dl_kernel<\d+, \d+, \d, 1>", "paper_2505_20600_amd/csrc/gemm.hip"),
     "gemm_down": (r"gemm_dl_kernel<\d+, \d+, \d, 4>", "paper_2505_20600_amd/csrc/gemm.hip"),
+    "gather": (r"::gather_kernel", "paper_2505_20600_amd/csrc/rows.hip"),
+    "scatter": (r"::(scatter_masked|merge)_kernel", "paper_2505_20600_amd/csrc/rows.hip"),
 }
 MARKER = "spin_kernel"
 

@@ -666,10 +666,10 @@ hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
         const char* v = std::getenv("MS_GEMM_PIPE");
         return v && std::strcmp(v, "staged") == 0;
     }();
-    static const int force_stages = [] {
-        const char* v = std::getenv("MS_GEMM_STAGES");
-        return v ? std::atoi(v) : 0;
-    }();
+    // tuning knob MS_GEMM_STAGES: the stage count of every direct-to-LDS
+    // launch (read per launch, so a test can take each stage variant in turn)
+    const char* fs = std::getenv("MS_GEMM_STAGES");
+    const int force_stages = fs ? std::atoi(fs) : 0;
     if (staged) {
         if (g.bm == 256 && g.bn == 256) return launch_tile<bf16_t, 256, 256>(g, s);
         if (g.bm == 256 && g.bn == 128) return launch_tile<bf16_t, 256, 128>(g, s);

@@ -9,7 +9,11 @@ from paper_2505_20600_amd import maskstep as MS
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-TILES = [(256, 256), (256, 192), (256, 128), (128, 128), (128, 64), (64, 128), (64, 64)]
+TILES = [(256, 256), (256, 192), (192, 192), (256, 128), (128, 128), (128, 64), (64, 128), (64, 64)]
+# every deeper stage variant the library builds (tile, stages); the forced-tile
+# tests above run two stages
+STAGED = [((192, 192), 3), ((256, 128), 3), ((128, 128), 3), ((128, 128), 4), ((128, 64), 3), ((128, 64), 4),
+          ((64, 128), 3), ((64, 128), 4), ((64, 64), 3), ((64, 64), 4)]
 
 
 def _ref(A, W, b, R, epi):
@@ -40,6 +44,38 @@ def test_linear_tiles_match_fp32_reference(tile, epi):
     torch.cuda.synchronize()
     e = _err(out, _ref(A, W, b, R, epi))
     print(f"[parity] tile {tile} epi {epi}: max-norm rel err {e:.2e}")
+    assert e <= 2e-2
+
+
+@pytest.fixture
+def stage_override():
+    """Sets MS_GEMM_STAGES for one test (the library reads it at every launch)."""
+    import os
+    old = os.environ.get("MS_GEMM_STAGES")
+    yield lambda n: os.environ.__setitem__("MS_GEMM_STAGES", str(n))
+    if old is None:
+        os.environ.pop("MS_GEMM_STAGES", None)
+    else:
+        os.environ["MS_GEMM_STAGES"] = old
+
+
+@pytest.mark.parametrize("tile,stages", STAGED, ids=lambda v: f"{v[0]}x{v[1]}" if isinstance(v, tuple) else f"s{v}")
+@pytest.mark.parametrize("shape", [(300, 516, 320), (4100, 3000, 704)], ids=["ragged", "persistent"])
+def test_linear_stage_variants_match_fp32_reference(tile, stages, shape, stage_override):
+    """Each multi-stage main loop: ragged edges, K steps fewer and more than
+    the stages, and (second shape) more tiles than resident workgroups."""
+    stage_override(stages)
+    g = torch.Generator(device=DEV).manual_seed(hash((tile, stages, shape)) % 1000)
+    M, N, K = shape
+    A = torch.randn(M, K, device=DEV, generator=g).bfloat16()
+    W = (torch.randn(N, K, device=DEV, generator=g) * 0.05).bfloat16()
+    b = (torch.randn(N, device=DEV, generator=g) * 0.05).bfloat16()
+    R = torch.randn(M, N, device=DEV, generator=g).bfloat16()
+    out = torch.empty(M, N, device=DEV, dtype=torch.bfloat16)
+    MS.ms_linear(A, W, b, out, resid=R, epilogue=MS.MS_EPI_BIAS_RESID, tile=tile, ksplit=1)
+    torch.cuda.synchronize()
+    e = _err(out, _ref(A, W, b, R, MS.MS_EPI_BIAS_RESID))
+    print(f"[parity] tile {tile} stages {stages} {shape}: max-norm rel err {e:.2e}")
     assert e <= 2e-2
 
 
