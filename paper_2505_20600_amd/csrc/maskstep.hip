@@ -1193,6 +1193,8 @@ ms_status ms_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* 
     if (M < 0 || N < 4 || K < 1 || N % 4) return fail(MS_ESHAPE, "need M >= 0, N a positive multiple of 4");
     const int bk = dtype == MS_BF16 ? 64 : 32;
     if (K % bk) return fail(MS_ESHAPE, "K must be a multiple of %d", bk);
+    // the bf16 kernels address a tile's rows (up to 256 x K) with 32-bit buffer offsets
+    if (dtype == MS_BF16 && (int64_t)K * 2 * 256 >= (1ll << 32)) return fail(MS_ESHAPE, "K must be below 2^23");
     if (epilogue < MS_EPI_BIAS || epilogue > MS_EPI_BIAS_GELU) return fail(MS_EINVAL, "unknown epilogue %d", epilogue);
     if (!A || !W || !bias || !out || (epilogue == MS_EPI_BIAS_RESID && !resid))
         return fail(MS_EINVAL, "NULL operand");

@@ -115,6 +115,21 @@ def test_step_init_validates_before_any_device_work():
         assert h.value is None
 
 
+def test_linear_validates_before_any_device_work():
+    """The row GEMM's shape checks come before any pointer or device use; the
+    bf16 kernels address a tile's rows with 32-bit offsets, so K stops below 2^23."""
+    lib = MS.load()
+    def call(dtype, M, N, K, epi=MS.MS_EPI_BIAS, tile=(0, 0)):
+        return lib.ms_linear(dtype, M, N, K, None, None, None, None, None, epi, tile[0], tile[1], 0, None, 0, None)
+    assert call(MS.MS_BF16, 16, 6, 64) == MS.MS_ESHAPE            # N not a multiple of 4
+    assert call(MS.MS_BF16, 16, 8, 96) == MS.MS_ESHAPE            # K not a multiple of 64
+    assert call(MS.MS_BF16, 16, 8, 1 << 23) == MS.MS_ESHAPE
+    assert "2^23" in lib.mask_last_error().decode()
+    assert call(MS.MS_BF16, 16, 8, (1 << 23) - 64, epi=7) == MS.MS_EINVAL
+    assert call(MS.MS_BF16, 16, 8, 64) == MS.MS_EINVAL            # NULL operands
+    assert call(7, 16, 8, 64) == MS.MS_EDTYPE
+
+
 def test_calls_without_a_step_context_fail_cleanly():
     lib = MS.load()
     assert lib.mask_gather_rows(None, 16, 16, None) == MS.MS_ESTATE
