@@ -75,8 +75,11 @@ struct GemmPlan {
     int bm, bn, ksplit, stages;
 };
 
-// Partial buffer the split-K plan may use (float32 elements).
-constexpr size_t kGemmPartFloats = size_t(4) << 20;
+// Partial buffer the split-K plans of a step may use (float32 elements):
+// 5461 rows of the model width (16 MiB at d_model 768, 64 MiB at 3072), so
+// the narrow row blocks whose N = d_model projections need a K split to fill
+// the CUs (e.g. 2048 text rows ahead of a LayerNorm) get one at every width.
+constexpr size_t gemm_part_floats(size_t d_model) { return size_t(5461) * d_model; }
 
 // Tile shape and K split for an M x N x K product on 256 CUs.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, size_t part_capacity_floats);

@@ -138,7 +138,7 @@ Layout make_layout(const ms_model_desc& d, int32_t B) {
     L.kv_dense = take(BT * 2 * dm * e);
     L.part_o = take(attn_part_rows(d, B) * dm * 2);   // bf16
     L.part_ml = take(attn_part_rows(d, B) * (size_t)d.n_heads * 2 * 4);
-    L.gemm_part = take(ms::kGemmPartFloats * 4);
+    L.gemm_part = take(ms::gemm_part_floats(dm) * 4);
     L.total = off;
     return L;
 }
@@ -365,7 +365,7 @@ struct LnAfter {
 // fused into the split-K sum when the plan splits K (bias + residual
 // epilogue only), else a LayerNorm launch of its own.
 hipError_t run_gemm(ms_step* s, ms::GemmDesc& g, int cls, hipStream_t st, const LnAfter* ln = nullptr) {
-    const ms::GemmPlan p = ms::plan_gemm(s->desc.dtype, g.M, g.N, g.K, ms::kGemmPartFloats);
+    const ms::GemmPlan p = ms::plan_gemm(s->desc.dtype, g.M, g.N, g.K, ms::gemm_part_floats(s->d));
     g.bm = p.bm;
     g.bn = p.bn;
     g.stages = p.stages;
