@@ -138,10 +138,11 @@ typedef struct {
     int32_t n_qtiles;    /* attention query tiles */
     int32_t text_rows;   /* packed rows that use the text weight set */
     int32_t dense_prefix;/* blocks computed over every token (mask_step_set_dense_prefix) */
-    int32_t copy_spans;  /* host-to-device copies one cached block's load issues */
-    int64_t copy_rows;   /* image rows those copies move (unmasked runs merged across short
-                            masked gaps, so >= the unmasked rows of the requests that
-                            recompute anything); bytes = rows x 2 d x elt (K/V) or d x elt (Y) */
+    int32_t copy_spans;  /* host-to-device copies one cached block's load issues (contiguous
+                            or strided 2-D; mask_plan_copies per recomputing request) */
+    int64_t copy_rows;   /* image rows those copies move (>= the unmasked rows of the
+                            requests that recompute anything: the plan may include masked
+                            rows); bytes = rows x 2 d x elt (K/V) or d x elt (Y) */
 } ms_step_info;
 
 /* Bytes of device workspace a step over `batch` requests needs (worst case,
@@ -207,6 +208,23 @@ ms_status mask_step_set_dense_prefix(ms_step* step, int32_t k, void* stream);
  * in *latency_ms_out (may be NULL). Host-only. */
 ms_status mask_plan_dense_prefix(int32_t n_layers, double load_ms, double cached_ms, double full_ms,
                                  int32_t* k_out, double* latency_ms_out);
+
+/* Cache-load plan of one request (block-wise loading, Sec. 4.2 and Fig. 8:
+ * a cached block loads the cached rows of the unmasked image tokens only), as
+ * the step context plans it for each request that recomputes rows.
+ * Host-only. mask: [grid_h * grid_w] uint8 of one request, row-major on the
+ * token grid, non-zero = masked. copy_cost_rows: what one copy command costs,
+ * in rows of link time (the step uses 512 KiB / (2 d_model x element size)).
+ * The plan is a list of copies; copy i is out[3i .. 3i+2] = (n0, w, h): image
+ * rows n0 + j * grid_w + [0, w) for j < h, one strided 2-D copy when h > 1
+ * (then w < grid_w), else one contiguous copy of w rows. The copies cover
+ * every unmasked row and may include masked ones; the planner minimises
+ * sum(copy_cost_rows + w * h) heuristically and never returns a plan costlier
+ * than unmasked runs merged across gaps of at most copy_cost_rows rows.
+ * *n_out receives the number of copies; MS_ESHAPE (nothing written) when it
+ * exceeds cap. out: caller-owned, 3 * cap int32. */
+ms_status mask_plan_copies(const uint8_t* mask, int32_t grid_h, int32_t grid_w, double copy_cost_rows,
+                           int32_t* out, int32_t cap, int32_t* n_out);
 
 /* Worker-load estimate (Sec. 4.3): linear regression models, fitted offline,
  * that map a batch's computation (FLOPs of Table 1 at the requests' mask
@@ -356,9 +374,10 @@ ms_status mask_profiler_intervals(int32_t* cls, double* start_ms, double* end_ms
 /* Message of the calling thread's last error ("" if none). */
 const char* mask_last_error(void);
 
-/* Version of this interface: 5 (2 added Y caching's kinds and calls, 3 the
+/* Version of this interface: 6 (2 added Y caching's kinds and calls, 3 the
  * cost-model and routing calls, 4 the copy figures of ms_step_info and
- * mask_profiler_intervals, 5 mask_step_init_static). */
+ * mask_profiler_intervals, 5 mask_step_init_static, 6 mask_plan_copies and
+ * strided 2-D cache loads). */
 int32_t mask_abi_version(void);
 
 #ifdef __cplusplus

@@ -17,7 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmaskstep.so")
 
-SOURCES = ["compact.hip", "rows.hip", "gemm.hip", "attention.hip", "maskstep.hip", "noalloc.hip"]
+SOURCES = ["compact.hip", "rows.hip", "gemm.hip", "attention.hip", "maskstep.hip", "noalloc.hip",
+           "copyplan.hip"]
 HEADERS = ["common.h", "kernels.h", "step_internal.h"]
 
 ARCH = "gfx950"

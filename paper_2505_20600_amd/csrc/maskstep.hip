@@ -21,20 +21,17 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 5;
+constexpr int32_t kAbiVersion = 6;
 constexpr int kMaxBatch = 64;
-// A block's cache load is one host-to-device copy per run of unmasked rows,
-// with runs merged across masked gaps that cost less link time than a copy of
-// their own. Measured on MI355X from pinned host memory: a copy costs the copy
-// engine ~9 us beyond its bytes (500 copies of 384 KiB run at 24 GB/s, 4 of
-// 48 MiB at 57 GB/s), worth ~512 KiB at the link's rate. Spreading the copies
+// A block's cache load is a set of host-to-device copies that covers the
+// unmasked rows (copyplan.hip). Measured on MI355X from pinned host memory: a
+// copy costs the copy engine ~9 us beyond its bytes (500 copies of 384 KiB
+// run at 24 GB/s, 4 of 48 MiB at 57 GB/s), worth ~512 KiB at the link's
+// rate, whether it is contiguous or a strided 2-D copy. Spreading the copies
 // over several streams hides that cost only while no kernels run: next to the
 // compute stream's GEMMs, hundreds of small copies per block crawl at 30-34
-// GB/s on 1, 2 or 4 streams, while merged copies keep the link's full rate.
-// Gaps of up to 512 KiB merge (on the 19-block d=3072 workload: 1.3x the
-// needed bytes at 56 GB/s, 52.5 ms per step, against 54.6 ms for 256 KiB and
-// 60 ms for 128 KiB).
-constexpr size_t kGapMergeBytes = 512 * 1024;
+// GB/s on 1, 2 or 4 streams. The plan prices a command at 512 KiB of rows.
+constexpr size_t kCopyCostBytes = 512 * 1024;
 
 thread_local std::string g_err;
 
@@ -144,7 +141,8 @@ Layout make_layout(const ms_model_desc& d, int32_t B) {
 }
 
 struct Span {
-    int b, n0, n1;   // image rows [n0, n1) of request b
+    int b;              // request
+    ms::CopyRect r;     // image rows r.n0 + i * grid_w + [0, r.w) for i < r.h
 };
 
 // One packed-row layout of the step: the masked rows, or every token (dense blocks).
@@ -282,30 +280,20 @@ bool request_recomputes(const ms_step* s, const uint8_t* m) {
     return false;
 }
 
+bool env_flag(const char* name);
+
 void plan_spans(ms_step* s, const std::vector<uint8_t>& mask) {
     s->spans.clear();
     const size_t row_bytes = 2ull * s->d * s->elt;
-    size_t gap_bytes = kGapMergeBytes;
-    if (const char* v = std::getenv("MS_COPY_GAP_BYTES")) gap_bytes = (size_t)std::atoll(v);   // tuning knob
-    const int gap_rows = (int)(gap_bytes / row_bytes);
+    size_t cost_bytes = kCopyCostBytes;
+    if (const char* v = std::getenv("MS_COPY_GAP_BYTES")) cost_bytes = (size_t)std::atoll(v);   // tuning knob
+    const double C = (double)cost_bytes / (double)row_bytes;
+    std::vector<ms::CopyRect> rects;
     for (int b = 0; b < s->B; ++b) {
         const uint8_t* m = mask.data() + (size_t)b * s->N;
         if (!request_recomputes(s, m)) continue;   // no query attends over its keys
-        int n = 0;
-        Span cur{b, -1, -1};
-        while (n < s->N) {
-            while (n < s->N && m[n]) ++n;
-            if (n >= s->N) break;
-            int n0 = n;
-            while (n < s->N && !m[n]) ++n;
-            if (cur.n0 >= 0 && n0 - cur.n1 <= gap_rows && gap_rows > 0) {
-                cur.n1 = n;
-            } else {
-                if (cur.n0 >= 0) s->spans.push_back(cur);
-                cur = Span{b, n0, n};
-            }
-        }
-        if (cur.n0 >= 0) s->spans.push_back(cur);
+        ms::plan_copies(m, s->desc.grid_h, s->desc.grid_w, C, !env_flag("MS_COPY_RUNS_ONLY"), rects);
+        for (const ms::CopyRect& r : rects) s->spans.push_back(Span{b, r});
     }
 }
 
@@ -560,11 +548,17 @@ ms_status prefetch(ms_step* s, HostLayer h, void* d_slot, hipStream_t cs, hipEve
     const size_t row_bytes = (y ? 1ull : 2ull) * s->d * s->elt;
     const size_t drows = y ? (size_t)s->N : (size_t)s->T, dtext = y ? 0 : (size_t)s->desc.n_text;
     char* dst = static_cast<char*>(d_slot);
+    const size_t pitch = (size_t)s->desc.grid_w * row_bytes;   // one grid row, host and device alike
     for (const Span& sp : s->spans) {
-        const char* src = h.req ? static_cast<const char*>(h.req[sp.b]) + (size_t)sp.n0 * row_bytes
-                                : static_cast<const char*>(h.base) + ((size_t)sp.b * s->N + sp.n0) * row_bytes;
-        const size_t dof = ((size_t)sp.b * drows + dtext + sp.n0) * row_bytes;
-        MS_HIP(hipMemcpyAsync(dst + dof, src, (size_t)(sp.n1 - sp.n0) * row_bytes, hipMemcpyHostToDevice, cs));
+        const ms::CopyRect& r = sp.r;
+        const char* src = h.req ? static_cast<const char*>(h.req[sp.b]) + (size_t)r.n0 * row_bytes
+                                : static_cast<const char*>(h.base) + ((size_t)sp.b * s->N + r.n0) * row_bytes;
+        const size_t dof = ((size_t)sp.b * drows + dtext + r.n0) * row_bytes;
+        if (r.h == 1)
+            MS_HIP(hipMemcpyAsync(dst + dof, src, (size_t)r.w * row_bytes, hipMemcpyHostToDevice, cs));
+        else
+            MS_HIP(hipMemcpy2DAsync(dst + dof, pitch, src, pitch, (size_t)r.w * row_bytes, (size_t)r.h,
+                                    hipMemcpyHostToDevice, cs));
     }
     return MS_OK;
 }
@@ -724,7 +718,7 @@ ms_status mask_step_get_info(const ms_step* s, ms_step_info* info) {
     info->dense_prefix = s->dense_prefix;
     info->copy_spans = (int32_t)s->spans.size();
     int64_t rows = 0;
-    for (const Span& sp : s->spans) rows += sp.n1 - sp.n0;
+    for (const Span& sp : s->spans) rows += (int64_t)sp.r.w * sp.r.h;
     info->copy_rows = rows;
     return ok();
 }
@@ -834,6 +828,26 @@ ms_status mask_plan_dense_prefix(int32_t n_layers, double load_ms, double cached
     double lat = 0.0;
     plan_prefix(n_layers, load_ms, cached_ms, full_ms, k_out, &lat);
     if (latency_ms_out) *latency_ms_out = lat;
+    return ok();
+}
+
+ms_status mask_plan_copies(const uint8_t* mask, int32_t grid_h, int32_t grid_w, double copy_cost_rows,
+                           int32_t* out, int32_t cap, int32_t* n_out) {
+    if (!mask || !n_out) return fail(MS_EINVAL, "mask and n_out must be non-NULL");
+    if (grid_h < 1 || grid_w < 1 || (int64_t)grid_h * grid_w > (1 << 20))
+        return fail(MS_ESHAPE, "grid %d x %d: need 1 .. 2^20 image tokens", grid_h, grid_w);
+    if (!(copy_cost_rows >= 0.0) || !std::isfinite(copy_cost_rows))
+        return fail(MS_EINVAL, "copy_cost_rows must be finite and >= 0");
+    if (cap < 0 || (cap > 0 && !out)) return fail(MS_EINVAL, "need cap >= 0 and out when cap > 0");
+    std::vector<ms::CopyRect> rects;
+    ms::plan_copies(mask, grid_h, grid_w, copy_cost_rows, true, rects);
+    *n_out = (int32_t)rects.size();
+    if ((int64_t)rects.size() > cap) return fail(MS_ESHAPE, "the plan has %d copies, cap is %d", *n_out, cap);
+    for (size_t i = 0; i < rects.size(); ++i) {
+        out[3 * i] = rects[i].n0;
+        out[3 * i + 1] = rects[i].w;
+        out[3 * i + 2] = rects[i].h;
+    }
     return ok();
 }
 

@@ -10,6 +10,8 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+import numpy as np
+
 import torch  # loads torch's HIP runtime first, so the library binds to the same one
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -97,6 +99,7 @@ def load() -> C.CDLL:
             "mask_profiler_stop": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
             "mask_profiler_intervals": (i32, [C.POINTER(C.c_int32), C.POINTER(C.c_double), C.POINTER(C.c_double),
                                               i32, C.POINTER(C.c_int32)]),
+            "mask_plan_copies": (i32, [vp, i32, i32, C.c_double, C.POINTER(i32), i32, C.POINTER(i32)]),
             "mask_fit_linear": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_double), i32, C.POINTER(C.c_double),
                                       C.POINTER(C.c_double), C.POINTER(C.c_double)]),
             "mask_batch_cost": (i32, [C.POINTER(ModelDesc), C.POINTER(CostModel), C.POINTER(i32), i32,
@@ -121,7 +124,7 @@ EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask
             "mask_stack_forward", "mask_step_destroy",
             "mask_step_set_dense_prefix", "mask_plan_dense_prefix",
             "mask_profiler_start", "mask_profiler_stop", "mask_profiler_intervals", "ms_linear",
-            "mask_fit_linear", "mask_batch_cost", "mask_route_request")
+            "mask_fit_linear", "mask_batch_cost", "mask_route_request", "mask_plan_copies")
 
 MS_EPI_BIAS, MS_EPI_BIAS_RESID, MS_EPI_BIAS_GELU = 0, 1, 2
 
@@ -211,6 +214,20 @@ def mask_plan_dense_prefix(n_layers: int, load_ms: float, cached_ms: float, full
     lat = C.c_double()
     _check(load().mask_plan_dense_prefix(n_layers, load_ms, cached_ms, full_ms, C.byref(k), C.byref(lat)))
     return k.value, lat.value
+
+
+def mask_plan_copies(mask, grid_h: int, grid_w: int, copy_cost_rows: float):
+    """Copies (n0, w, h) of one request's cache-load plan: rows n0 + j * grid_w + [0, w), j < h."""
+    m = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8).reshape(-1))
+    if m.size != grid_h * grid_w:
+        raise ValueError(f"mask has {m.size} entries, the grid {grid_h} x {grid_w}")
+    n = C.c_int32()
+    st = load().mask_plan_copies(m.ctypes.data, grid_h, grid_w, copy_cost_rows, None, 0, C.byref(n))
+    if st not in (MS_OK, MS_ESHAPE) or (st == MS_ESHAPE and n.value == 0):
+        _check(st)
+    out = (C.c_int32 * max(1, 3 * n.value))()
+    _check(load().mask_plan_copies(m.ctypes.data, grid_h, grid_w, copy_cost_rows, out, n.value, C.byref(n)))
+    return [(out[3 * i], out[3 * i + 1], out[3 * i + 2]) for i in range(n.value)]
 
 
 def mask_fit_linear(x, y):

@@ -17,45 +17,50 @@ def _gpu():
         pytest.fail("no GPU visible: the gpu-marked tests must run on an MI355X")
 
 
-def _spans(mask, gap_rows, recomputes):
-    """Unmasked runs of each recomputing request, merged across masked gaps of <= gap_rows."""
-    out = []
-    for b, m in enumerate(mask):
-        if not recomputes[b]:
-            continue
-        runs, n, N = [], 0, len(m)
-        while n < N:
-            while n < N and m[n]:
-                n += 1
-            if n >= N:
-                break
-            n0 = n
-            while n < N and not m[n]:
-                n += 1
-            if runs and n0 - runs[-1][1] <= gap_rows:
-                runs[-1][1] = n
-            else:
-                runs.append([n0, n])
-        out += runs
-    return out
-
-
 @pytest.mark.parametrize("d_model", [256, 3072])
-def test_copy_rows_are_the_merged_unmasked_runs(d_model):
-    shape = W.ModelShape("spans", 2, d_model, d_model // 64, 4, 32, 32, dtype="bf16", batch=3)
+def test_copy_figures_are_the_planned_copies(d_model):
+    """copy_spans / copy_rows of a step context are the cache-load plans of its
+    recomputing requests (mask_plan_copies, a command priced at 512 KiB)."""
+    shape = W.ModelShape("spans", 2, d_model, d_model // 64, 4, 32, 32, dtype="bf16", batch=4)
     g = np.random.default_rng(5)
-    mask = np.zeros((3, shape.n_image), np.uint8)
+    mask = np.zeros((4, shape.n_image), np.uint8)
     mask[0, g.choice(shape.n_image, 300, replace=False)] = 1      # scattered: many short gaps
     mask[1, 100:400] = 1                                           # one long gap
-    # request 2 recomputes nothing: no copies for it
+    mask[2].reshape(32, 32)[8:24, 4:28] = 1                        # a rectangle: a strided copy at d 3072
+    # request 3 recomputes nothing: no copies for it
     step = G.new_step(shape, mask)
     info = step.info()
-    row_bytes = 2 * d_model * 2
-    spans = _spans(mask, (512 * 1024) // row_bytes, [True, True, False])   # gaps up to 512 KiB merge
-    assert info.copy_spans == len(spans)
-    assert info.copy_rows == sum(b - a for a, b in spans)
-    unmasked = int((mask[:2] == 0).sum())
-    assert info.copy_rows >= unmasked
+    C = (512 * 1024) / (2 * d_model * 2)
+    plans = [MS.mask_plan_copies(mask[b], 32, 32, C) for b in range(3)]
+    assert info.copy_spans == sum(len(p) for p in plans)
+    assert info.copy_rows == sum(w * h for p in plans for _, w, h in p)
+    assert info.copy_rows >= int((mask[:3] == 0).sum())
+    if d_model == 3072:
+        assert any(h > 1 for p in plans for _, _, h in p)
+
+
+def test_strided_cache_loads_match_resident(monkeypatch):
+    """Blob masks with a command priced at 8 KiB (a few 1 KiB K/V rows), so the
+    loads are strided 2-D copies around the blobs: streamed == resident, bit for
+    bit, in both cache forms."""
+    monkeypatch.setenv("MS_COPY_GAP_BYTES", "8192")
+    shape = W.ModelShape("strided", 3, 256, 2, 4, 16, 16, n_text=0, dtype="bf16", batch=2)
+    ws = W.stack_weights(shape, 91, random_ln=True, std=0.03)
+    xt = W.template_hidden(shape, 91)
+    kv = np.stack([W.synthetic_kv_cache(shape, 91, l) for l in range(shape.n_layers)])
+    yc = W.synthetic_y_cache(shape, 91)
+    mask = np.stack([W.blob_mask(16, 16, r, W.rng(91, 3, b)) for b, r in enumerate((0.3, 0.5))])
+    x = W.edited_hidden(shape, 91, xt, mask)
+    plans = [MS.mask_plan_copies(m, 16, 16, 8192 / (2 * 256 * 2)) for m in mask]
+    assert any(h > 1 for p in plans for _, _, h in p)
+    y_res, _, step = G.run_stack(shape, mask, x, kv, yc, ws)
+    assert step.info().copy_spans == sum(len(p) for p in plans)
+    y_kv, _, _ = G.run_stack(shape, mask, x, kv, yc, ws, pinned=True, n_slots=2)
+    np.testing.assert_array_equal(y_kv, y_res)
+    yin = np.stack([np.asarray(yc)[:, shape.n_text:]] * shape.n_layers)
+    y_y, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True, pinned=True, n_slots=2)
+    y_yres, _, _ = G.run_stack(shape, mask, x, yin, yc, ws, inputs=True)
+    np.testing.assert_array_equal(y_y, y_yres)
 
 
 def test_profiler_intervals_match_the_totals():
