@@ -844,7 +844,7 @@ def main():
     if pinned and not args.no_profile_pass:
         stream_info = stream_overlap(MS.profiler_intervals(), args.steps)
         row_bytes = (1 if yc_mode else 2) * shape.d_model * (2 if shape.dtype == "bf16" else 4)
-        copy_rows = [c.info().copy_rows for c in ctx]
+        copy_rows = [c.info().copy_rows_y if yc_mode else c.info().copy_rows for c in ctx]
         copied = sum((shape.n_layers - prefix[s % args.masks]) * copy_rows[s % args.masks]
                      for s in range(args.steps)) * row_bytes
         needed = sum((shape.n_layers - prefix[s % args.masks]) * unmasked[s % args.masks]

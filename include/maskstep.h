@@ -138,11 +138,14 @@ typedef struct {
     int32_t n_qtiles;    /* attention query tiles */
     int32_t text_rows;   /* packed rows that use the text weight set */
     int32_t dense_prefix;/* blocks computed over every token (mask_step_set_dense_prefix) */
-    int32_t copy_spans;  /* host-to-device copies one cached block's load issues (contiguous
-                            or strided 2-D; mask_plan_copies per recomputing request) */
+    int32_t copy_spans;  /* host-to-device copies one cached block's K/V load issues
+                            (contiguous or strided 2-D; mask_plan_copies per recomputing
+                            request, a command priced at 512 KiB of rows) */
     int64_t copy_rows;   /* image rows those copies move (>= the unmasked rows of the
                             requests that recompute anything: the plan may include masked
-                            rows); bytes = rows x 2 d x elt (K/V) or d x elt (Y) */
+                            rows); bytes = rows x 2 d x elt */
+    int32_t copy_spans_y;/* the same for a Y-cache load (rows of d elements: a command */
+    int64_t copy_rows_y; /*  is worth twice as many rows); bytes = rows x d x elt */
 } ms_step_info;
 
 /* Bytes of device workspace a step over `batch` requests needs (worst case,
@@ -376,8 +379,8 @@ const char* mask_last_error(void);
 
 /* Version of this interface: 6 (2 added Y caching's kinds and calls, 3 the
  * cost-model and routing calls, 4 the copy figures of ms_step_info and
- * mask_profiler_intervals, 5 mask_step_init_static, 6 mask_plan_copies and
- * strided 2-D cache loads). */
+ * mask_profiler_intervals, 5 mask_step_init_static, 6 mask_plan_copies,
+ * strided 2-D cache loads and the Y-load figures of ms_step_info). */
 int32_t mask_abi_version(void);
 
 #ifdef __cplusplus

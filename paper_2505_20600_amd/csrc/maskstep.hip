@@ -201,7 +201,7 @@ struct ms_step {
     Packing dp;                 // every token (dense-prefix blocks), built on first use
     bool dense_ready = false;
     int dense_prefix = 0;
-    std::vector<Span> spans;
+    std::vector<Span> spans, spans_y;   // cache-load copies of one block: K/V rows, Y rows
     // unmasked image rows: index into a [B][N] input cache and flat token row (Y caching)
     int U = 0;
     std::vector<int32_t> h_usrc, h_utok;
@@ -283,17 +283,21 @@ bool request_recomputes(const ms_step* s, const uint8_t* m) {
 bool env_flag(const char* name);
 
 void plan_spans(ms_step* s, const std::vector<uint8_t>& mask) {
-    s->spans.clear();
-    const size_t row_bytes = 2ull * s->d * s->elt;
     size_t cost_bytes = kCopyCostBytes;
     if (const char* v = std::getenv("MS_COPY_GAP_BYTES")) cost_bytes = (size_t)std::atoll(v);   // tuning knob
-    const double C = (double)cost_bytes / (double)row_bytes;
+    const bool strided = !env_flag("MS_COPY_RUNS_ONLY");
     std::vector<ms::CopyRect> rects;
-    for (int b = 0; b < s->B; ++b) {
-        const uint8_t* m = mask.data() + (size_t)b * s->N;
-        if (!request_recomputes(s, m)) continue;   // no query attends over its keys
-        ms::plan_copies(m, s->desc.grid_h, s->desc.grid_w, C, !env_flag("MS_COPY_RUNS_ONLY"), rects);
-        for (const ms::CopyRect& r : rects) s->spans.push_back(Span{b, r});
+    // a command's price in rows depends on the row: 2 d elements (K/V) or d (Y)
+    for (int y = 0; y < 2; ++y) {
+        std::vector<Span>& out = y ? s->spans_y : s->spans;
+        out.clear();
+        const double C = (double)cost_bytes / (double)((y ? 1ull : 2ull) * s->d * s->elt);
+        for (int b = 0; b < s->B; ++b) {
+            const uint8_t* m = mask.data() + (size_t)b * s->N;
+            if (!request_recomputes(s, m)) continue;   // no query attends over its keys
+            ms::plan_copies(m, s->desc.grid_h, s->desc.grid_w, C, strided, rects);
+            for (const ms::CopyRect& r : rects) out.push_back(Span{b, r});
+        }
     }
 }
 
@@ -549,7 +553,7 @@ ms_status prefetch(ms_step* s, HostLayer h, void* d_slot, hipStream_t cs, hipEve
     const size_t drows = y ? (size_t)s->N : (size_t)s->T, dtext = y ? 0 : (size_t)s->desc.n_text;
     char* dst = static_cast<char*>(d_slot);
     const size_t pitch = (size_t)s->desc.grid_w * row_bytes;   // one grid row, host and device alike
-    for (const Span& sp : s->spans) {
+    for (const Span& sp : y ? s->spans_y : s->spans) {
         const ms::CopyRect& r = sp.r;
         const char* src = h.req ? static_cast<const char*>(h.req[sp.b]) + (size_t)r.n0 * row_bytes
                                 : static_cast<const char*>(h.base) + ((size_t)sp.b * s->N + r.n0) * row_bytes;
@@ -717,9 +721,10 @@ ms_status mask_step_get_info(const ms_step* s, ms_step_info* info) {
     info->text_rows = s->mp.text_rows;
     info->dense_prefix = s->dense_prefix;
     info->copy_spans = (int32_t)s->spans.size();
-    int64_t rows = 0;
-    for (const Span& sp : s->spans) rows += (int64_t)sp.r.w * sp.r.h;
-    info->copy_rows = rows;
+    info->copy_spans_y = (int32_t)s->spans_y.size();
+    info->copy_rows = info->copy_rows_y = 0;
+    for (const Span& sp : s->spans) info->copy_rows += (int64_t)sp.r.w * sp.r.h;
+    for (const Span& sp : s->spans_y) info->copy_rows_y += (int64_t)sp.r.w * sp.r.h;
     return ok();
 }
 

@@ -55,7 +55,8 @@ class CostModel(C.Structure):
 class StepInfo(C.Structure):
     _fields_ = [("batch", C.c_int32), ("rows", C.c_int32), ("n_segments", C.c_int32),
                 ("n_qtiles", C.c_int32), ("text_rows", C.c_int32), ("dense_prefix", C.c_int32),
-                ("copy_spans", C.c_int32), ("copy_rows", C.c_int64)]
+                ("copy_spans", C.c_int32), ("copy_rows", C.c_int64), ("copy_spans_y", C.c_int32),
+                ("copy_rows_y", C.c_int64)]
 
 
 class MaskStepError(RuntimeError):

@@ -37,6 +37,9 @@ def test_copy_figures_are_the_planned_copies(d_model):
     assert info.copy_rows >= int((mask[:3] == 0).sum())
     if d_model == 3072:
         assert any(h > 1 for p in plans for _, _, h in p)
+    plans_y = [MS.mask_plan_copies(mask[b], 32, 32, 2 * C) for b in range(3)]   # Y rows: half the bytes
+    assert info.copy_spans_y == sum(len(p) for p in plans_y)
+    assert info.copy_rows_y == sum(w * h for p in plans_y for _, w, h in p)
 
 
 def test_strided_cache_loads_match_resident(monkeypatch):
