@@ -380,12 +380,11 @@ __global__ __launch_bounds__(kWave * dl_waves(BM, BN)) void gemm_dl_kernel(GemmD
     // row are XOR-swizzled by (row & 15), so both the 16-row writes and the
     // row-wise reads are conflict-free. Tiles too large for one pass stage
     // the rows of one wave row (BM / 2) at a time.
-    // Measured per epilogue (c2 / c4 / c5): staging pays for the QKV split
-    // (-7..-13%, its K/V rows are scattered) and the split-K partials; for
-    // the residual and GELU epilogues the direct stores are as fast or faster.
+    // The host picks the path per launch (GemmDesc::direct_out): direct
+    // stores only for the GELU epilogue of launches with few tiles per CU.
     const int hw_next = hw + (int)gridDim.x;
     const bool more = hw_next < total;
-    if (EPI != kEpiQKV && EPI != kEpiBias && g.ksplit == 1) {
+    if (EPI == kEpiBiasGelu && g.direct_out) {
         // direct stores from registers: the next tile's first stages load
         // during them (every wave is past its last read of the stages)
         const int cm0 = m0, cn0 = n0;
@@ -659,6 +658,18 @@ hipError_t launch_gemm(int dtype, GemmDesc& g, hipStream_t s) {
         return v ? std::max(1, std::atoi(v)) : 0;
     }();
     g.group_m = group_m > 0 ? group_m : (g.M >= kGroupLargeRows ? kGroupMLarge : kGroupM);
+    // Output path of the direct-to-LDS kernel: restaged through LDS (whole
+    // rows per store), except the unsplit GELU epilogue of launches with fewer
+    // than 8 tiles per CU, stored from registers so that the next tile's first
+    // loads run under the stores. Measured per shape against the other path
+    // (MI355X): residual epilogues restaged 1-6% faster or even everywhere
+    // (16384x3072x3072 362 -> 339 us); GELU restaged 10% faster at
+    // 16384x12288x3072 (12 tiles per CU), 1-6% slower at 2-3 (2048 and 4096 x
+    // 12288 x 3072, 6855x4608x1152).
+    {
+        const long tiles = (long)((g.M + g.bm - 1) / std::max(1, g.bm)) * ((g.N + g.bn - 1) / std::max(1, g.bn));
+        g.direct_out = g.epilogue == kEpiBiasGelu && g.ksplit == 1 && tiles < 8L * kCUs;
+    }
     if (dtype != kBF16) return launch_tile<float, 64, 64>(g, s);
     // main loop: direct-to-LDS (default) or the register-staged double buffer
     // (tuning knob MS_GEMM_PIPE=staged); MS_GEMM_STAGES overrides the stage count

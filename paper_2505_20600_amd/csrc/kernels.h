@@ -68,6 +68,7 @@ struct GemmDesc {
     int ksplit;         // K-range splits (1: epilogue fused in the GEMM)
     int kchunk;         // set by launch_gemm
     int group_m;        // set by launch_gemm: m-tiles per group of the tile order
+    int direct_out;     // set by launch_gemm: output stored from registers, not restaged in LDS
     float* part;        // ksplit > 1: [ksplit][M][N] float32 partials
 };
 

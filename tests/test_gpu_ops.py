@@ -139,13 +139,15 @@ def test_linear_rejects_bad_arguments():
         MS.ms_linear(A, W, b, out, ksplit=2)                          # no workspace
 
 
-@pytest.mark.parametrize("tile,M,N", [((64, 64), 4096, 2112), ((128, 64), 3000, 2048), ((256, 256), 4608, 4352)],
-                         ids=["64x64", "128x64", "256x256"])
+@pytest.mark.parametrize("tile,M,N", [((64, 64), 4096, 2112), ((128, 64), 3000, 2048), ((256, 256), 4608, 4352),
+                                      ((128, 64), 8192, 2048), ((256, 256), 16384, 8448)],
+                         ids=["64x64", "128x64", "256x256", "128x64-8-per-CU", "256x256-8-per-CU"])
 @pytest.mark.parametrize("epi", [MS.MS_EPI_BIAS, MS.MS_EPI_BIAS_RESID, MS.MS_EPI_BIAS_GELU],
                          ids=["bias", "resid", "gelu"])
 def test_linear_more_tiles_than_resident_workgroups(tile, M, N, epi):
     """More tiles than the CUs hold at once: each workgroup loops over several tiles,
-    loading the next tile's first stages during the current tile's epilogue."""
+    loading the next tile's first stages during the current tile's epilogue. With 8
+    or more tiles per CU the GELU output is restaged through LDS too."""
     g = torch.Generator(device=DEV).manual_seed(hash((tile, epi, M)) % 1000)
     K = 192
     A = torch.randn(M, K, device=DEV, generator=g).bfloat16()
