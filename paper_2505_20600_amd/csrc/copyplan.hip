@@ -21,7 +21,9 @@
 //      order, a run that repeats the run one grid row earlier joining that
 //      run's strided copy,
 //   4. drops, one at a time, holes whose removal lowers the modelled cost
-//      (band boundaries add commands the band-wise model does not see),
+//      (band boundaries add commands the band-wise model does not see; bands
+//      and this pass are bounded so that the host time stays linear in the
+//      tokens),
 //   5. keeps the plan only if it is cheaper than plain runs merged across
 //      gaps shorter than one command's cost.
 // Cost model: every command costs `C` rows of link time, plus one row per row
@@ -42,6 +44,13 @@ struct Iv {
 struct Hole {
     int x0, x1, y0, y1;   // masked columns [x0, x1) of grid rows [y0, y1)
 };
+
+// Bounds on the planner's host time for tall grids and busy masks: bands of
+// at most kMaxBandRows rows (the band search is linear in the track length
+// times this), and the hole-dropping pass (each trial rebuilds the plan) only
+// while holes x tokens stays below kDropWork.
+constexpr int kMaxBandRows = 256;
+constexpr int64_t kDropWork = int64_t(1) << 26;
 
 double plan_cost(const std::vector<CopyRect>& p, double C) {
     double c = 0.0;
@@ -111,6 +120,7 @@ void band_holes(const uint8_t* m, int H, int P, double C, std::vector<Hole>& hol
     for (int y = 0; y < H; ++y) {
         cur.clear();
         const uint8_t* r = m + (size_t)y * P;
+        size_t p = 0;
         int x = 0;
         while (x < P) {
             while (x < P && !r[x]) ++x;
@@ -118,10 +128,14 @@ void band_holes(const uint8_t* m, int H, int P, double C, std::vector<Hole>& hol
             const int a = x;
             while (x < P && r[x]) ++x;
             const Iv iv{a, x};
+            // the first interval above that overlaps this one and whose track
+            // has no interval in this row yet (both rows are sorted: `p` only
+            // moves forward)
+            while (p < prev.size() && prev[p].first.e <= iv.a) ++p;
             int t = -1;
-            for (const auto& pt : prev)
-                if (used_in_row[pt.second] != y && pt.first.a < iv.e && iv.a < pt.first.e) {
-                    t = pt.second;
+            for (size_t q = p; q < prev.size() && prev[q].first.a < iv.e; ++q)
+                if (used_in_row[prev[q].second] != y) {
+                    t = prev[q].second;
                     break;
                 }
             if (t < 0) {
@@ -150,7 +164,7 @@ void band_holes(const uint8_t* m, int H, int P, double C, std::vector<Hole>& hol
             pick[i] = Hole{0, 0, 0, 0};
             int lo = 0, hi = P;
             double masked = 0.0;
-            for (int j = i - 1; j >= 0; --j) {
+            for (int j = i - 1; j >= std::max(0, i - kMaxBandRows); --j) {
                 lo = std::max(lo, tr.iv[j].a);
                 hi = std::min(hi, tr.iv[j].e);
                 if (hi <= lo) break;   // no common rectangle for this band or any longer one
@@ -195,6 +209,7 @@ void plan_copies(const uint8_t* m, int H, int P, double C, bool strided, std::ve
         return (int64_t)(holes[a].x1 - holes[a].x0) * (holes[a].y1 - holes[a].y0) <
                (int64_t)(holes[b].x1 - holes[b].x0) * (holes[b].y1 - holes[b].y0);
     });
+    if ((int64_t)holes.size() * N > kDropWork) order.clear();
     for (int i : order) {
         live[i] = 0;
         copies_outside(holes, live, H, P, keep, trial);

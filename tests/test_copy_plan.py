@@ -139,3 +139,25 @@ def test_plan_copies_validates_arguments():
     st = MS.load().mask_plan_copies(two.ctypes.data, 8, 8, 0.0, out, 1, C.byref(n))
     assert st == MS.MS_ESHAPE and n.value == 2   # two copies, room for one
     assert MS.load().mask_plan_copies(None, 8, 8, 0.0, out, 1, C.byref(n)) == MS.MS_EINVAL
+
+
+@pytest.mark.parametrize("H,P,kind", [(65536, 16, "column"), (1 << 20, 1, "runs"), (1024, 1024, "checker")])
+def test_planner_time_stays_bounded_on_tall_and_busy_grids(H, P, kind):
+    """The band search and the hole-dropping pass are bounded, so the planner's
+    host time stays linear in the tokens (these took seconds to minutes with an
+    unbounded band search)."""
+    import time
+    m = np.zeros((H, P), np.uint8)
+    if kind == "column":
+        m[:, 4:8] = 1
+    elif kind == "runs":
+        m[(np.arange(H) // 50) % 2 == 0] = 1
+    else:
+        m[::2, ::2] = 1
+        m[1::2, 1::2] = 1
+    t = time.perf_counter()
+    plan = MS.mask_plan_copies(m.reshape(-1), H, P, 42.7)
+    assert time.perf_counter() - t < 3.0
+    _check_plan(plan, m.reshape(-1), P)
+    if kind == "column":
+        assert plan == [(0, 4, 1), (8, 12, H - 1), ((H - 1) * P + 8, 8, 1)]
