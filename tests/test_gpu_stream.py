@@ -87,3 +87,49 @@ def test_profiler_intervals_match_the_totals():
         assert 0.0 <= a <= b
     for c, (ms, n) in tot.items():
         assert sum(b - a for cc, a, b in iv if cc == c) == pytest.approx(ms, rel=1e-3, abs=1e-3)
+
+
+@pytest.mark.parametrize("n_slots", [2, 5])
+def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots):
+    """Steps of two step contexts (different masks, different host caches) issued
+    back to back through the same slots, with no synchronisation between the
+    calls: a call's loads must not overwrite a slot the previous call's blocks
+    still read. Every output equals the same step run alone."""
+    shape = W.ModelShape("b2b", 5, 256, 2, 4, 16, 16, n_text=0, dtype="bf16", batch=2)
+    ws = W.stack_weights(shape, 93, random_ln=True, std=0.03)
+    dw = G.dev_weights(ws, shape)
+    wc = MS.weights_array(dw)
+    xt = W.template_hidden(shape, 93)
+    d_yc = G.to_dev(W.synthetic_y_cache(shape, 93), shape)
+    masks = [np.stack([W.blob_mask(16, 16, r, W.rng(93, 3, 10 * c + b)) for b, r in enumerate(rs)])
+             for c, rs in enumerate(((0.2, 0.4), (0.35, 0.1)))]
+    steps = [G.new_step(shape, m) for m in masks]
+    hosts = []
+    for c in range(2):
+        layers = []
+        for l in range(shape.n_layers):
+            img = W.synthetic_kv_cache(shape, 200 + c, l)[:, shape.n_text:]
+            t = torch.empty(img.shape, dtype=torch.bfloat16, pin_memory=True)
+            t.copy_(torch.as_tensor(np.ascontiguousarray(img, np.float32)).to(torch.bfloat16))
+            layers.append(t)
+        hosts.append(layers)
+    xs = [G.to_dev(W.edited_hidden(shape, 93, xt, m), shape) for m in masks]
+    slots = [torch.full((shape.batch, shape.n_tokens, 2, shape.d_model), float("nan"), dtype=torch.bfloat16,
+                        device=G.DEV) for _ in range(n_slots)]
+    copy = torch.cuda.Stream()
+    alone = []
+    for c in range(2):
+        y = torch.empty_like(d_yc)
+        steps[c].stack_forward(wc, xs[c], d_yc, hosts[c], y, pinned=True, slots=slots, copy_stream=copy)
+        torch.cuda.synchronize()
+        alone.append(y)
+    outs = []
+    for i in range(6):
+        c = i % 2
+        y = torch.empty_like(d_yc)
+        steps[c].stack_forward(wc, xs[c], d_yc, hosts[c], y, pinned=True, slots=slots, copy_stream=copy)
+        outs.append((c, y))
+    torch.cuda.synchronize()
+    assert not torch.equal(alone[0], alone[1])
+    for c, y in outs:
+        assert torch.equal(y, alone[c]), f"context {c}"
