@@ -103,9 +103,19 @@ typedef enum {
  *                     buffers; the j-th cached layer of the step uses
  *                     slots[j % n_slots], and its load (on the copy stream)
  *                     waits until the compute stream has finished with the
- *                     layer that used the slot before. With n_slots >= the
- *                     number of cached layers every load starts at once
- *                     (MI355X's HBM holds a whole stack's K/V easily).
+ *                     layer that used the slot before. Across calls: right
+ *                     after a mask_stack_forward call that streamed through
+ *                     the same list of slots (any step context), a call's
+ *                     first loads wait only for the blocks of that call that
+ *                     read their slots (its first half of cached blocks, then
+ *                     all of them), so in a run of steps the next step's
+ *                     loads start under the current step's last blocks;
+ *                     otherwise a call's loads wait for the call's start on
+ *                     the compute stream. A caller that writes or frees slot
+ *                     buffers orders that after the calls that use them.
+ *                     With n_slots >= the number of cached layers every load
+ *                     starts at once (MI355X's HBM holds a whole stack's K/V
+ *                     easily).
  *  MS_Y_DEVICE:       layer[l] is a device [B][N][d] buffer: block l's cached
  *                     input hidden state of the image tokens (only unmasked
  *                     rows are read). Each cached block recomputes the K/V of

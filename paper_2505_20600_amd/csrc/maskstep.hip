@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
 #include <new>
 #include <string>
 #include <vector>
@@ -206,6 +207,7 @@ struct ms_step {
     int U = 0;
     std::vector<int32_t> h_usrc, h_utok;
     std::vector<hipEvent_t> ev_copied, ev_consumed;   // created on first streamed use
+    uint64_t stack_calls = 0;   // mask_stack_forward calls on this context (event set parity)
     hipEvent_t ev_start = nullptr;
     int static_dev = -1;        // device whose static scratch is the workspace (mask_step_init_static)
 
@@ -223,6 +225,52 @@ void destroy_events(ms_step* s) {
     s->ev_consumed.clear();
     if (s->ev_start) (void)hipEventDestroy(s->ev_start);
     s->ev_start = nullptr;
+}
+
+// Release events of a slot ring (one per device and list of slot buffers),
+// recorded on the compute stream by the last call that streamed through it:
+// `half` after the block that read slot h - 1 (slots [0, h) free from then
+// on; h = 0 when a slot was read twice), `all` after its last cached block.
+// The next call's copy stream waits on `half` before its first load and on
+// `all` before its load into slot h, instead of waiting for the call's start:
+// its first loads then overlap the previous step's last blocks.
+struct RingRelease {
+    hipEvent_t half[2] = {nullptr, nullptr}, all[2] = {nullptr, nullptr};   // by call parity
+    int h = 0;
+    bool recorded = false;
+    uint64_t call = 0;   // the mask_stack_forward call that recorded them
+};
+std::mutex g_ring_mu;
+std::atomic<uint64_t> g_stack_calls{0};
+std::map<std::pair<int, std::vector<const void*>>, RingRelease> g_ring;
+
+ms_status ring_release(const ms_kv_source* kv, RingRelease** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(MS_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    std::vector<const void*> key(kv->slots, kv->slots + kv->n_slots);
+    std::lock_guard<std::mutex> lk(g_ring_mu);
+    RingRelease& r = g_ring[std::make_pair(dev, std::move(key))];
+    for (int i = 0; i < 2; ++i) {
+        if (!r.half[i]) {
+            e = hipEventCreateWithFlags(&r.half[i], hipEventDisableTiming);
+            if (e == hipSuccess) e = hipEventCreateWithFlags(&r.all[i], hipEventDisableTiming);
+            if (e != hipSuccess) {
+                if (r.half[i]) (void)hipEventDestroy(r.half[i]);
+                r.half[i] = r.all[i] = nullptr;
+                return fail(MS_EHIP, "event creation: %s", hipGetErrorString(e));
+            }
+        }
+    }
+    *out = &r;
+    return MS_OK;
+}
+
+// The per-block calls touch slots outside any ring's release events: the next
+// mask_stack_forward then waits for its own start again.
+void forget_rings() {
+    std::lock_guard<std::mutex> lk(g_ring_mu);
+    for (auto& kv : g_ring) kv.second.recorded = false;
 }
 
 ms_status ensure_events(ms_step* s, int n) {
@@ -962,6 +1010,7 @@ ms_status mask_gather_rows(ms_step* s, const void* d_x, void* d_xm, void* stream
 ms_status mask_block_forward(ms_step* s, int32_t layer, const ms_layer_weights* w, void* d_xm,
                              void* d_kv, void* stream) {
     if (!s) return fail(MS_ESTATE, "no step context");
+    forget_rings();
     if (layer < 0 || layer >= s->desc.n_layers) return fail(MS_EINVAL, "layer %d out of range", layer);
     if (!w || !d_kv) return fail(MS_EINVAL, "weights or kv is NULL");
     void* xm = d_xm ? d_xm : s->buf(s->lay.xm);
@@ -988,6 +1037,7 @@ ms_status mask_scatter_rows(ms_step* s, const void* d_xm, const void* d_ycache, 
 ms_status cache_prefetch_layer(ms_step* s, int32_t layer, const void* h_kv, void* d_slot,
                                void* copy_stream, void* wait_event, void* signal_event) {
     if (!s) return fail(MS_ESTATE, "no step context");
+    forget_rings();
     if (layer < 0 || layer >= s->desc.n_layers) return fail(MS_EINVAL, "layer %d out of range", layer);
     if (!h_kv || !d_slot) return fail(MS_EINVAL, "h_kv or slot is NULL");
     if (!aligned16(h_kv) || !aligned16(d_slot)) return fail(MS_EALIGN, "h_kv / slot not 16-byte aligned");
@@ -1001,6 +1051,7 @@ ms_status cache_prefetch_layer(ms_step* s, int32_t layer, const void* h_kv, void
 ms_status cache_prefetch_inputs(ms_step* s, int32_t layer, const void* h_yin, void* d_slot,
                                 void* copy_stream, void* wait_event, void* signal_event) {
     if (!s) return fail(MS_ESTATE, "no step context");
+    forget_rings();
     if (layer < 0 || layer >= s->desc.n_layers) return fail(MS_EINVAL, "layer %d out of range", layer);
     if (!h_yin || !d_slot) return fail(MS_EINVAL, "h_yin or slot is NULL");
     if (!aligned16(h_yin) || !aligned16(d_slot)) return fail(MS_EALIGN, "h_yin / slot not 16-byte aligned");
@@ -1014,6 +1065,7 @@ ms_status cache_prefetch_inputs(ms_step* s, int32_t layer, const void* h_yin, vo
 ms_status mask_recompute_kv(ms_step* s, int32_t layer, const ms_layer_weights* w, const void* d_yin,
                             void* d_kv, void* stream) {
     if (!s) return fail(MS_ESTATE, "no step context");
+    forget_rings();
     if (layer < 0 || layer >= s->desc.n_layers) return fail(MS_EINVAL, "layer %d out of range", layer);
     if (!w || !d_kv || (!d_yin && s->U > 0)) return fail(MS_EINVAL, "NULL argument");
     if (!aligned16(d_yin) || !aligned16(d_kv)) return fail(MS_EALIGN, "pointer not 16-byte aligned");
@@ -1059,6 +1111,10 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         return per_req ? HostLayer{nullptr, kv->request_layer + (size_t)l * s->B} : HostLayer{kv->layer[l], nullptr};
     };
     const int n_slots = pinned ? kv->n_slots : 0;
+    const uint64_t call_id = ++g_stack_calls;
+    // this call's load-landed events: alternate sets, so that no event is recorded again while
+    // a wait of the previous call on it may still be pending
+    const int ecp = (int)(s->stack_calls++ & 1) * (pinned ? kv->n_slots : 0);
     if (pinned) {
         if (n_slots < 1 || !kv->slots) return fail(MS_EINVAL, "a pinned cache needs n_slots >= 1 device slots");
         for (int i = 0; i < n_slots; ++i) {
@@ -1072,7 +1128,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 if (st != MS_OK) return st;
             }
         }
-        ms_status st = ensure_events(s, n_slots);
+        ms_status st = ensure_events(s, 2 * n_slots);
         if (st != MS_OK) return st;
     }
     if (!aligned16(d_x) || !aligned16(d_y) || !aligned16(d_ycache)) return fail(MS_EALIGN, "pointer not 16-byte aligned");
@@ -1093,23 +1149,43 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         // host stays far ahead of both streams either way).
         int issued = 0, launched = 0;
         auto allowed = [&]() { return std::min(n_cached, launched + n_slots); };
+        // the copy stream must not overwrite a slot an earlier call still reads: wait for the
+        // ring's release by the last call that streamed through it, else for this call's start
+        RingRelease* ring = nullptr;
+        int prev_h = 0;
+        bool prev_known = false;
+        if (stream_cache) {
+            ms_status st = ring_release(kv, &ring);
+            if (st != MS_OK) return st;
+            std::lock_guard<std::mutex> lk(g_ring_mu);
+            // only right after the call that released the ring: a call in between
+            // (a step that streams nothing) would otherwise run under the loads
+            prev_known = ring->recorded && ring->call + 1 == call_id;
+            prev_h = ring->h;
+        }
         auto issue_upto = [&](int limit) -> ms_status {
             for (; issued < limit; ++issued) {
                 const int sl = issued % n_slots;
-                ms_status st = prefetch_signal(s, host_layer(k + issued), kv->slots[sl], ps,
-                                               issued >= n_slots ? s->ev_consumed[sl] : nullptr, s->ev_copied[sl],
+                hipEvent_t wait = issued >= n_slots ? s->ev_consumed[sl] : nullptr;
+                const int pp = (int)((call_id - 1) & 1);   // the previous call's event set
+                if (prev_known && issued == 0) wait = prev_h > 0 ? ring->half[pp] : ring->all[pp];
+                else if (prev_known && issued == prev_h && prev_h > 0) wait = ring->all[pp];
+                ms_status st = prefetch_signal(s, host_layer(k + issued), kv->slots[sl], ps, wait, s->ev_copied[ecp + sl],
                                                ycache);
                 if (st != MS_OK) return st;
             }
             return MS_OK;
         };
         if (pipelined) {
-            // the copy stream must not overwrite a slot an earlier call still reads
-            MS_HIP(hipEventRecord(s->ev_start, cs));
-            MS_HIP(hipStreamWaitEvent(ps, s->ev_start, 0));
+            if (!prev_known) {
+                MS_HIP(hipEventRecord(s->ev_start, cs));
+                MS_HIP(hipStreamWaitEvent(ps, s->ev_start, 0));
+            }
             ms_status st = issue_upto(std::min(allowed(), 2));
             if (st != MS_OK) return st;
         }
+        // this call's release points: slots [0, h) after block h - 1, all after the last
+        const int my_h = n_cached <= n_slots ? (n_cached + 1) / 2 : 0;
         bool first_ln_ready = false;   // LayerNorm 1 of block k already in the scratch rows
         if (k > 0) {
             // dense prefix, no cache read: blocks [0, k-1) over every token. Block k-1 needs every
@@ -1162,7 +1238,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 } else if (stream_cache) {
                     ms_status st = issue_upto(allowed());   // includes load j
                     if (st != MS_OK) return st;
-                    MS_HIP(hipStreamWaitEvent(cs, s->ev_copied[j % n_slots], 0));
+                    MS_HIP(hipStreamWaitEvent(cs, s->ev_copied[ecp + j % n_slots], 0));
                 }
             }
             // K/V variant: the cache is the working K/V; Y variant: the unmasked
@@ -1181,6 +1257,16 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 // row its own load or fresh K/V did not write would see NaN
                 const size_t slot_bytes = (size_t)s->B * (ycache ? s->N : s->T) * (ycache ? 1 : 2) * s->d * s->elt;
                 MS_HIP(ms::launch_fill_u8(src, 0xFF, slot_bytes, cs));
+            }
+            if (stream_cache && (j + 1 == my_h || j + 1 == n_cached)) {
+                std::lock_guard<std::mutex> lk(g_ring_mu);
+                if (j + 1 == my_h) MS_HIP(hipEventRecord(ring->half[call_id & 1], cs));
+                if (j + 1 == n_cached) {
+                    MS_HIP(hipEventRecord(ring->all[call_id & 1], cs));
+                    ring->h = my_h;
+                    ring->recorded = true;
+                    ring->call = call_id;
+                }
             }
             if (pipelined) {
                 if (j + n_slots < n_cached) MS_HIP(hipEventRecord(s->ev_consumed[j % n_slots], cs));
