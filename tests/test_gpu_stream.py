@@ -89,12 +89,15 @@ def test_profiler_intervals_match_the_totals():
         assert sum(b - a for cc, a, b in iv if cc == c) == pytest.approx(ms, rel=1e-3, abs=1e-3)
 
 
-@pytest.mark.parametrize("n_slots", [2, 5])
-def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots):
+@pytest.mark.parametrize("n_slots,prefix", [(2, 0), (5, 0), (5, 2), (2, 3)])
+def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots, prefix):
     """Steps of two step contexts (different masks, different host caches) issued
     back to back through the same slots, with no synchronisation between the
     calls: a call's loads must not overwrite a slot the previous call's blocks
-    still read. Every output equals the same step run alone."""
+    still read (the next call's first loads may start under them). With a dense
+    prefix on one context the two stream different numbers of blocks; a third
+    context (every token masked) streams nothing, and the same context may run
+    twice in a row. Every output equals the same step run alone."""
     shape = W.ModelShape("b2b", 5, 256, 2, 4, 16, 16, n_text=0, dtype="bf16", batch=2)
     ws = W.stack_weights(shape, 93, random_ln=True, std=0.03)
     dw = G.dev_weights(ws, shape)
@@ -103,9 +106,12 @@ def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots):
     d_yc = G.to_dev(W.synthetic_y_cache(shape, 93), shape)
     masks = [np.stack([W.blob_mask(16, 16, r, W.rng(93, 3, 10 * c + b)) for b, r in enumerate(rs)])
              for c, rs in enumerate(((0.2, 0.4), (0.35, 0.1)))]
+    masks.append(np.ones_like(masks[0]))   # a third context that streams nothing (every token masked)
     steps = [G.new_step(shape, m) for m in masks]
+    if prefix:
+        steps[1].set_dense_prefix(prefix)   # the two contexts stream different numbers of blocks
     hosts = []
-    for c in range(2):
+    for c in range(3):
         layers = []
         for l in range(shape.n_layers):
             img = W.synthetic_kv_cache(shape, 200 + c, l)[:, shape.n_text:]
@@ -118,14 +124,14 @@ def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots):
                         device=G.DEV) for _ in range(n_slots)]
     copy = torch.cuda.Stream()
     alone = []
-    for c in range(2):
+    for c in range(3):
         y = torch.empty_like(d_yc)
         steps[c].stack_forward(wc, xs[c], d_yc, hosts[c], y, pinned=True, slots=slots, copy_stream=copy)
         torch.cuda.synchronize()
         alone.append(y)
     outs = []
-    for i in range(6):
-        c = i % 2
+    order = [0, 1] * 3 if n_slots == 5 else [0, 1, 2, 0, 2, 1, 1, 0]
+    for c in order:
         y = torch.empty_like(d_yc)
         steps[c].stack_forward(wc, xs[c], d_yc, hosts[c], y, pinned=True, slots=slots, copy_stream=copy)
         outs.append((c, y))
