@@ -384,7 +384,7 @@ def fit_cost_models(key, shape, n_points, torch, MS, W):
         a, b, r2 = MS.mask_fit_linear(xs, ys)
         if b < 0 or a < 0:
             # a cost model has no negative part: a negative slope (latency flat in the amount,
-            # e.g. span-merged copies that move nearly every row) keeps the mean, a negative
+            # e.g. copies that move nearly every row whatever the mask) keeps the mean, a negative
             # intercept the line through the origin
             if b < 0:
                 a, b, r2 = float(np.mean(ys)), 0.0, 0.0

@@ -1,4 +1,4 @@
-"""The copy figures of a step context (span-merged host-to-device copies of one
+"""The copy figures of a step context (the planned host-to-device copies of one
 cached block) and the profiler's interval timeline, through the C ABI."""
 import numpy as np
 import pytest
