@@ -510,10 +510,14 @@ def measure_ceilings(torch):
     x.fill_(1)
     t_cp = best_ms(lambda: y.copy_(x))
     del x, y
+    from paper_2505_20600_amd import maskstep as MS
     return {"gemm_bf16_8192_tflops": round(2.0 * n ** 3 / (t_mm / 1e3) / 1e12, 1),
             "d2d_copy_gbs": round(2.0 * nb / (t_cp / 1e3) / 1e9, 1),
             "h2d_pinned_gbs": round(h2d_ceiling(torch, torch.cuda.current_stream()), 2),
-            "note": "best of 5 (GEMM, copy) or 3 (H2D) timed runs; copy counts bytes read + written"}
+            **MS.probe_ceilings(),
+            "note": "best of 5 (GEMM, copy) or 3 (H2D) timed runs; copy counts bytes read + written; "
+                    "mfma_* / lds_* / operand_stream_*: the library's diagnostic probes (second of two "
+                    "launches), clock from the shader clock counter against the 100 MHz constant clock"}
 
 
 def h2d_ceiling(torch, stream, nbytes=256 << 20):

@@ -384,6 +384,24 @@ ms_status mask_profiler_stop(double* total_ms, int64_t* launches, int64_t* dropp
 ms_status mask_profiler_intervals(int32_t* cls, double* start_ms, double* end_ms, int32_t capacity,
                                   int32_t* count);
 
+/* Diagnostic probes of the rates that bound this library's kernels on the
+ * current GPU, for measurement tools (bench.py --ceilings), not for a
+ * denoising step: each allocates its own small buffers, launches, times with
+ * HIP events and synchronises the device. Synthetic work, no inputs.
+ * mask_probe_mfma: matrix-core issue rate with eight independent accumulator
+ *   chains per wave; kind 0 = v_mfma_f32_16x16x32_bf16, 1 = 32x32x16;
+ *   waves_per_simd 1..4 resident at once on every CU. *tflops_out: dense bf16
+ *   TFLOP/s; *clock_ghz_out (may be NULL): the shader clock during the run
+ *   (clock counter against the 100 MHz constant clock).
+ * mask_probe_lds: aggregate TB/s of conflict-free 16-byte LDS reads.
+ * mask_probe_operand_stream: 256 workgroups of 8 waves each move 64 KB per
+ *   step from a window shared by 16 of them (like GEMM operand panels),
+ *   to_lds != 0: by direct-to-LDS buffer loads into a two-stage LDS ring,
+ *   else into registers; *us_per_step_out and the aggregate *tbs_out. */
+ms_status mask_probe_mfma(int32_t kind, int32_t waves_per_simd, double* tflops_out, double* clock_ghz_out);
+ms_status mask_probe_lds(double* tbs_out);
+ms_status mask_probe_operand_stream(int32_t to_lds, double* us_per_step_out, double* tbs_out);
+
 /* Message of the calling thread's last error ("" if none). */
 const char* mask_last_error(void);
 

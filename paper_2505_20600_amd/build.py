@@ -18,7 +18,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmaskstep.so")
 
 SOURCES = ["compact.hip", "rows.hip", "gemm.hip", "attention.hip", "maskstep.hip", "noalloc.hip",
-           "copyplan.hip"]
+           "copyplan.hip", "probes.hip"]
 HEADERS = ["common.h", "kernels.h", "step_internal.h"]
 
 ARCH = "gfx950"

@@ -101,6 +101,9 @@ def load() -> C.CDLL:
             "mask_profiler_intervals": (i32, [C.POINTER(C.c_int32), C.POINTER(C.c_double), C.POINTER(C.c_double),
                                               i32, C.POINTER(C.c_int32)]),
             "mask_plan_copies": (i32, [vp, i32, i32, C.c_double, C.POINTER(i32), i32, C.POINTER(i32)]),
+            "mask_probe_mfma": (i32, [i32, i32, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
+            "mask_probe_lds": (i32, [C.POINTER(C.c_double)]),
+            "mask_probe_operand_stream": (i32, [i32, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
             "mask_fit_linear": (i32, [C.POINTER(C.c_double), C.POINTER(C.c_double), i32, C.POINTER(C.c_double),
                                       C.POINTER(C.c_double), C.POINTER(C.c_double)]),
             "mask_batch_cost": (i32, [C.POINTER(ModelDesc), C.POINTER(CostModel), C.POINTER(i32), i32,
@@ -125,7 +128,8 @@ EXPORTED = ("mask_abi_version", "mask_last_error", "mask_workspace_bytes", "mask
             "mask_stack_forward", "mask_step_destroy",
             "mask_step_set_dense_prefix", "mask_plan_dense_prefix",
             "mask_profiler_start", "mask_profiler_stop", "mask_profiler_intervals", "ms_linear",
-            "mask_fit_linear", "mask_batch_cost", "mask_route_request", "mask_plan_copies")
+            "mask_fit_linear", "mask_batch_cost", "mask_route_request", "mask_plan_copies",
+            "mask_probe_mfma", "mask_probe_lds", "mask_probe_operand_stream")
 
 MS_EPI_BIAS, MS_EPI_BIAS_RESID, MS_EPI_BIAS_GELU = 0, 1, 2
 
@@ -229,6 +233,27 @@ def mask_plan_copies(mask, grid_h: int, grid_w: int, copy_cost_rows: float):
     out = (C.c_int32 * max(1, 3 * n.value))()
     _check(load().mask_plan_copies(m.ctypes.data, grid_h, grid_w, copy_cost_rows, out, n.value, C.byref(n)))
     return [(out[3 * i], out[3 * i + 1], out[3 * i + 2]) for i in range(n.value)]
+
+
+def probe_ceilings():
+    """The diagnostic probes (matrix-core issue rate and clock, LDS reads, operand stream) on cuda:0."""
+    lib = load()
+    out = {}
+    for kind, name in ((0, "16x16x32"), (1, "32x32x16")):
+        for wps in (1, 2):
+            tf, ghz = C.c_double(), C.c_double()
+            _check(lib.mask_probe_mfma(kind, wps, C.byref(tf), C.byref(ghz)))
+            out[f"mfma_{name}_bf16_{wps}wave_tflops"] = round(tf.value, 1)
+            out[f"mfma_{name}_bf16_{wps}wave_clock_ghz"] = round(ghz.value, 3)
+    tb = C.c_double()
+    _check(lib.mask_probe_lds(C.byref(tb)))
+    out["lds_read_tbs"] = round(tb.value, 1)
+    for to_lds, name in ((1, "to_lds"), (0, "to_vgprs")):
+        us, tbs = C.c_double(), C.c_double()
+        _check(lib.mask_probe_operand_stream(to_lds, C.byref(us), C.byref(tbs)))
+        out[f"operand_stream_{name}_us_per_64kb_step"] = round(us.value, 3)
+        out[f"operand_stream_{name}_tbs"] = round(tbs.value, 2)
+    return out
 
 
 def mask_fit_linear(x, y):

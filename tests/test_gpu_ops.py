@@ -160,3 +160,17 @@ def test_linear_more_tiles_than_resident_workgroups(tile, M, N, epi):
     e = _err(out, _ref(A, W, b, R, epi))
     print(f"[parity] persistent tile {tile} {M}x{N} epi {epi}: max-norm rel err {e:.2e}")
     assert e <= 2e-2
+
+
+def test_diagnostic_probes_report_plausible_rates():
+    """The probes behind bench.py --ceilings: matrix-core rate below the 2.5 PFLOP/s
+    nominal dense peak and a clock near the 2.4 GHz nominal, LDS and operand-stream
+    rates positive, the direct-to-LDS stream at least as fast as through VGPRs."""
+    r = MS.probe_ceilings()
+    print("[probe]", r)
+    for k, v in r.items():
+        assert v > 0, k
+    for k in ("mfma_16x16x32_bf16_2wave_tflops", "mfma_32x32x16_bf16_2wave_tflops"):
+        assert 500 < r[k] < 2600, k
+    assert 1.0 < r["mfma_16x16x32_bf16_2wave_clock_ghz"] < 3.0
+    assert r["operand_stream_to_lds_tbs"] >= 0.9 * r["operand_stream_to_vgprs_tbs"]
