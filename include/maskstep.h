@@ -110,8 +110,9 @@ typedef enum {
  *                     read their slots (its first half of cached blocks, then
  *                     all of them), so in a run of steps the next step's
  *                     loads start under the current step's last blocks;
- *                     otherwise a call's loads wait for the call's start on
- *                     the compute stream. A caller that writes or frees slot
+ *                     otherwise (and under stream capture) a call's loads
+ *                     wait for the call's start on the compute stream. A
+ *                     caller that writes or frees slot
  *                     buffers orders that after the calls that use them.
  *                     With n_slots >= the number of cached layers every load
  *                     starts at once (MI355X's HBM holds a whole stack's K/V

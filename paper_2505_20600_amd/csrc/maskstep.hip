@@ -1154,14 +1154,21 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         RingRelease* ring = nullptr;
         int prev_h = 0;
         bool prev_known = false;
+        // Under stream capture the release points of eager calls mean nothing to the replays
+        // (and the replays' records are not seen here): a captured call orders its loads after
+        // its own start, and the next call does the same.
+        hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+        MS_HIP(hipStreamIsCapturing(cs, &capture));
+        const bool capturing = capture != hipStreamCaptureStatusNone;
         if (stream_cache) {
             ms_status st = ring_release(kv, &ring);
             if (st != MS_OK) return st;
             std::lock_guard<std::mutex> lk(g_ring_mu);
             // only right after the call that released the ring: a call in between
             // (a step that streams nothing) would otherwise run under the loads
-            prev_known = ring->recorded && ring->call + 1 == call_id;
+            prev_known = !capturing && ring->recorded && ring->call + 1 == call_id;
             prev_h = ring->h;
+            if (capturing) ring->recorded = false;
         }
         auto issue_upto = [&](int limit) -> ms_status {
             for (; issued < limit; ++issued) {
@@ -1258,7 +1265,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
                 const size_t slot_bytes = (size_t)s->B * (ycache ? s->N : s->T) * (ycache ? 1 : 2) * s->d * s->elt;
                 MS_HIP(ms::launch_fill_u8(src, 0xFF, slot_bytes, cs));
             }
-            if (stream_cache && (j + 1 == my_h || j + 1 == n_cached)) {
+            if (stream_cache && !capturing && (j + 1 == my_h || j + 1 == n_cached)) {
                 std::lock_guard<std::mutex> lk(g_ring_mu);
                 if (j + 1 == my_h) MS_HIP(hipEventRecord(ring->half[call_id & 1], cs));
                 if (j + 1 == n_cached) {

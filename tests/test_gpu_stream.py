@@ -139,3 +139,73 @@ def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots, prefix)
     assert not torch.equal(alone[0], alone[1])
     for c, y in outs:
         assert torch.equal(y, alone[c]), f"context {c}"
+
+
+@pytest.mark.parametrize("pinned", [False, True], ids=["resident", "streamed"])
+def test_step_replays_as_a_graph(pinned):
+    """One step captured as a HIP graph (torch.cuda.graph) and replayed three times,
+    with eager steps of another context through the same slots in between: every
+    replay equals the eager step bit for bit. A captured call orders its loads after
+    its own start (no release points of eager calls inside a graph)."""
+    shape = W.ModelShape("graph", 3, 256, 2, 4, 16, 16, n_text=0, dtype="bf16", batch=2)
+    ws = W.stack_weights(shape, 95, random_ln=True, std=0.03)
+    wc = MS.weights_array(G.dev_weights(ws, shape))
+    xt = W.template_hidden(shape, 95)
+    d_yc = G.to_dev(W.synthetic_y_cache(shape, 95), shape)
+    masks = [np.stack([W.blob_mask(16, 16, r, W.rng(95, 3, 10 * c + b)) for b, r in enumerate(rs)])
+             for c, rs in enumerate(((0.3, 0.15), (0.2, 0.45)))]
+    steps = [G.new_step(shape, m) for m in masks]
+    xs = [G.to_dev(W.edited_hidden(shape, 95, xt, m), shape) for m in masks]
+    kvs = []
+    for c in range(2):
+        layers = []
+        for l in range(shape.n_layers):
+            full = W.synthetic_kv_cache(shape, 300 + c, l)
+            if pinned:
+                t = torch.empty(full[:, shape.n_text:].shape, dtype=torch.bfloat16, pin_memory=True)
+                t.copy_(torch.as_tensor(np.ascontiguousarray(full[:, shape.n_text:], np.float32)).to(torch.bfloat16))
+            else:
+                t = G.to_dev(full, shape)
+            layers.append(t)
+        kvs.append(layers)
+    slots = [torch.empty((shape.batch, shape.n_tokens, 2, shape.d_model), dtype=torch.bfloat16, device=G.DEV)
+             for _ in range(2)] if pinned else []
+    copy = torch.cuda.Stream() if pinned else None
+
+    def run(c, y, stream=None):
+        if not pinned:   # the resident cache is also the working K/V: start each step from the cache
+            kv = [t.clone() for t in kvs[c]]
+        else:
+            kv = kvs[c]
+        steps[c].stack_forward(wc, xs[c], d_yc, kv, y, pinned=pinned, slots=slots, stream=stream,
+                               copy_stream=copy)
+        return kv
+
+    y_ref = torch.empty_like(d_yc)
+    run(0, y_ref)
+    torch.cuda.synchronize()
+    y_other = torch.empty_like(d_yc)
+    run(1, y_other)
+    torch.cuda.synchronize()
+    # capture step 0 (resident: on a private copy of the cache that each replay restarts from)
+    y_g = torch.empty_like(d_yc)
+    kv_g = [t.clone() for t in kvs[0]] if not pinned else None
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    with torch.cuda.stream(cap):
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            steps[0].stack_forward(wc, xs[0], d_yc, kv_g if not pinned else kvs[0], y_g, pinned=pinned, slots=slots,
+                                   copy_stream=copy)
+    torch.cuda.synchronize()
+    for i in range(3):
+        if not pinned:
+            for dst, src in zip(kv_g, kvs[0]):
+                dst.copy_(src)
+        y_g.fill_(float("nan"))
+        graph.replay()
+        y_o = torch.empty_like(d_yc)
+        run(1, y_o)   # eager work of another context through the same slots
+        torch.cuda.synchronize()
+        assert torch.equal(y_g, y_ref), f"replay {i}"
+        assert torch.equal(y_o, y_other), f"eager step after replay {i}"
