@@ -678,7 +678,7 @@ def main():
 
     def one_step(i):
         ctx[i].stack_forward(wc, xs[i], ycache, kv_layers, y, pinned=pinned, slots=slots, stream=stream,
-                             copy_stream=copy_stream, inputs=yc_mode)
+                             copy_stream=copy_stream, inputs=yc_mode, loads_ahead=True)
         return Ms[i]
 
     def timed_once(fn):

@@ -103,16 +103,17 @@ typedef enum {
  *                     buffers; the j-th cached layer of the step uses
  *                     slots[j % n_slots], and its load (on the copy stream)
  *                     waits until the compute stream has finished with the
- *                     layer that used the slot before. Across calls: right
- *                     after a mask_stack_forward call that streamed through
- *                     the same list of slots (any step context), a call's
- *                     first loads wait only for the blocks of that call that
- *                     read their slots (its first half of cached blocks, then
- *                     all of them), so in a run of steps the next step's
- *                     loads start under the current step's last blocks;
- *                     otherwise (and under stream capture) a call's loads
- *                     wait for the call's start on the compute stream. A
- *                     caller that writes or frees slot
+ *                     layer that used the slot before. Across calls: with
+ *                     flags & MS_KV_LOADS_AHEAD, right after a
+ *                     mask_stack_forward call that streamed through the same
+ *                     list of slots (any step context), a call's first loads
+ *                     wait only for the blocks of that call that read their
+ *                     slots (its first half of cached blocks, then all of
+ *                     them), so in a run of steps the next step's loads start
+ *                     under the current step's last blocks; otherwise (and
+ *                     under stream capture) a call's loads wait for the
+ *                     call's start on the compute stream. A caller that
+ *                     writes or frees slot
  *                     buffers orders that after the calls that use them.
  *                     With n_slots >= the number of cached layers every load
  *                     starts at once (MI355X's HBM holds a whole stack's K/V
@@ -138,7 +139,16 @@ typedef struct {
     int32_t n_slots;            /* host-pinned kinds only, >= 1 */
     void* const* slots;         /* [n_slots], host-pinned kinds only */
     const void* const* request_layer;   /* host-pinned kinds only: [n_layers * B] or NULL */
+    int32_t flags;              /* MS_KV_* flags below, 0 for none */
 } ms_kv_source;
+
+/* flags: the caller guarantees that between this call and the previous
+ * mask_stack_forward call through the same list of slots nothing else reads
+ * or writes those slots (no graph replay, per-block call or kernel of its own
+ * on them). The call's first loads may then start under the previous call's
+ * last blocks (see MS_KV_HOST_PINNED); without it a call's loads wait for the
+ * call's start on the compute stream. */
+#define MS_KV_LOADS_AHEAD 1
 
 typedef struct ms_step ms_step;   /* opaque host object, one per mask set */
 
@@ -406,10 +416,11 @@ ms_status mask_probe_operand_stream(int32_t to_lds, double* us_per_step_out, dou
 /* Message of the calling thread's last error ("" if none). */
 const char* mask_last_error(void);
 
-/* Version of this interface: 6 (2 added Y caching's kinds and calls, 3 the
+/* Version of this interface: 7 (2 added Y caching's kinds and calls, 3 the
  * cost-model and routing calls, 4 the copy figures of ms_step_info and
  * mask_profiler_intervals, 5 mask_step_init_static, 6 mask_plan_copies,
- * strided 2-D cache loads and the Y-load figures of ms_step_info). */
+ * strided 2-D cache loads and the Y-load figures of ms_step_info, 7
+ * ms_kv_source.flags and the probes). */
 int32_t mask_abi_version(void);
 
 #ifdef __cplusplus

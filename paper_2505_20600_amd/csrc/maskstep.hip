@@ -22,7 +22,7 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 6;
+constexpr int32_t kAbiVersion = 7;
 constexpr int kMaxBatch = 64;
 // A block's cache load is a set of host-to-device copies that covers the
 // unmasked rows (copyplan.hip). Measured on MI355X from pinned host memory: a
@@ -1166,7 +1166,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             std::lock_guard<std::mutex> lk(g_ring_mu);
             // only right after the call that released the ring: a call in between
             // (a step that streams nothing) would otherwise run under the loads
-            prev_known = !capturing && ring->recorded && ring->call + 1 == call_id;
+            prev_known = (kv->flags & MS_KV_LOADS_AHEAD) && !capturing && ring->recorded && ring->call + 1 == call_id;
             prev_h = ring->h;
             if (capturing) ring->recorded = false;
         }

@@ -42,7 +42,10 @@ class LayerWeights(C.Structure):
 
 class KVSource(C.Structure):
     _fields_ = [("kind", C.c_int32), ("layer", C.POINTER(C.c_void_p)), ("n_slots", C.c_int32),
-                ("slots", C.POINTER(C.c_void_p)), ("request_layer", C.POINTER(C.c_void_p))]
+                ("slots", C.POINTER(C.c_void_p)), ("request_layer", C.POINTER(C.c_void_p)), ("flags", C.c_int32)]
+
+
+MS_KV_LOADS_AHEAD = 1
 
 
 class CostModel(C.Structure):
@@ -410,12 +413,14 @@ class MaskStep:
         _check(self._lib.mask_step_set_dense_prefix(self.handle, k, _stream(stream)))
 
     def stack_forward(self, weights_c, x, ycache, kv_layers, y, *, pinned: bool = False, slots=(),
-                      stream=None, copy_stream=None, inputs: bool = False, per_request=None):
+                      stream=None, copy_stream=None, inputs: bool = False, per_request=None,
+                      loads_ahead: bool = False):
         """``weights_c`` from weights_array(); ``kv_layers``: [L] tensors (device or pinned host),
         per-layer K/V [B][T|N][2][d], or with ``inputs`` the cached block inputs [B][N][d]
         (Y caching); ``slots``: device buffers the pinned layers stream through. With
         ``pinned``, ``per_request`` may replace ``kv_layers``: [L][B] pinned per-request
-        buffers (or None for requests that recompute nothing)."""
+        buffers (or None for requests that recompute nothing). ``loads_ahead``: MS_KV_LOADS_AHEAD
+        (nothing else touches the slots between consecutive calls through them)."""
         if per_request is not None:
             L = len(per_request)
             ptrs = (C.c_void_p * 1)()
@@ -431,7 +436,8 @@ class MaskStep:
         sl = (C.c_void_p * max(1, len(slots)))(*[_ptr(t) for t in slots])
         kind = (MS_Y_HOST_PINNED if pinned else MS_Y_DEVICE) if inputs else \
                (MS_KV_HOST_PINNED if pinned else MS_KV_DEVICE)
-        src = KVSource(kind, layer_p, len(slots) if pinned else 0, C.cast(sl, C.POINTER(C.c_void_p)), req_p)
+        src = KVSource(kind, layer_p, len(slots) if pinned else 0, C.cast(sl, C.POINTER(C.c_void_p)), req_p,
+                       MS_KV_LOADS_AHEAD if loads_ahead else 0)
         cs = _stream(stream)
         ps = _stream(copy_stream) if copy_stream is not None else cs
         _check(self._lib.mask_stack_forward(self.handle, weights_c, _ptr(x), _ptr(ycache), C.byref(src),

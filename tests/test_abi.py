@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_abi_version():
-    assert MS.load().mask_abi_version() == 6
+    assert MS.load().mask_abi_version() == 7
 
 
 def test_kv_block_of_4_gib_is_rejected():

@@ -89,12 +89,13 @@ def test_profiler_intervals_match_the_totals():
         assert sum(b - a for cc, a, b in iv if cc == c) == pytest.approx(ms, rel=1e-3, abs=1e-3)
 
 
-@pytest.mark.parametrize("n_slots,prefix", [(2, 0), (5, 0), (5, 2), (2, 3)])
-def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots, prefix):
+@pytest.mark.parametrize("n_slots,prefix,form", [(2, 0, "kv"), (5, 0, "kv"), (5, 2, "kv"), (2, 3, "kv"),
+                                                 (5, 0, "y"), (2, 2, "y")])
+def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots, prefix, form):
     """Steps of two step contexts (different masks, different host caches) issued
     back to back through the same slots, with no synchronisation between the
     calls: a call's loads must not overwrite a slot the previous call's blocks
-    still read (the next call's first loads may start under them). With a dense
+    still read (with MS_KV_LOADS_AHEAD the next call's first loads start under them). With a dense
     prefix on one context the two stream different numbers of blocks; a third
     context (every token masked) streams nothing, and the same context may run
     twice in a row. Every output equals the same step run alone."""
@@ -114,26 +115,34 @@ def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots, prefix)
     for c in range(3):
         layers = []
         for l in range(shape.n_layers):
-            img = W.synthetic_kv_cache(shape, 200 + c, l)[:, shape.n_text:]
+            # K/V form: [B][N][2][d] rows; Y form: the block inputs [B][N][d]
+            img = (W.synthetic_kv_cache(shape, 200 + c, l) if form == "kv"
+                   else W.synthetic_y_cache(shape, 200 + 10 * c + l))[:, shape.n_text:]
             t = torch.empty(img.shape, dtype=torch.bfloat16, pin_memory=True)
             t.copy_(torch.as_tensor(np.ascontiguousarray(img, np.float32)).to(torch.bfloat16))
             layers.append(t)
         hosts.append(layers)
     xs = [G.to_dev(W.edited_hidden(shape, 93, xt, m), shape) for m in masks]
-    slots = [torch.full((shape.batch, shape.n_tokens, 2, shape.d_model), float("nan"), dtype=torch.bfloat16,
-                        device=G.DEV) for _ in range(n_slots)]
+    slot_shape = ((shape.batch, shape.n_tokens, 2, shape.d_model) if form == "kv"
+                  else (shape.batch, shape.n_image, shape.d_model))
+    slots = [torch.full(slot_shape, float("nan"), dtype=torch.bfloat16, device=G.DEV) for _ in range(n_slots)]
     copy = torch.cuda.Stream()
+
+    def call(c, y):
+        steps[c].stack_forward(wc, xs[c], d_yc, hosts[c], y, pinned=True, slots=slots, copy_stream=copy,
+                               inputs=form == "y", loads_ahead=True)
+
     alone = []
     for c in range(3):
         y = torch.empty_like(d_yc)
-        steps[c].stack_forward(wc, xs[c], d_yc, hosts[c], y, pinned=True, slots=slots, copy_stream=copy)
+        call(c, y)
         torch.cuda.synchronize()
         alone.append(y)
     outs = []
     order = [0, 1] * 3 if n_slots == 5 else [0, 1, 2, 0, 2, 1, 1, 0]
     for c in order:
         y = torch.empty_like(d_yc)
-        steps[c].stack_forward(wc, xs[c], d_yc, hosts[c], y, pinned=True, slots=slots, copy_stream=copy)
+        call(c, y)
         outs.append((c, y))
     torch.cuda.synchronize()
     assert not torch.equal(alone[0], alone[1])
@@ -146,7 +155,8 @@ def test_step_replays_as_a_graph(pinned):
     """One step captured as a HIP graph (torch.cuda.graph) and replayed three times,
     with eager steps of another context through the same slots in between: every
     replay equals the eager step bit for bit. A captured call orders its loads after
-    its own start (no release points of eager calls inside a graph)."""
+    its own start, and so do the eager calls, which run without MS_KV_LOADS_AHEAD (a
+    replay touches the slots between them)."""
     shape = W.ModelShape("graph", 3, 256, 2, 4, 16, 16, n_text=0, dtype="bf16", batch=2)
     ws = W.stack_weights(shape, 95, random_ln=True, std=0.03)
     wc = MS.weights_array(G.dev_weights(ws, shape))
