@@ -10,7 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
-#include <map>
+#include <list>
 #include <new>
 #include <string>
 #include <vector>
@@ -239,18 +239,57 @@ struct RingRelease {
     int h = 0;
     bool recorded = false;
     uint64_t call = 0;   // the mask_stack_forward call that recorded them
+    uint64_t gen = 0;    // bumped when the entry passes to another slot list
+};
+// Only the ring of the call right before can release a call's loads early, so
+// the registry keeps a few rings per device: a caller that streams through new
+// slot buffers every step takes over the least recently used entry (its
+// events, never destroyed, are recorded again from then on) instead of
+// growing the registry.
+constexpr int kRingsPerDevice = 16;
+struct RingEntry {
+    int dev = 0;
+    std::vector<const void*> slots;
+    uint64_t last_use = 0;
+    RingRelease r;
 };
 std::mutex g_ring_mu;
 std::atomic<uint64_t> g_stack_calls{0};
-std::map<std::pair<int, std::vector<const void*>>, RingRelease> g_ring;
+std::list<RingEntry> g_rings;   // stable addresses
+uint64_t g_ring_clock = 0;
 
-ms_status ring_release(const ms_kv_source* kv, RingRelease** out) {
+ms_status ring_release(const ms_kv_source* kv, RingRelease** out, uint64_t* gen) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return fail(MS_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
     std::vector<const void*> key(kv->slots, kv->slots + kv->n_slots);
     std::lock_guard<std::mutex> lk(g_ring_mu);
-    RingRelease& r = g_ring[std::make_pair(dev, std::move(key))];
+    RingEntry* hit = nullptr;
+    RingEntry* lru = nullptr;
+    int on_dev = 0;
+    for (RingEntry& en : g_rings) {
+        if (en.dev != dev) continue;
+        if (en.slots == key) {
+            hit = &en;
+            break;
+        }
+        ++on_dev;
+        if (!lru || en.last_use < lru->last_use) lru = &en;
+    }
+    if (!hit && on_dev >= kRingsPerDevice) {
+        hit = lru;
+        hit->slots = std::move(key);
+        hit->r.recorded = false;
+        ++hit->r.gen;
+    } else if (!hit) {
+        g_rings.emplace_back();
+        hit = &g_rings.back();
+        hit->dev = dev;
+        hit->slots = std::move(key);
+    }
+    hit->last_use = ++g_ring_clock;
+    RingRelease& r = hit->r;
+    *gen = r.gen;
     for (int i = 0; i < 2; ++i) {
         if (!r.half[i]) {
             e = hipEventCreateWithFlags(&r.half[i], hipEventDisableTiming);
@@ -270,7 +309,7 @@ ms_status ring_release(const ms_kv_source* kv, RingRelease** out) {
 // mask_stack_forward then waits for its own start again.
 void forget_rings() {
     std::lock_guard<std::mutex> lk(g_ring_mu);
-    for (auto& kv : g_ring) kv.second.recorded = false;
+    for (RingEntry& en : g_rings) en.r.recorded = false;
 }
 
 ms_status ensure_events(ms_step* s, int n) {
@@ -1152,6 +1191,7 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         // the copy stream must not overwrite a slot an earlier call still reads: wait for the
         // ring's release by the last call that streamed through it, else for this call's start
         RingRelease* ring = nullptr;
+        uint64_t ring_gen = 0;
         int prev_h = 0;
         bool prev_known = false;
         // Under stream capture the release points of eager calls mean nothing to the replays
@@ -1161,12 +1201,13 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
         MS_HIP(hipStreamIsCapturing(cs, &capture));
         const bool capturing = capture != hipStreamCaptureStatusNone;
         if (stream_cache) {
-            ms_status st = ring_release(kv, &ring);
+            ms_status st = ring_release(kv, &ring, &ring_gen);
             if (st != MS_OK) return st;
             std::lock_guard<std::mutex> lk(g_ring_mu);
             // only right after the call that released the ring: a call in between
             // (a step that streams nothing) would otherwise run under the loads
-            prev_known = (kv->flags & MS_KV_LOADS_AHEAD) && !capturing && ring->recorded && ring->call + 1 == call_id;
+            prev_known = (kv->flags & MS_KV_LOADS_AHEAD) && !capturing && ring->gen == ring_gen && ring->recorded &&
+                         ring->call + 1 == call_id;
             prev_h = ring->h;
             if (capturing) ring->recorded = false;
         }
@@ -1267,12 +1308,15 @@ ms_status mask_stack_forward(ms_step* s, const ms_layer_weights* w, const void* 
             }
             if (stream_cache && !capturing && (j + 1 == my_h || j + 1 == n_cached)) {
                 std::lock_guard<std::mutex> lk(g_ring_mu);
-                if (j + 1 == my_h) MS_HIP(hipEventRecord(ring->half[call_id & 1], cs));
-                if (j + 1 == n_cached) {
-                    MS_HIP(hipEventRecord(ring->all[call_id & 1], cs));
-                    ring->h = my_h;
-                    ring->recorded = true;
-                    ring->call = call_id;
+                // unless another slot list has taken the entry over meanwhile
+                if (ring->gen == ring_gen) {
+                    if (j + 1 == my_h) MS_HIP(hipEventRecord(ring->half[call_id & 1], cs));
+                    if (j + 1 == n_cached) {
+                        MS_HIP(hipEventRecord(ring->all[call_id & 1], cs));
+                        ring->h = my_h;
+                        ring->recorded = true;
+                        ring->call = call_id;
+                    }
                 }
             }
             if (pipelined) {

@@ -150,6 +150,41 @@ def test_back_to_back_steps_of_two_contexts_share_slots_exactly(n_slots, prefix,
         assert torch.equal(y, alone[c]), f"context {c}"
 
 
+def test_many_slot_lists_back_to_back():
+    """Steps of one context through 18 different lists of slot buffers in turn,
+    then the first list again, back to back with MS_KV_LOADS_AHEAD and no
+    synchronisation: more lists than the library keeps release rings for (16
+    per device), so entries pass from list to list and the first list's entry
+    is gone when it returns. Every output equals the step run alone."""
+    shape = W.ModelShape("rings", 4, 256, 2, 4, 16, 16, n_text=0, dtype="bf16", batch=2)
+    ws = W.stack_weights(shape, 94, random_ln=True, std=0.03)
+    wc = MS.weights_array(G.dev_weights(ws, shape))
+    xt = W.template_hidden(shape, 94)
+    d_yc = G.to_dev(W.synthetic_y_cache(shape, 94), shape)
+    mask = np.stack([W.blob_mask(16, 16, r, W.rng(94, 3, b)) for b, r in enumerate((0.25, 0.45))])
+    step = G.new_step(shape, mask)
+    host = [G._pinned(W.synthetic_kv_cache(shape, 94, l)[:, shape.n_text:], shape) for l in range(shape.n_layers)]
+    x = G.to_dev(W.edited_hidden(shape, 94, xt, mask), shape)
+    lists = [[torch.full((shape.batch, shape.n_tokens, 2, shape.d_model), float("nan"), dtype=torch.bfloat16,
+                         device=G.DEV) for _ in range(2)] for _ in range(18)]
+    copy = torch.cuda.Stream()
+
+    def call(slots, y):
+        step.stack_forward(wc, x, d_yc, host, y, pinned=True, slots=slots, copy_stream=copy, loads_ahead=True)
+
+    alone = torch.empty_like(d_yc)
+    call(lists[0], alone)
+    torch.cuda.synchronize()
+    outs = []
+    for i in list(range(18)) + [0, 0, 5]:
+        y = torch.empty_like(d_yc)
+        call(lists[i], y)
+        outs.append((i, y))
+    torch.cuda.synchronize()
+    for i, y in outs:
+        assert torch.equal(y, alone), f"slot list {i}"
+
+
 @pytest.mark.parametrize("pinned", [False, True], ids=["resident", "streamed"])
 def test_step_replays_as_a_graph(pinned):
     """One step captured as a HIP graph (torch.cuda.graph) and replayed three times,
