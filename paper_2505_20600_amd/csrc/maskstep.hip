@@ -711,6 +711,11 @@ ms_status set_error(ms_status st, const char* fmt, ...) {
     return st;
 }
 
+ms_status clear_error() {
+    g_err.clear();
+    return MS_OK;
+}
+
 ms_status workspace_need(const ms_model_desc* desc, int32_t batch, size_t* need) {
     ms_status st = validate_desc(desc);
     if (st != MS_OK) return st;

@@ -200,7 +200,7 @@ ms_status mask_probe_mfma(int32_t kind, int32_t waves_per_simd, double* tflops_o
 done:
     if (out) (void)hipFree(out);
     if (clocks) (void)hipFree(clocks);
-    return st;
+    return st == MS_OK ? ms::clear_error() : st;
 }
 
 ms_status mask_probe_lds(double* tbs_out) {
@@ -224,7 +224,7 @@ ms_status mask_probe_lds(double* tbs_out) {
     *tbs_out = (double)blocks * kProbeThreads * iters * 8 * 16 / (ms_ * 1e-3) / 1e12;
 done:
     if (out) (void)hipFree(out);
-    return st;
+    return st == MS_OK ? ms::clear_error() : st;
 }
 
 ms_status mask_probe_operand_stream(int32_t to_lds, double* us_per_step_out, double* tbs_out) {
@@ -255,7 +255,7 @@ ms_status mask_probe_operand_stream(int32_t to_lds, double* us_per_step_out, dou
 done:
     if (src) (void)hipFree(src);
     if (out) (void)hipFree(out);
-    return st;
+    return st == MS_OK ? ms::clear_error() : st;
 }
 
 }  // extern "C"

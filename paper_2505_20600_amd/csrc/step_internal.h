@@ -14,6 +14,8 @@ namespace ms {
 
 // Records the calling thread's error message (mask_last_error) and returns `st`.
 ms_status set_error(ms_status st, const char* fmt, ...);
+// Clears the calling thread's error message; returns MS_OK.
+ms_status clear_error();
 
 // Bytes of workspace a step over `batch` requests of `desc` needs (*need), after
 // the validation mask_workspace_bytes does.

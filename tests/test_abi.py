@@ -115,6 +115,20 @@ def test_step_init_validates_before_any_device_work():
         assert h.value is None
 
 
+def test_probes_validate_before_any_device_work():
+    """The diagnostic probes reject bad arguments with MS_EINVAL and a message,
+    before any HIP call (so this runs without a GPU)."""
+    lib = MS.load()
+    tf, ghz, us, tb = C.c_double(), C.c_double(), C.c_double(), C.c_double()
+    for args in ((2, 1, C.byref(tf), C.byref(ghz)), (0, 0, C.byref(tf), None), (0, 5, C.byref(tf), None),
+                 (1, 1, None, C.byref(ghz))):
+        assert lib.mask_probe_mfma(*args) == MS.MS_EINVAL
+        assert lib.mask_last_error()
+    assert lib.mask_probe_lds(None) == MS.MS_EINVAL
+    assert lib.mask_probe_operand_stream(1, None, C.byref(tb)) == MS.MS_EINVAL
+    assert lib.mask_probe_operand_stream(0, C.byref(us), None) == MS.MS_EINVAL
+
+
 def test_linear_validates_before_any_device_work():
     """The row GEMM's shape checks come before any pointer or device use; the
     bf16 kernels address a tile's rows with 32-bit offsets, so K stops below 2^23."""

@@ -174,3 +174,9 @@ def test_diagnostic_probes_report_plausible_rates():
         assert 500 < r[k] < 2600, k
     assert 1.0 < r["mfma_16x16x32_bf16_2wave_clock_ghz"] < 3.0
     assert r["operand_stream_to_lds_tbs"] >= 0.9 * r["operand_stream_to_vgprs_tbs"]
+    # a failed call's message does not outlive a later successful probe
+    import ctypes as C
+    lib = MS.load()
+    tb = C.c_double()
+    assert lib.mask_probe_lds(None) == MS.MS_EINVAL and lib.mask_last_error()
+    assert lib.mask_probe_lds(C.byref(tb)) == MS.MS_OK and lib.mask_last_error() == b""
